@@ -1,0 +1,230 @@
+/*
+ * fmm8 -- Strassen-type rank-7 bilinear matrix multiplication under a
+ * block-scaled e4m3 model, with an fp64 error measurement, on AMD MI355X
+ * (gfx950).
+ *
+ * The operation (Section 2.1 and Section 2.2 of "Fast Matrix Multiplication
+ * in fp8: Certified Coefficient Optimization and Measured Error"):
+ *
+ *   A (M x K) and B (K x N) are split into a 2^l x 2^l grid of sub-blocks.
+ *   For every term r of the depth-l flattened realization (U, V, w)
+ *     x_r = sum_b U[r,b] A_b   (fp32)          -- encoded combinations,
+ *     y_r = sum_b V[r,b] B_b   (fp32)
+ *   are formed from the unquantized operands, quantized to e4m3 with one
+ *   scale per block of `block` consecutive elements along the contracted
+ *   axis (Assumption 1; Appendix E.2), multiplied with fp32 accumulation,
+ *   and decoded:  C_(I,K) = sum_r w[r, K 2^l + I] P_r.
+ *
+ * Coefficient conventions (Appendix A, eq. A.1): rv(A) = (a11,a12,a21,a22);
+ * U_r is indexed by 2i+j for A-block (i,j), V_r by 2j+k, and the third factor
+ * is cyclic, w_r = rv(W_r^T), indexed by 2k+i.  A depth-l table (Section 3.2,
+ * Kronecker powers; Section 4.3, flattened realizations) has T = R^l terms
+ * r = sum_t r_t R^(l-t) and 4^l columns, sub-block (P,Q) at column P 2^l + Q;
+ * each entry is the product of the l base coefficients, multiplied left to
+ * right in binary64 and rounded once to binary32.
+ *
+ * Memory and ownership.  Every device buffer is allocated and owned by the
+ * caller; matrices are row-major and contiguous, batch-major.  Opaque host
+ * handles (fmm_real, fmm_plan) are owned by the library and released with
+ * their _destroy call.  fmm_encode, fmm_multiply and fmm_matmul never
+ * allocate; fmm_plan_create uploads the plan's coefficient tables to the
+ * device that is current at the time of the call, and the plan may only be
+ * used with that device.
+ *
+ * Execution.  Device calls are asynchronous on `stream` (a hipStream_t
+ * passed as void*; NULL is the null stream) and never synchronize the host.
+ * A plan is immutable: one plan may be used concurrently on several streams
+ * with distinct workspaces.
+ *
+ * Errors.  Every call returns an int status: FMM_OK (0) or a negative code.
+ * No exception crosses the boundary.  Device-side problems (a failed launch)
+ * are reported as FMM_ERR_HIP; fmm_status_string() names any code, and
+ * fmm_last_error_detail() returns the last HIP error string of the calling
+ * thread.  Non-finite inputs are undefined behaviour.
+ */
+#ifndef FMM8_H
+#define FMM8_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+  FMM_OK = 0,
+  FMM_ERR_ARG = -1,          /* null pointer, out-of-range enum, bad tolerance */
+  FMM_ERR_SHAPE = -2,        /* dimensions not divisible as required */
+  FMM_ERR_UNSUPPORTED = -3,  /* a shape/rule/block/depth this build does not run */
+  FMM_ERR_NOT_EXACT = -4,    /* Brent residual above the tolerance */
+  FMM_ERR_SINGULAR = -5,     /* a basis change with |det| < 1e-12 */
+  FMM_ERR_HIP = -6,          /* a HIP runtime call or a kernel launch failed */
+  FMM_ERR_DEVICE = -7,       /* the device is not gfx950 */
+  FMM_ERR_WORKSPACE = -8,    /* workspace too small or misaligned */
+  FMM_ERR_NOMEM = -9         /* host allocation failed */
+};
+
+/* ---- named realizations ------------------------------------------------ */
+enum {
+  FMM_CUBIC8 = 0,            /* the cubic <2,2,2;8> algorithm, Phi = 8 (Section 3.2) */
+  FMM_STRASSEN = 1,          /* Strassen 1969, M1..M7 in classical order, Phi = 32 */
+  FMM_WINOGRAD = 2,          /* Strassen-Winograd variant, raw gauge, Phi = 56 (Table E.2) */
+  FMM_TSTAR = 3              /* the Phi-optimal T*, Phi = 200/9 (Theorem 1; eq. A.2) */
+};
+
+/* ---- block-scale rules (Appendix E.2; power-of-two variants) ------------ */
+enum {
+  FMM_RULE_FP32_AMAX = 0,    /* s = fl32(max(amax, fl32(1e-12)) / 448), stored as fp32 */
+  FMM_RULE_POW2_CEIL = 1,    /* s = 2^e, e the least integer with a <= 448 2^e; E8M0 byte */
+  FMM_RULE_POW2_OCP = 2      /* s = 2^(floor(log2 a) - 8) (OCP MX rule, clips to 448); E8M0 */
+};
+
+/* ---- plan flags ---------------------------------------------------------- */
+enum {
+  /* Sum the products of the dequantized operands at fp32 precision.  The
+   * default sub-product path feeds the e4m3 codes and E8M0 scales to the
+   * fp8 matrix cores, whose dot product aligns each group of eight products
+   * to the group's largest and keeps 13 bits below it (measured on gfx950);
+   * with this flag the codes are converted exactly to bf16 and multiplied on
+   * the bf16 matrix cores (23 retained bits), each block's partial sum is
+   * scaled and accumulated in fp32.  Half the peak rate of the default path.
+   * FP32_AMAX scales and block 16 always take this path. */
+  FMM_FLAG_EXACT_DOT = 1
+};
+
+typedef struct fmm_real fmm_real;   /* a base realization (U, V, w), R x 4 each, binary64 */
+typedef struct fmm_plan fmm_plan;   /* one problem shape bound to a realization */
+
+typedef struct {
+  int64_t batch;   /* number of independent products, >= 0 */
+  int64_t M, K, N; /* each >= 0 and divisible by 2^depth; K / 2^depth divisible by block */
+  int32_t depth;   /* recursion (Kronecker) depth l: 1, 2 or 3 */
+  int32_t block;   /* e4m3 block length along the contracted axis: 16, 32 or 128 */
+  int32_t rule;    /* FMM_RULE_* */
+  int32_t flags;   /* FMM_FLAG_* bits; others must be 0 */
+} fmm_plan_desc;
+
+/* Where the quantized operands of one side sit inside a workspace.
+ * codes : uint8 e4m3 codes, [batch][terms][rows][kdim], contracted axis last
+ *         (A side: rows = M / 2^l; B side: rows = N / 2^l, i.e. y_r transposed)
+ * scales: [batch][terms][rows][kblocks], one per block; uint8 E8M0 (e + 127)
+ *         when scale_bytes == 1, IEEE binary32 when scale_bytes == 4. */
+typedef struct {
+  void *codes;
+  void *scales;
+  int64_t batch, terms, rows, kdim, kblocks;
+  int32_t scale_bytes;
+  int32_t reserved;
+} fmm_view;
+
+/* ---- realizations (host only; no device needed) ------------------------ */
+
+/* A named realization.  *out receives a new handle. */
+int fmm_realization_builtin(int which, fmm_real **out);
+
+/* A realization of <2,2,2;R> (1 <= R <= 8) from caller arrays U, V, w, each
+ * R x 4 row-major binary64 in the conventions above.  If the Brent residual
+ * max|sum_r U_r (x) V_r (x) w_r - <2,2,2>| exceeds tol the call fails with
+ * FMM_ERR_NOT_EXACT (tol < 0 is FMM_ERR_ARG). */
+int fmm_realization_create(int R, const double *U, const double *V, const double *w,
+                           double tol, fmm_real **out);
+
+/* D . g for g = (X, Y, Z) in GL(2)^3 (eq. A.1):
+ *   u -> u (X (x) Y^-T), v -> v (Y (x) Z^-T), w -> w (Z (x) X^-T),
+ * each 2x2 factor given row-major (4 doubles).  Evaluated in binary64 in
+ * this order: the inverse by the adjugate (det = a d - b c, entries divided
+ * by det), then the Kronecker matrix, then u K with each entry summed in
+ * ascending index; no fused multiply-add.  |det| < 1e-12 gives
+ * FMM_ERR_SINGULAR. */
+int fmm_realization_transform(const fmm_real *d, const double X[4], const double Y[4],
+                              const double Z[4], fmm_real **out);
+
+/* The canonical rebalanced gauge (Appendix E.2):
+ * (U_r, V_r, W_r) -> (U_r / s_r, s_r V_r, W_r), s_r = sqrt(|U_r| / |V_r|). */
+int fmm_realization_rebalance(const fmm_real *d, fmm_real **out);
+
+/* Phi = sum_r |U_r|^2 |V_r|^2 |W_r|^2 and Gamma = sum_r |U_r||V_r||W_r|
+ * (Section 2.1) of the depth-l flattening (Phi^l, Gamma^l), and the Brent
+ * residual of the base realization.  Any output pointer may be NULL. */
+int fmm_realization_metrics(const fmm_real *d, int depth, double *phi, double *gamma,
+                            double *brent_resid);
+
+/* R (base rank) and T = R^depth. */
+int fmm_realization_terms(const fmm_real *d, int depth, int64_t *rank, int64_t *terms);
+
+/* The base coefficients, R x 4 binary64 each (any pointer may be NULL). */
+int fmm_realization_coefficients(const fmm_real *d, double *U, double *V, double *w);
+
+/* The exact fp32 depth-l tables the kernels use, T x 4^l each. */
+int fmm_realization_tables(const fmm_real *d, int depth, float *U, float *V, float *w);
+
+void fmm_realization_destroy(fmm_real *d);
+
+/* ---- plans and the product --------------------------------------------- */
+
+/* Validates desc (FMM_ERR_ARG / FMM_ERR_SHAPE / FMM_ERR_UNSUPPORTED are
+ * returned before any device call), then uploads the coefficient tables to
+ * the current device (FMM_ERR_DEVICE if it is not gfx950). */
+int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out);
+
+/* Bytes of device workspace fmm_encode/fmm_multiply/fmm_matmul need: the
+ * codes and scales of both operands, plus, at depth >= 2, the inner-level
+ * partial products.  The workspace must be 256-byte aligned. */
+int fmm_plan_workspace_size(const fmm_plan *p, size_t *bytes);
+
+/* Steps "encode + quantize" of both operands (device pointers dA: batch x M x K,
+ * dB: batch x K x N, fp32, each 16-byte aligned) into the workspace. */
+int fmm_encode(const fmm_plan *p, const float *dA, const float *dB, void *dWs, void *stream);
+
+/* Pointers and extents of the quantized operands inside dWs (host call). */
+int fmm_operand_views(const fmm_plan *p, void *dWs, fmm_view *a, fmm_view *b);
+
+/* Steps "fp8 sub-products + W-combine": reads the encoded workspace and writes
+ * C (batch x M x N fp32).  At depth >= 2 it also uses the workspace's
+ * partial-product region. */
+int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream);
+
+/* fmm_encode followed by fmm_multiply. */
+int fmm_matmul(const fmm_plan *p, const float *dA, const float *dB, float *dC, void *dWs,
+               void *stream);
+
+void fmm_plan_destroy(fmm_plan *p);
+
+/* ---- error measurement (Appendix E.2: relative error against an fp64 product) */
+
+/* dCref = A B in binary64 (batch x M x N), from the fp32 operands. */
+int fmm_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *dA,
+                      const float *dB, double *dCref, void *stream);
+
+/* Device scratch the reduction below needs. */
+int fmm_error_stats_scratch_size(int64_t batch, int64_t M, int64_t N, size_t *bytes);
+
+/* Per product b: dOut[2b] = sum (C - Cref)^2, dOut[2b+1] = sum Cref^2, binary64,
+ * by a fixed-order two-pass reduction (identical results run to run).
+ * dOut is a device pointer to 2*batch doubles. */
+int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const double *dCref,
+                    double *dOut, void *dScratch, size_t scratch_bytes, void *stream);
+
+/* ---- the codec alone --------------------------------------------------- */
+
+/* dOut[i] = e4m3 code of dIn[i] at unit scale: round to nearest, ties to the
+ * even mantissa field, saturate to +-448, keep the sign (the cast the
+ * quantizer applies after dividing by the block scale).  n >= 0; dIn must be
+ * 16-byte and dOut 4-byte aligned. */
+int fmm_e4m3_quantize(const float *dIn, uint8_t *dOut, int64_t n, void *stream);
+
+/* ---- misc ---------------------------------------------------------------- */
+
+const char *fmm_status_string(int status);
+const char *fmm_last_error_detail(void);
+/* FMM_OK if device `device` is a gfx950, FMM_ERR_DEVICE if not, FMM_ERR_HIP
+ * if it cannot be queried. */
+int fmm_device_check(int device);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FMM8_H */

@@ -1,0 +1,78 @@
+// Internal declarations shared by the host library and the kernel launchers.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/fmm8.h"
+
+namespace fmm {
+
+constexpr int kMaxRank = 8;    // <2,2,2;R>, R <= 8 (cubic has 8 terms)
+constexpr int kMaxDepth = 3;
+
+struct Realization {
+  int R;
+  double U[kMaxRank][4];
+  double V[kMaxRank][4];
+  double W[kMaxRank][4];
+};
+
+int realization_builtin(int which, Realization &d);
+double brent_residual(const Realization &d);
+int realization_transform(const Realization &d, const double X[4], const double Y[4],
+                          const double Z[4], Realization &out);
+void realization_rebalance(const Realization &d, Realization &out);
+void realization_phi_gamma(const Realization &d, double &phi, double &gamma);
+int64_t ipow(int64_t b, int e);
+void flatten(const double (*base)[4], int R, int depth, float *out);
+
+// ---- device-side coefficient tables -------------------------------------
+// For one operand side: the nonzero coefficients of each flattened term in
+// ascending sub-block order.  offsets[r] .. offsets[r+1] index entries.
+struct CoefEntry {
+  int32_t block;   // sub-block index P 2^l + Q
+  float coef;      // fp32 flattened coefficient (nonzero)
+};
+
+// Everything a launch needs, in one struct passed by value.
+struct Problem {
+  int64_t batch, M, K, N;
+  int64_t mp, kp, np;      // M / 2^l, K / 2^l, N / 2^l
+  int depth, nsplit;       // nsplit = 2^l
+  int block, rule;
+  int R;                   // base rank
+  int64_t T;               // R^l
+  int64_t To;              // R^(l-1): number of outer terms
+  int64_t kblocks;         // kp / block
+  int scale_bytes;         // 1 (E8M0) or 4 (fp32)
+  int exact_dot;           // FMM_FLAG_EXACT_DOT requested
+};
+
+// Layout of a workspace: byte offsets from its base.
+struct Workspace {
+  size_t a_codes, b_codes, a_scales, b_scales, partial, total;
+};
+
+// Device copies of the plan's tables (one allocation).
+struct DeviceTables {
+  const int32_t *a_off;        // T + 1
+  const CoefEntry *a_ent;
+  const int32_t *b_off;
+  const CoefEntry *b_ent;
+  const float *w_inner;        // R x 4 fp32 base w (the inner-level decoder)
+  const float *w_outer;        // To x 4^(l-1) fp32 flattened depth-(l-1) w (depth >= 2)
+};
+
+// ---- launchers (kernels_*.hip); return a hipError_t as int ---------------
+int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
+                  uint8_t *ws, const Workspace &wl, void *stream);
+int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl, float *C, void *stream);
+int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *A,
+                         const float *B, double *Cref, void *stream);
+size_t error_stats_scratch_bytes(int64_t batch, int64_t M, int64_t N);
+int launch_error_stats(int64_t batch, int64_t M, int64_t N, const float *C, const double *Cref,
+                       double *out, void *scratch, void *stream);
+int launch_e4m3_quantize(const float *in, uint8_t *out, int64_t n, void *stream);
+
+}  // namespace fmm

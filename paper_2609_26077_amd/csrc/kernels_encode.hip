@@ -1,0 +1,181 @@
+// Fused operand combine + block quantization (the encoder of Assumption 1).
+//
+// One workgroup owns a tile of TR "rows" x TL contracted positions of the
+// sub-block grid and produces the codes and scales of every flattened term
+// for that tile.  A rows are rows of A's sub-blocks; B rows are columns of
+// B's sub-blocks, so both outputs have the contracted axis last.
+//
+//   1. stage: the tile of all 4^l sub-blocks is read from HBM (coalesced)
+//      into LDS as fp32, laid out [block][row][l] with the contracted axis
+//      contiguous (the B side transposes on the way in);
+//   2. combine: a wave takes 64 items (row, 4 consecutive l) of one term; each
+//      lane forms x = sum_b c_b a_b over the term's nonzero coefficients in
+//      ascending b, as separate fp32 multiplies and adds;
+//   3. quantize: the block maximum over `block` consecutive l is reduced
+//      across the block/4 lanes that hold it, the rule gives the scale, the
+//      lane divides and casts its four values and stores one word of codes.
+#include <hip/hip_runtime.h>
+
+#include "device.h"
+#include "internal.h"
+
+namespace fmm {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTL = 128;            // contracted positions per tile (>= every block size)
+constexpr int kStride = kTL + 4;    // LDS row stride in floats (conflict-free transposed writes)
+constexpr int kLdsFloats = 16896;   // 4^l * TR * kStride for every depth (67.6 KB)
+
+template <int DEPTH>
+struct Tile {
+  static constexpr int nblk = 1 << (2 * DEPTH);
+  static constexpr int TR = 128 / nblk;      // 32, 8, 2 rows
+  static_assert(nblk * TR * kStride == kLdsFloats, "LDS size");
+};
+
+template <int SIDE, int DEPTH>
+__global__ __launch_bounds__(kThreads) void encode_kernel(
+    const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
+    const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
+    int64_t tiles_l) {
+  using TT = Tile<DEPTH>;
+  constexpr int TR = TT::TR;
+  constexpr int NB = TT::nblk;
+  constexpr int n = 1 << DEPTH;
+  __shared__ float4 lds4[kLdsFloats / 4];
+  float *lds = reinterpret_cast<float *>(lds4);
+
+  const int t = threadIdx.x;
+  const int64_t bt = blockIdx.y;                         // batch element
+  const int64_t tile = blockIdx.x;
+  const int64_t row0 = (tile / tiles_l) * TR;
+  const int64_t l0 = (tile % tiles_l) * kTL;
+  const int64_t rows = SIDE == 0 ? pb.mp : pb.np;        // rows of the output
+  const int64_t kp = pb.kp;
+
+  // ---- 1. stage the tile ----------------------------------------------------
+  if (SIDE == 0) {
+    // A (M x K): block b = I n + J holds rows I m' + p, columns J k' + l.
+    const float *Ab = src + bt * pb.M * pb.K;
+    for (int e = t; e < NB * TR * (kTL / 4); e += kThreads) {
+      const int b = e / (TR * (kTL / 4));
+      const int rem = e % (TR * (kTL / 4));
+      const int r = rem / (kTL / 4);
+      const int c4 = rem % (kTL / 4);
+      const int64_t p = row0 + r, l = l0 + 4 * c4;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (p < rows && l < kp) {
+        const int I = b / n, J = b % n;
+        v = *reinterpret_cast<const float4 *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l);
+      }
+      *reinterpret_cast<float4 *>(lds + (b * TR + r) * kStride + 4 * c4) = v;
+    }
+  } else {
+    // B (K x N): block b = J n + K holds rows J k' + l, columns K n' + q;
+    // lanes run along q so each of the four loads is coalesced.
+    const float *Bb = src + bt * pb.K * pb.N;
+    for (int e = t; e < NB * TR * (kTL / 4); e += kThreads) {
+      const int b = e / (TR * (kTL / 4));
+      const int rem = e % (TR * (kTL / 4));
+      const int q = rem % TR;
+      const int c4 = rem / TR;
+      const int64_t qq = row0 + q, l = l0 + 4 * c4;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (qq < rows && l < kp) {
+        const int J = b / n, Kb = b % n;
+        const float *p = Bb + (J * kp + l) * pb.N + Kb * pb.np + qq;
+        v.x = p[0];
+        v.y = p[pb.N];
+        v.z = p[2 * pb.N];
+        v.w = p[3 * pb.N];
+      }
+      *reinterpret_cast<float4 *>(lds + (b * TR + q) * kStride + 4 * c4) = v;
+    }
+  }
+  __syncthreads();
+
+  // ---- 2./3. combine and quantize ----------------------------------------------
+  constexpr int P = TR * (kTL / 4);          // positions per term (multiple of 64)
+  const int64_t T = pb.T;
+  const int gl = pb.block / 4;               // lanes per block
+  const int64_t kb_count = pb.kblocks;
+  for (int64_t item = t; item < T * P; item += kThreads) {
+    const int64_t r = __builtin_amdgcn_readfirstlane((int)(item / P));   // wave-uniform term
+    const int pos = (int)(item % P);
+    const int row = pos / (kTL / 4);
+    const int c4 = pos % (kTL / 4);
+    const int beg = __builtin_amdgcn_readfirstlane(off[r]);
+    const int end = __builtin_amdgcn_readfirstlane(off[r + 1]);
+    float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
+    for (int e = beg; e < end; ++e) {
+      const int b = ent[e].block;
+      const float c = ent[e].coef;
+      const float4 v = *reinterpret_cast<const float4 *>(lds + (b * TR + row) * kStride + 4 * c4);
+      const float t0 = __fmul_rn(c, v.x), t1 = __fmul_rn(c, v.y);
+      const float t2 = __fmul_rn(c, v.z), t3 = __fmul_rn(c, v.w);
+      if (e == beg) {
+        x0 = t0; x1 = t1; x2 = t2; x3 = t3;
+      } else {
+        x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
+        x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
+      }
+    }
+    // block maximum across the gl lanes of this block (all lanes take part)
+    float m = fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3)));
+    for (int s = 1; s < gl; s <<= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
+    const dev::Scale sc = dev::block_scale(m, pb.rule);
+    const uint32_t w = dev::e4m3_pack4(dev::scaled(x0, sc, pb.rule), dev::scaled(x1, sc, pb.rule),
+                                       dev::scaled(x2, sc, pb.rule), dev::scaled(x3, sc, pb.rule));
+    const int64_t p = row0 + row;
+    const int64_t l = l0 + 4 * c4;
+    if (p < rows && l < kp) {
+      const int64_t rowid = (bt * T + r) * rows + p;
+      *reinterpret_cast<uint32_t *>(codes + rowid * kp + l) = w;
+      if ((c4 % gl) == 0) {
+        const int64_t kb = l / pb.block;
+        if (pb.scale_bytes == 1)
+          scales[rowid * kb_count + kb] = (uint8_t)sc.stored;
+        else
+          reinterpret_cast<uint32_t *>(scales)[rowid * kb_count + kb] = sc.stored;
+      }
+    }
+  }
+}
+
+template <int SIDE, int DEPTH>
+hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
+                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
+  const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
+  const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
+  const int64_t tiles_r = (rows + Tile<DEPTH>::TR - 1) / Tile<DEPTH>::TR;
+  const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
+  hipLaunchKernelGGL((encode_kernel<SIDE, DEPTH>), grid, dim3(kThreads), 0, st, src, pb, off,
+                     ent, codes, scales, tiles_l);
+  return hipGetLastError();
+}
+
+template <int SIDE>
+hipError_t launch_depth(const Problem &pb, const float *src, const int32_t *off,
+                        const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
+  switch (pb.depth) {
+    case 1: return launch_side<SIDE, 1>(pb, src, off, ent, codes, scales, st);
+    case 2: return launch_side<SIDE, 2>(pb, src, off, ent, codes, scales, st);
+    case 3: return launch_side<SIDE, 3>(pb, src, off, ent, codes, scales, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
+                  uint8_t *ws, const Workspace &wl, void *stream) {
+  if (pb.batch == 0 || pb.M == 0 || pb.N == 0 || pb.K == 0) return hipSuccess;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_depth<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, st);
+  if (e != hipSuccess) return e;
+  return launch_depth<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, st);
+}
+
+}  // namespace fmm

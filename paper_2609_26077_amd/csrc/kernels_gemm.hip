@@ -1,0 +1,466 @@
+// fp8 sub-products with fp32 accumulation and the fused W-combine.
+//
+// A workgroup owns a BM x BN tile of the m' x n' grid and one outer term
+// r_o; it runs the K loop of each of the R inner terms r = r_o R + r_i in turn
+// (one flattened (term, k-step) pipeline), and after each term adds
+// w[r_i][q] * P_r into four quadrant accumulators q = 2k + i held in
+// registers.  At depth 1 the quadrants are the four blocks of C and are
+// written once; at depth >= 2 they are the inner-level partial products,
+// combined over r_o by outer_combine_kernel.
+//
+// MX path (power-of-two scales, block 32 or 128): v_mfma_scale_f32_32x32x64_f8f6f4
+// applies the E8M0 block scales in hardware.  Operand layout of that
+// instruction (measured): lane (r, h = lane/32) holds row r, contracted bytes
+// [16h, 16h+16) in VGPRs 0-3 and [32+16h, +16) in VGPRs 4-7; VGPRs 0-3 of all
+// lanes form the instruction's first 32-element scale block, VGPRs 4-7 the
+// second, and lane r + 32 kb supplies the scale of block kb of row r.
+//
+// The fp8 dot product of those instructions aligns each group of eight
+// products to the group's largest and keeps 13 bits below it (measured:
+// 1 + 2^-13 survives, 1 + 2^-14 returns 1; groups are summed at fp32 grade).
+//
+// Exact-dot path (fp32 scales, block 16, or FMM_FLAG_EXACT_DOT): the codes are
+// converted exactly to bf16 (v_cvt_scalef32_pk_bf16_fp8 at scale 1) and fed to
+// v_mfma_f32_32x32x16_bf16 (lane (r, h) holds row r, elements [8h, 8h+8);
+// 23 retained bits), summed per block in a temporary and scaled by sA * sB in
+// fp32 -- the products of the dequantized operands accumulated in fp32.
+//
+// Output layout of the 32x32 instructions: lane l, register j holds
+// column l % 32, row 8 (j / 4) + 4 (l / 32) + j % 4.
+#include <hip/hip_runtime.h>
+
+#include "device.h"
+#include "internal.h"
+
+namespace fmm {
+
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// eight e4m3 codes (little-endian in two words) -> eight bf16, exactly
+__device__ __forceinline__ v8bf e4m3x8_to_bf16(uint2 w) {
+  const v2bf a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, false);
+  const v2bf b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, true);
+  const v2bf c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, false);
+  const v2bf d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, true);
+  v8bf r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
+  r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
+  return r;
+}
+
+constexpr int BM = 128, BN = 128, BK = 128;
+constexpr int kThreads = 256;
+
+struct GemmArgs {
+  const uint8_t *xa, *xb;        // codes, [batch][T][rows][kp]
+  const uint8_t *sa, *sb;        // scales, [batch][T][rows][kblocks]
+  float *out;                    // C (depth 1) or partial products (depth >= 2)
+  int64_t mp, np, kp, kblocks, T, To, M, N;
+  int R, block, depth, tiles_n;
+  const float *w;                // R x 4 inner decoder weights (device)
+};
+
+// LDS tile: 128 rows x 128 bytes; 16-byte chunk c of row r sits at chunk c ^ (r & 7)
+__device__ __forceinline__ int swz(int row, int chunk) { return row * BK + 16 * (chunk ^ (row & 7)); }
+
+// Global -> registers for one (term, k-step): each thread moves four 16-byte chunks
+// of A and four of B.  Rows past the end and chunks past kp read as zero.
+struct Stage {
+  uint4 a[4], b[4];
+};
+
+__device__ __forceinline__ void load_stage(const GemmArgs &g, int64_t bt, int64_t r, int64_t k0,
+                                           int64_t pm0, int64_t pn0, Stage &s) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = t + kThreads * j;
+    const int row = c >> 3, ch = c & 7;
+    const int64_t k = k0 + 16 * ch;
+    const int64_t pa = pm0 + row, pb = pn0 + row;
+    uint4 za = make_uint4(0, 0, 0, 0), zb = make_uint4(0, 0, 0, 0);
+    if (pa < g.mp && k < g.kp)
+      za = *reinterpret_cast<const uint4 *>(g.xa + ((bt * g.T + r) * g.mp + pa) * g.kp + k);
+    if (pb < g.np && k < g.kp)
+      zb = *reinterpret_cast<const uint4 *>(g.xb + ((bt * g.T + r) * g.np + pb) * g.kp + k);
+    s.a[j] = za;
+    s.b[j] = zb;
+  }
+}
+
+__device__ __forceinline__ void store_stage(uint8_t *la, uint8_t *lb, const Stage &s) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = t + kThreads * j;
+    const int row = c >> 3, ch = c & 7;
+    *reinterpret_cast<uint4 *>(la + swz(row, ch)) = s.a[j];
+    *reinterpret_cast<uint4 *>(lb + swz(row, ch)) = s.b[j];
+  }
+}
+
+// E8M0 scale bytes a lane needs for one k-step: [tile i][substep s] for A, [j][s] for B.
+struct MxScales {
+  int a[2][2], b[2][2];
+};
+
+__device__ __forceinline__ int scale_byte(const uint8_t *base, int64_t rowid_valid, int64_t rowid,
+                                          int64_t kblocks, int64_t k, int64_t kp, int block) {
+  if (!rowid_valid || k >= kp) return 127;  // padding: codes are zero, scale 1.0
+  return base[rowid * kblocks + k / block];
+}
+
+__device__ __forceinline__ void load_mx_scales(const GemmArgs &g, int64_t bt, int64_t r, int64_t k0,
+                                               int64_t rowa0, int64_t rowb0, MxScales &sc) {
+  const int lane = threadIdx.x & 63;
+  const int r32 = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int64_t k = k0 + 64 * s + 32 * h;
+      const int64_t pa = rowa0 + 32 * i + r32;
+      const int64_t pb = rowb0 + 32 * i + r32;
+      sc.a[i][s] = scale_byte(g.sa, pa < g.mp, (bt * g.T + r) * g.mp + pa, g.kblocks, k, g.kp, g.block);
+      sc.b[i][s] = scale_byte(g.sb, pb < g.np, (bt * g.T + r) * g.np + pb, g.kblocks, k, g.kp, g.block);
+    }
+}
+
+__device__ __forceinline__ v8i frag_mx(const uint8_t *lt, int row, int s, int h) {
+  const uint4 lo = *reinterpret_cast<const uint4 *>(lt + swz(row, 4 * s + h));
+  const uint4 hi = *reinterpret_cast<const uint4 *>(lt + swz(row, 4 * s + 2 + h));
+  v8i f;
+  f[0] = (int)lo.x; f[1] = (int)lo.y; f[2] = (int)lo.z; f[3] = (int)lo.w;
+  f[4] = (int)hi.x; f[5] = (int)hi.y; f[6] = (int)hi.z; f[7] = (int)hi.w;
+  return f;
+}
+
+__device__ __forceinline__ void store_tile(const GemmArgs &g, int64_t bt, int64_t ro, int q,
+                                           int64_t p0, int64_t c0, const v16f &v) {
+  // p0/c0: first row/column of this 32x32 tile in the m' x n' grid
+  const int lane = threadIdx.x & 63;
+  const int64_t col = c0 + (lane & 31);
+  if (col >= g.np) return;
+  const int iq = q & 1, kq = q >> 1;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int64_t row = p0 + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+    if (row < g.mp) {
+      if (g.depth == 1) {
+        g.out[bt * g.M * g.N + (iq * g.mp + row) * g.N + kq * g.np + col] = v[j];
+      } else {
+        g.out[(((bt * g.To + ro) * 4 + q) * g.mp + row) * g.np + col] = v[j];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads, 1) void gemm_mx_kernel(GemmArgs g) {
+  __shared__ uint4 lds_raw[2 * 2 * BM * BK / 16];
+  uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
+  const int t = threadIdx.x;
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r32 = lane & 31, h = lane >> 5;
+  const int64_t tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  const int64_t ro = blockIdx.y, bt = blockIdx.z;
+  const int64_t pm0 = tm * BM, pn0 = tn * BN;
+  const int64_t rowa0 = pm0 + wm * 64, rowb0 = pn0 + wn * 64;
+
+  const int64_t nsteps = (g.kp + BK - 1) / BK;
+  const int64_t total = (int64_t)g.R * nsteps;
+
+  v16f acc[2][2];
+  v16f quad[4][2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = (v16f){};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) quad[q][i][j] = (v16f){};
+    }
+
+  Stage st;
+  MxScales sc, sc_next;
+  load_stage(g, bt, ro * g.R, 0, pm0, pn0, st);
+  load_mx_scales(g, bt, ro * g.R, 0, rowa0, rowb0, sc);
+  store_stage(lds, lds + BM * BK, st);
+  __syncthreads();
+
+  for (int64_t it = 0; it < total; ++it) {
+    const int ri = (int)(it / nsteps);
+    const int64_t ks = it % nsteps;
+    const int buf = (int)(it & 1);
+    const bool more = it + 1 < total;
+    if (more) {
+      const int64_t rn = ro * g.R + (it + 1) / nsteps;
+      const int64_t kn = ((it + 1) % nsteps) * BK;
+      load_stage(g, bt, rn, kn, pm0, pn0, st);
+      load_mx_scales(g, bt, rn, kn, rowa0, rowb0, sc_next);
+    }
+    const uint8_t *la = lds + buf * 2 * BM * BK;
+    const uint8_t *lb = la + BM * BK;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      v8i fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = frag_mx(la, wm * 64 + 32 * i + r32, s, h);
+        fb[i] = frag_mx(lb, wn * 64 + 32 * i + r32, s, h);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              fa[i], fb[j], acc[i][j], 0, 0, 0, sc.a[i][s], 0, sc.b[j][s]);
+    }
+    if (ks == nsteps - 1) {
+      // end of term ri: quadrant q += w[ri][q] * P
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float wq = g.w[4 * ri + q];
+        if (wq != 0.0f) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) quad[q][i][j][e] = __fmaf_rn(wq, acc[i][j][e], quad[q][i][j][e]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+    }
+    if (more) {
+      uint8_t *na = lds + (buf ^ 1) * 2 * BM * BK;
+      store_stage(na, na + BM * BK, st);
+      sc = sc_next;
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        store_tile(g, bt, ro, q, rowa0 + 32 * i, rowb0 + 32 * j, quad[q][i][j]);
+}
+
+// ---------------------------------------------------------------------------
+// Promotion path: fp32 block scales (or block 16)
+// ---------------------------------------------------------------------------
+
+constexpr int kMaxKbPerStep = BK / 16;   // block 16 -> 8 blocks per k-step
+
+__global__ __launch_bounds__(kThreads, 1) void gemm_promote_kernel(GemmArgs g, int scale_bytes) {
+  __shared__ uint4 lds_raw[2 * 2 * BM * BK / 16];
+  __shared__ float lsa[BM * kMaxKbPerStep];
+  __shared__ float lsb[BN * kMaxKbPerStep];
+  uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
+  const int t = threadIdx.x;
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r32 = lane & 31, h = lane >> 5;
+  const int64_t tm = blockIdx.x / g.tiles_n, tn = blockIdx.x % g.tiles_n;
+  const int64_t ro = blockIdx.y, bt = blockIdx.z;
+  const int64_t pm0 = tm * BM, pn0 = tn * BN;
+  const int64_t rowa0 = pm0 + wm * 64, rowb0 = pn0 + wn * 64;
+  const int64_t nsteps = (g.kp + BK - 1) / BK;
+  const int64_t total = (int64_t)g.R * nsteps;
+  const int kb_step = BK / g.block > 0 ? BK / g.block : 1;  // blocks per k-step (block <= 128)
+  const int chunks_per_block = g.block / 16;
+
+  v16f acc[2][2], quad[4][2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = (v16f){};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) quad[q][i][j] = (v16f){};
+    }
+
+  Stage st;
+  load_stage(g, bt, ro * g.R, 0, pm0, pn0, st);
+  store_stage(lds, lds + BM * BK, st);
+
+  for (int64_t it = 0; it < total; ++it) {
+    const int ri = (int)(it / nsteps);
+    const int64_t ks = it % nsteps;
+    const int64_t r = ro * g.R + ri;
+    const int buf = (int)(it & 1);
+    const bool more = it + 1 < total;
+    // scales of this step into LDS (fp32 values)
+    for (int e = t; e < (BM + BN) * kb_step; e += kThreads) {
+      const bool isb = e >= BM * kb_step;
+      const int ee = isb ? e - BM * kb_step : e;
+      const int row = ee / kb_step, kbl = ee % kb_step;
+      const int64_t kb = ks * kb_step + kbl;
+      const int64_t p = (isb ? pn0 : pm0) + row;
+      const int64_t rows = isb ? g.np : g.mp;
+      float v = 0.f;
+      if (p < rows && kb < g.kblocks) {
+        const int64_t idx = ((bt * g.T + r) * rows + p) * g.kblocks + kb;
+        const uint8_t *base = isb ? g.sb : g.sa;
+        if (scale_bytes == 4)
+          v = reinterpret_cast<const float *>(base)[idx];
+        else
+          v = __uint_as_float((uint32_t)base[idx] << 23);   // 2^(e8m0 - 127)
+      }
+      (isb ? lsb : lsa)[row * kMaxKbPerStep + kbl] = v;
+    }
+    __syncthreads();
+    if (more) {
+      const int64_t rn = ro * g.R + (it + 1) / nsteps;
+      const int64_t kn = ((it + 1) % nsteps) * BK;
+      load_stage(g, bt, rn, kn, pm0, pn0, st);
+    }
+    const uint8_t *la = lds + buf * 2 * BM * BK;
+    const uint8_t *lb = la + BM * BK;
+    for (int kbl = 0; kbl < kb_step; ++kbl) {
+      v16f tmp[2][2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) tmp[i][j] = (v16f){};
+      for (int cc = 0; cc < chunks_per_block; ++cc) {
+        const int c = kbl * chunks_per_block + cc;   // 16-byte chunk within the step
+        v8bf fa[2], fb[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int rowa = wm * 64 + 32 * i + r32, rowb = wn * 64 + 32 * i + r32;
+          fa[i] = e4m3x8_to_bf16(*reinterpret_cast<const uint2 *>(la + swz(rowa, c) + 8 * h));
+          fb[i] = e4m3x8_to_bf16(*reinterpret_cast<const uint2 *>(lb + swz(rowb, c) + 8 * h));
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            tmp[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], tmp[i][j], 0, 0, 0);
+      }
+      // promote: acc += sA[row] sB[col] tmp
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const float sbv = lsb[(wn * 64 + 32 * j + r32) * kMaxKbPerStep + kbl];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int row = wm * 64 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+            const float s = lsa[row * kMaxKbPerStep + kbl] * sbv;
+            acc[i][j][e] = __fmaf_rn(s, tmp[i][j][e], acc[i][j][e]);
+          }
+        }
+    }
+    if (ks == nsteps - 1) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float wq = g.w[4 * ri + q];
+        if (wq != 0.0f) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) quad[q][i][j][e] = __fmaf_rn(wq, acc[i][j][e], quad[q][i][j][e]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+    }
+    __syncthreads();   // everyone is done with this buffer and with lsa/lsb
+    if (more) {
+      uint8_t *na = lds + (buf ^ 1) * 2 * BM * BK;
+      store_stage(na, na + BM * BK, st);
+    }
+  }
+
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        store_tile(g, bt, ro, q, rowa0 + 32 * i, rowb0 + 32 * j, quad[q][i][j]);
+}
+
+// ---------------------------------------------------------------------------
+// Outer combine (depth >= 2): C block (I, K) with I = 2 I_o + i, K = 2 K_o + k:
+//   C = sum_{r_o} w_outer[r_o][K_o 2^(l-1) + I_o] * Q[r_o][2k + i]
+// ---------------------------------------------------------------------------
+template <int NO>   // NO = 4^(l-1) outer blocks
+__global__ __launch_bounds__(256) void outer_combine_kernel(const float *__restrict__ Q,
+                                                            const float *__restrict__ wo,
+                                                            float *__restrict__ C, Problem pb) {
+  constexpr int no = NO == 4 ? 2 : 4;   // 2^(l-1)
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // p * n' + q
+  const int iq = blockIdx.y;                                           // inner quadrant 2k + i
+  const int64_t bt = blockIdx.z;
+  if (pos >= pb.mp * pb.np) return;
+  const int64_t p = pos / pb.np, q = pos % pb.np;
+  float acc[NO];
+#pragma unroll
+  for (int o = 0; o < NO; ++o) acc[o] = 0.f;
+  for (int64_t ro = 0; ro < pb.To; ++ro) {
+    const float v = Q[(((bt * pb.To + ro) * 4 + iq) * pb.mp + p) * pb.np + q];
+#pragma unroll
+    for (int o = 0; o < NO; ++o) acc[o] = __fmaf_rn(wo[ro * NO + o], v, acc[o]);
+  }
+  const int i = iq & 1, k = iq >> 1;
+#pragma unroll
+  for (int o = 0; o < NO; ++o) {
+    const int Ko = o / no, Io = o % no;       // column index o = K_o 2^(l-1) + I_o
+    const int64_t I = 2 * Io + i, K = 2 * Ko + k;
+    C[bt * pb.M * pb.N + (I * pb.mp + p) * pb.N + K * pb.np + q] = acc[o];
+  }
+}
+
+}  // namespace
+
+int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *ws,
+                    const Workspace &wl, float *C, void *stream) {
+  if (pb.batch == 0 || pb.M == 0 || pb.N == 0) return hipSuccess;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  GemmArgs g;
+  g.xa = ws + wl.a_codes;
+  g.xb = ws + wl.b_codes;
+  g.sa = ws + wl.a_scales;
+  g.sb = ws + wl.b_scales;
+  g.out = pb.depth == 1 ? C : reinterpret_cast<float *>(const_cast<uint8_t *>(ws) + wl.partial);
+  g.mp = pb.mp; g.np = pb.np; g.kp = pb.kp; g.kblocks = pb.kblocks;
+  g.T = pb.T; g.To = pb.To; g.M = pb.M; g.N = pb.N;
+  g.R = pb.R; g.block = pb.block; g.depth = pb.depth;
+  const int64_t tiles_m = (pb.mp + BM - 1) / BM, tiles_n = (pb.np + BN - 1) / BN;
+  g.tiles_n = (int)tiles_n;
+  g.w = tab.w_inner;
+  const dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)pb.To, (unsigned)pb.batch);
+  const bool mx = !pb.exact_dot && pb.rule != dev::RULE_FP32_AMAX && (pb.block == 32 || pb.block == 128);
+  if (mx)
+    hipLaunchKernelGGL(gemm_mx_kernel, grid, dim3(kThreads), 0, st, g);
+  else
+    hipLaunchKernelGGL(gemm_promote_kernel, grid, dim3(kThreads), 0, st, g, pb.scale_bytes);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || pb.depth == 1) return e;
+  const int64_t npos = pb.mp * pb.np;
+  const dim3 g2((unsigned)((npos + 255) / 256), 4, (unsigned)pb.batch);
+  if (pb.depth == 2)
+    hipLaunchKernelGGL(outer_combine_kernel<4>, g2, dim3(256), 0, st, g.out, tab.w_outer, C, pb);
+  else
+    hipLaunchKernelGGL(outer_combine_kernel<16>, g2, dim3(256), 0, st, g.out, tab.w_outer, C, pb);
+  return hipGetLastError();
+}
+
+}  // namespace fmm

@@ -1,0 +1,280 @@
+// Plans, workspace layout and the device entry points of the C-ABI.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_detail;
+
+int hip_status(int e) {
+  if (e == hipSuccess) return FMM_OK;
+  g_detail = hipGetErrorString(static_cast<hipError_t>(e));
+  return FMM_ERR_HIP;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool is_gfx950(int dev) {
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return false;
+  return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+}
+
+}  // namespace
+
+struct fmm_plan {
+  fmm::Problem pb;
+  fmm::Workspace wl;
+  fmm::DeviceTables tab;
+  void *dev_tables;   // one device allocation backing tab
+  int device;
+};
+
+extern "C" {
+
+const char *fmm_status_string(int status) {
+  switch (status) {
+    case FMM_OK: return "ok";
+    case FMM_ERR_ARG: return "invalid argument";
+    case FMM_ERR_SHAPE: return "shape not divisible as required";
+    case FMM_ERR_UNSUPPORTED: return "unsupported configuration";
+    case FMM_ERR_NOT_EXACT: return "realization is not exact (Brent residual above tolerance)";
+    case FMM_ERR_SINGULAR: return "singular basis change";
+    case FMM_ERR_HIP: return "HIP runtime error";
+    case FMM_ERR_DEVICE: return "device is not gfx950";
+    case FMM_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case FMM_ERR_NOMEM: return "host allocation failed";
+    default: return "unknown status";
+  }
+}
+
+const char *fmm_last_error_detail(void) { return g_detail.c_str(); }
+
+int fmm_device_check(int device) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) return FMM_ERR_HIP;
+  return is_gfx950(device) ? FMM_OK : FMM_ERR_DEVICE;
+}
+
+int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out) {
+  if (!out) return FMM_ERR_ARG;
+  *out = nullptr;
+  if (!d || !desc) return FMM_ERR_ARG;
+  const fmm_plan_desc &q = *desc;
+  if ((q.flags & ~FMM_FLAG_EXACT_DOT) != 0 || q.batch < 0 || q.M < 0 || q.K < 0 || q.N < 0) return FMM_ERR_ARG;
+  if (q.depth < 1 || q.depth > fmm::kMaxDepth) return FMM_ERR_ARG;
+  if (q.block != 16 && q.block != 32 && q.block != 128) return FMM_ERR_ARG;
+  if (q.rule < FMM_RULE_FP32_AMAX || q.rule > FMM_RULE_POW2_OCP) return FMM_ERR_ARG;
+  const int64_t n = int64_t(1) << q.depth;
+  if (q.M % n || q.K % n || q.N % n) return FMM_ERR_SHAPE;
+  if ((q.K / n) % q.block) return FMM_ERR_SHAPE;
+  // grid limits of the launches (batch on grid z/y, terms on grid y)
+  if (q.batch > 65535) return FMM_ERR_UNSUPPORTED;
+
+  // the realization, as the C-ABI sees it
+  int64_t R = 0, T = 0;
+  if (fmm_realization_terms(d, q.depth, &R, &T) != FMM_OK) return FMM_ERR_ARG;
+
+  fmm_plan *p = new (std::nothrow) fmm_plan;
+  if (!p) return FMM_ERR_NOMEM;
+  fmm::Problem &pb = p->pb;
+  pb.batch = q.batch; pb.M = q.M; pb.K = q.K; pb.N = q.N;
+  pb.depth = q.depth; pb.nsplit = (int)n;
+  pb.mp = q.M / n; pb.kp = q.K / n; pb.np = q.N / n;
+  pb.block = q.block; pb.rule = q.rule;
+  pb.R = (int)R; pb.T = T; pb.To = fmm::ipow(R, q.depth - 1);
+  pb.kblocks = pb.kp / q.block;
+  pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
+  pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
+
+  // workspace layout
+  fmm::Workspace &wl = p->wl;
+  size_t off = 0;
+  const size_t B = (size_t)q.batch;
+  wl.a_codes = off; off = align256(off + B * T * pb.mp * pb.kp);
+  wl.b_codes = off; off = align256(off + B * T * pb.np * pb.kp);
+  wl.a_scales = off; off = align256(off + B * T * pb.mp * pb.kblocks * pb.scale_bytes);
+  wl.b_scales = off; off = align256(off + B * T * pb.np * pb.kblocks * pb.scale_bytes);
+  wl.partial = off;
+  if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
+  wl.total = off;
+
+  // host tables: fp32 flattened U, V (nonzeros in ascending block order), base w, outer w
+  const int nb = (int)(n * n);
+  std::vector<float> U((size_t)T * nb), V((size_t)T * nb);
+  fmm_realization_tables(d, q.depth, U.data(), V.data(), nullptr);
+  std::vector<int32_t> aoff(T + 1), boff(T + 1);
+  std::vector<fmm::CoefEntry> aent, bent;
+  for (int64_t r = 0; r < T; ++r) {
+    aoff[r] = (int32_t)aent.size();
+    boff[r] = (int32_t)bent.size();
+    for (int b = 0; b < nb; ++b) {
+      const float u = U[r * nb + b], v = V[r * nb + b];
+      if (u != 0.0f) aent.push_back({b, u});
+      if (v != 0.0f) bent.push_back({b, v});
+    }
+  }
+  aoff[T] = (int32_t)aent.size();
+  boff[T] = (int32_t)bent.size();
+  std::vector<float> wbase((size_t)R * 4);
+  fmm_realization_tables(d, 1, nullptr, nullptr, wbase.data());
+  std::vector<float> wouter;
+  if (q.depth >= 2) {
+    const int no = 1 << (2 * (q.depth - 1));
+    wouter.resize((size_t)pb.To * no);
+    fmm_realization_tables(d, q.depth - 1, nullptr, nullptr, wouter.data());
+  }
+
+  // device copy: [aoff][boff][aent][bent][winner][wouter]
+  const size_t s_aoff = align256((T + 1) * sizeof(int32_t));
+  const size_t s_boff = s_aoff;
+  const size_t s_aent = align256(std::max<size_t>(1, aent.size()) * sizeof(fmm::CoefEntry));
+  const size_t s_bent = align256(std::max<size_t>(1, bent.size()) * sizeof(fmm::CoefEntry));
+  const size_t s_wi = align256(wbase.size() * sizeof(float));
+  const size_t s_wo = align256(std::max<size_t>(1, wouter.size()) * sizeof(float));
+  const size_t tot = s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo;
+  std::vector<uint8_t> host(tot, 0);
+  std::memcpy(host.data(), aoff.data(), (T + 1) * sizeof(int32_t));
+  std::memcpy(host.data() + s_aoff, boff.data(), (T + 1) * sizeof(int32_t));
+  if (!aent.empty()) std::memcpy(host.data() + s_aoff + s_boff, aent.data(), aent.size() * sizeof(fmm::CoefEntry));
+  if (!bent.empty())
+    std::memcpy(host.data() + s_aoff + s_boff + s_aent, bent.data(), bent.size() * sizeof(fmm::CoefEntry));
+  std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent, wbase.data(), wbase.size() * sizeof(float));
+  if (!wouter.empty())
+    std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent + s_wi, wouter.data(),
+                wouter.size() * sizeof(float));
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    delete p;
+    return hip_status(hipErrorNoDevice);
+  }
+  if (!is_gfx950(dev)) {
+    delete p;
+    return FMM_ERR_DEVICE;
+  }
+  p->device = dev;
+  void *dt = nullptr;
+  int e = hipMalloc(&dt, tot);
+  if (e == hipSuccess) e = hipMemcpy(dt, host.data(), tot, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    if (dt) (void)hipFree(dt);
+    delete p;
+    return hip_status(e);
+  }
+  p->dev_tables = dt;
+  uint8_t *base = reinterpret_cast<uint8_t *>(dt);
+  p->tab.a_off = reinterpret_cast<const int32_t *>(base);
+  p->tab.b_off = reinterpret_cast<const int32_t *>(base + s_aoff);
+  p->tab.a_ent = reinterpret_cast<const fmm::CoefEntry *>(base + s_aoff + s_boff);
+  p->tab.b_ent = reinterpret_cast<const fmm::CoefEntry *>(base + s_aoff + s_boff + s_aent);
+  p->tab.w_inner = reinterpret_cast<const float *>(base + s_aoff + s_boff + s_aent + s_bent);
+  p->tab.w_outer = reinterpret_cast<const float *>(base + s_aoff + s_boff + s_aent + s_bent + s_wi);
+  *out = p;
+  return FMM_OK;
+}
+
+int fmm_plan_workspace_size(const fmm_plan *p, size_t *bytes) {
+  if (!p || !bytes) return FMM_ERR_ARG;
+  *bytes = p->wl.total;
+  return FMM_OK;
+}
+
+int fmm_operand_views(const fmm_plan *p, void *dWs, fmm_view *a, fmm_view *b) {
+  if (!p) return FMM_ERR_ARG;
+  uint8_t *ws = reinterpret_cast<uint8_t *>(dWs);
+  const fmm::Problem &pb = p->pb;
+  if (a) {
+    a->codes = ws ? ws + p->wl.a_codes : nullptr;
+    a->scales = ws ? ws + p->wl.a_scales : nullptr;
+    a->batch = pb.batch; a->terms = pb.T; a->rows = pb.mp; a->kdim = pb.kp;
+    a->kblocks = pb.kblocks; a->scale_bytes = pb.scale_bytes; a->reserved = 0;
+  }
+  if (b) {
+    b->codes = ws ? ws + p->wl.b_codes : nullptr;
+    b->scales = ws ? ws + p->wl.b_scales : nullptr;
+    b->batch = pb.batch; b->terms = pb.T; b->rows = pb.np; b->kdim = pb.kp;
+    b->kblocks = pb.kblocks; b->scale_bytes = pb.scale_bytes; b->reserved = 0;
+  }
+  return FMM_OK;
+}
+
+static int check_ws(const fmm_plan *p, const void *ws) {
+  if (p->wl.total > 0 && !ws) return FMM_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return FMM_ERR_WORKSPACE;
+  return FMM_OK;
+}
+
+int fmm_encode(const fmm_plan *p, const float *dA, const float *dB, void *dWs, void *stream) {
+  if (!p) return FMM_ERR_ARG;
+  const fmm::Problem &pb = p->pb;
+  const bool empty = pb.batch == 0 || pb.M == 0 || pb.N == 0 || pb.K == 0;
+  if (!empty && (!dA || !dB)) return FMM_ERR_ARG;
+  if (!empty && ((reinterpret_cast<uintptr_t>(dA) | reinterpret_cast<uintptr_t>(dB)) % 16)) return FMM_ERR_ARG;
+  int st = check_ws(p, dWs);
+  if (st != FMM_OK) return st;
+  return hip_status(fmm::launch_encode(pb, p->tab, dA, dB, reinterpret_cast<uint8_t *>(dWs), p->wl, stream));
+}
+
+int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream) {
+  if (!p) return FMM_ERR_ARG;
+  const fmm::Problem &pb = p->pb;
+  const bool empty = pb.batch == 0 || pb.M == 0 || pb.N == 0;
+  if (!empty && !dC) return FMM_ERR_ARG;
+  int st = check_ws(p, dWs);
+  if (st != FMM_OK) return st;
+  return hip_status(fmm::launch_multiply(pb, p->tab, reinterpret_cast<const uint8_t *>(dWs),
+                                         p->wl, dC, stream));
+}
+
+int fmm_matmul(const fmm_plan *p, const float *dA, const float *dB, float *dC, void *dWs,
+               void *stream) {
+  int st = fmm_encode(p, dA, dB, dWs, stream);
+  if (st != FMM_OK) return st;
+  return fmm_multiply(p, dWs, dC, stream);
+}
+
+void fmm_plan_destroy(fmm_plan *p) {
+  if (!p) return;
+  if (p->dev_tables) (void)hipFree(p->dev_tables);
+  delete p;
+}
+
+int fmm_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *dA,
+                      const float *dB, double *dCref, void *stream) {
+  if (batch < 0 || M < 0 || K < 0 || N < 0 || batch > 65535) return FMM_ERR_ARG;
+  if (batch > 0 && M > 0 && N > 0 && (!dCref || (K > 0 && (!dA || !dB)))) return FMM_ERR_ARG;
+  return hip_status(fmm::launch_reference_f64(batch, M, K, N, dA, dB, dCref, stream));
+}
+
+int fmm_error_stats_scratch_size(int64_t batch, int64_t M, int64_t N, size_t *bytes) {
+  if (batch < 0 || M < 0 || N < 0 || !bytes) return FMM_ERR_ARG;
+  *bytes = fmm::error_stats_scratch_bytes(batch, M, N);
+  return FMM_OK;
+}
+
+int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const double *dCref,
+                    double *dOut, void *dScratch, size_t scratch_bytes, void *stream) {
+  if (batch < 0 || M < 0 || N < 0 || batch > 65535) return FMM_ERR_ARG;
+  if (batch == 0) return FMM_OK;
+  if (!dOut || (M * N > 0 && (!dC || !dCref))) return FMM_ERR_ARG;
+  if (!dScratch || scratch_bytes < fmm::error_stats_scratch_bytes(batch, M, N)) return FMM_ERR_WORKSPACE;
+  return hip_status(fmm::launch_error_stats(batch, M, N, dC, dCref, dOut, dScratch, stream));
+}
+
+int fmm_e4m3_quantize(const float *dIn, uint8_t *dOut, int64_t n, void *stream) {
+  if (n < 0) return FMM_ERR_ARG;
+  if (n == 0) return FMM_OK;
+  if (!dIn || !dOut) return FMM_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(dIn) % 16 || reinterpret_cast<uintptr_t>(dOut) % 4) return FMM_ERR_ARG;
+  return hip_status(fmm::launch_e4m3_quantize(dIn, dOut, n, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+"""Convenience wrappers over the C-ABI with torch-owned device buffers.
+
+Allocation and marshalling only: the arithmetic of every call happens in the
+library's HIP kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (Realization, fmm_encode, fmm_error_stats, fmm_error_stats_scratch_size,
+               fmm_matmul, fmm_multiply, fmm_operand_views, fmm_plan_create,
+               fmm_plan_workspace_size, fmm_realization_builtin, fmm_reference_f64, make_desc)
+
+
+class FMM:
+    """One planned product shape on one device, with its own workspace."""
+
+    def __init__(self, realization, batch, M, K, N, depth=1, block=32, rule="pow2_ceil",
+                 device="cuda:0", exact_dot=False):
+        if not isinstance(realization, Realization):
+            realization = fmm_realization_builtin(realization)
+        self.real = realization
+        self.device = torch.device(device)
+        self.shape = (int(batch), int(M), int(K), int(N))
+        self.depth, self.block = int(depth), int(block)
+        with torch.cuda.device(self.device):
+            self.plan = fmm_plan_create(realization, make_desc(batch, M, K, N, depth, block, rule,
+                                                               exact_dot=exact_dot))
+            nbytes = fmm_plan_workspace_size(self.plan)
+            self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        self.scale_bytes = 4 if (rule in ("fp32_amax", 0)) else 1
+
+    def matmul(self, A, B, C=None, stream=None):
+        b, M, K, N = self.shape
+        if C is None:
+            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        fmm_matmul(self.plan, A, B, C, self.ws, stream)
+        return C
+
+    def encode(self, A, B, stream=None):
+        fmm_encode(self.plan, A, B, self.ws, stream)
+
+    def multiply(self, C=None, stream=None):
+        b, M, K, N = self.shape
+        if C is None:
+            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        fmm_multiply(self.plan, self.ws, C, stream)
+        return C
+
+    def operands(self):
+        """torch views of (a_codes, a_scales, b_codes, b_scales) in the workspace."""
+        a, b = fmm_operand_views(self.plan, self.ws)
+        base = self.ws.data_ptr()
+        out = []
+        for v in (a, b):
+            nc = v.batch * v.terms * v.rows * v.kdim
+            ns = v.batch * v.terms * v.rows * v.kblocks
+            c0 = v.codes - base
+            s0 = v.scales - base
+            codes = self.ws[c0:c0 + nc].view(v.batch, v.terms, v.rows, v.kdim)
+            sraw = self.ws[s0:s0 + ns * v.scale_bytes]
+            if v.scale_bytes == 4:
+                scales = sraw.view(torch.float32).view(v.batch, v.terms, v.rows, v.kblocks)
+            else:
+                scales = sraw.view(v.batch, v.terms, v.rows, v.kblocks)
+            out += [codes, scales]
+        return tuple(out)
+
+
+def reference_f64(A, B, stream=None):
+    b, M, K = A.shape
+    N = B.shape[2]
+    Cref = torch.empty((b, M, N), dtype=torch.float64, device=A.device)
+    fmm_reference_f64(b, M, K, N, A, B, Cref, stream)
+    return Cref
+
+
+def error_stats(C, Cref, stream=None):
+    """(err2, ref2) per product as numpy float64 arrays (one host sync)."""
+    b, M, N = C.shape
+    nbytes = fmm_error_stats_scratch_size(b, M, N)
+    scratch = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=C.device)
+    out = torch.empty((b, 2), dtype=torch.float64, device=C.device)
+    fmm_error_stats(b, M, N, C, Cref, out, scratch, nbytes, stream)
+    o = out.cpu().numpy()
+    return o[:, 0].copy(), o[:, 1].copy()

@@ -1,0 +1,144 @@
+"""GPU parity against the oracle at sizes the oracle finishes in seconds.
+
+Shapes span several GEMM tiles (128 x 128) and encoder tiles, with ragged
+tails in every dimension (m', n' not multiples of 128, k' not a multiple of
+the 128-byte k-step), every realization, scale rule, block size and depth,
+batches, transformed realizations, and the degenerate inputs the quantizer
+has (all-zero blocks, blocks below the clamp, saturation).
+"""
+import numpy as np
+import pytest
+
+import fmm_inputs as gen
+from tests.gpu_helpers import check_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("exact", [False, True])
+@pytest.mark.parametrize("name", ["cubic8", "strassen", "winograd", "tstar"])
+def test_config1_shape_all_realizations(name, exact):
+    """256^3, N(0,1), block 32, power-of-two (E8M0) scales, depth 1."""
+    r = check_case(name, "gaussian", 2, 256, 256, 256, 1, 32, 1, seed=0, cfg=1, exact=exact)
+    print(name, r, flush=True)
+
+
+@pytest.mark.parametrize("rule", [0, 1, 2])
+@pytest.mark.parametrize("bs", [16, 32, 128])
+def test_rules_and_blocks(rule, bs):
+    """All three scale rules x all block sizes (fp8 and exact-dot paths)."""
+    r = check_case("tstar", "student_t3", 1, 384, 512, 320, 1, bs, rule, seed=1, cfg=2, ns=False)
+    print(r, flush=True)
+    check_case("tstar", "student_t3", 1, 384, 512, 320, 1, bs, rule, seed=1, cfg=2, exact=True)
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 64, 2), (1, 66, 192, 130), (3, 258, 320, 194),
+                                   (2, 130, 1088, 62), (1, 512, 576, 256)])
+def test_ragged_shapes(shape):
+    """Tails: m', n' not multiples of the 128 tile; k' not a multiple of 128."""
+    b, M, K, N = shape
+    tiny = M * N <= 16
+    r = check_case("strassen", "gaussian", b, M, K, N, 1, 32, 1, seed=2, cfg=3, ns=not tiny)
+    print(r, flush=True)
+    check_case("strassen", "gaussian", b, M, K, N, 1, 32, 1, seed=2, cfg=3, exact=True)
+
+
+@pytest.mark.parametrize("depth,name", [(2, "tstar"), (2, "strassen"), (3, "tstar"),
+                                        (2, "cubic8")])
+def test_depths(depth, name):
+    n = 2 ** depth
+    for exact in (False, True):
+        check_case(name, "uniform", 1, 64 * n + 16 * n, 64 * n, 48 * n, depth, 32, 1, seed=3,
+                   cfg=4, exact=exact)
+
+
+def test_depth2_rules_blocks():
+    check_case("winograd", "gaussian", 2, 264, 512, 200, 2, 16, 0, seed=4, cfg=5)
+    for exact in (False, True):
+        check_case("tstar", "rowscaled", 1, 256, 1024, 256, 2, 128, 2, seed=4, cfg=5,
+                   exact=exact, ns=False)
+
+
+def test_transformed_realizations():
+    """Random GL(2)^3 changes of Strassen (the batched sweep's arms)."""
+    for i, g in enumerate(gen.basis_changes(4, seed=7)):
+        for exact in (False, True):
+            r = check_case(("strassen", g), "student_t3", 4, 128, 128, 128, 1, 32, 1, seed=7,
+                           cfg=6, trial=i, exact=exact, ns=False)
+            print(i, r, flush=True)
+
+
+def test_rowscaled_family():
+    """Per-row log-uniform scales over four decades stress the blocks along K."""
+    for depth in (1, 2, 3):
+        n = 2 ** depth
+        for exact in (False, True):
+            r = check_case("tstar", "rowscaled", 1, 32 * n, 64 * n, 32 * n, depth, 32, 1, seed=8,
+                           cfg=7, exact=exact, ns=False)
+            print(depth, r, flush=True)
+
+
+def test_degenerate_blocks():
+    """Zero rows/columns (clamp, zero codes), tiny blocks (below 1e-12), huge
+    blocks, negative zeros, and K = 0."""
+    import torch
+    from tests.gpu_helpers import run_gpu
+    from oracle import e4m3, fmm
+    from oracle import realizations as R
+    A, B = gen.operands("gaussian", 1, 128, 256, 128, seed=9)
+    A[0, 3, :] = 0.0
+    A[0, 5, :64] = -0.0
+    A[0, 7, :] *= np.float32(1e-14)
+    A[0, 9, :] *= np.float32(1e30)
+    B[0, :, 11] = 0.0
+    B[0, 32:64, 12] = np.float32(3e-13)
+    tabs = R.tables_f32(R.builtin_f64("tstar"), 1)
+    for rule in (0, 1, 2):
+        g = run_gpu("tstar", A, B, 1, 32, rule)
+        o = fmm.fmm(A[0], B[0], tabs, 1, 32, rule)
+        from tests.gpu_helpers import compare_operands
+        compare_operands(g["ops"], o["a"], o["b"], 0, rule)
+        Cg, Co = g["C"][0].astype(np.float64), o["C"]
+        assert np.abs(Cg - Co).max() <= 1e-5 * np.linalg.norm(Co)
+    # K = 0: C is zero
+    import paper_2609_26077_amd as fm
+    from paper_2609_26077_amd.runner import FMM
+    f = FMM("tstar", 1, 64, 0, 64, 1, 32, "pow2_ceil")
+    A0 = torch.zeros((1, 64, 0), device="cuda:0")
+    B0 = torch.zeros((1, 0, 64), device="cuda:0")
+    C = f.matmul(A0, B0)
+    assert torch.count_nonzero(C).item() == 0
+
+
+def test_batch_of_small_products():
+    """The batched sweep's layout: many independent 512^3 products."""
+    for exact in (False, True):
+        r = check_case("tstar", "student_t3", 16, 512, 512, 512, 1, 32, 1, seed=10, cfg=8,
+                       check_every=5, exact=exact, ns=False)
+        print(r, flush=True)
+
+
+def test_deterministic():
+    """Two identical runs give identical C and identical error sums."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
+    A, B = gen.operands("gaussian", 2, 384, 512, 256, seed=11)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM("tstar", 2, 384, 512, 256, 1, 32, "pow2_ceil")
+    C1 = f.matmul(dA, dB).clone()
+    C2 = f.matmul(dA, dB).clone()
+    assert torch.equal(C1, C2)
+    Cr = reference_f64(dA, dB)
+    assert error_stats(C1, Cr)[0].tolist() == error_stats(C2, Cr)[0].tolist()
+
+
+def test_encode_then_multiply_equals_matmul():
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    A, B = gen.operands("uniform", 1, 256, 256, 256, seed=12)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM("winograd", 1, 256, 256, 256, 2, 32, "pow2_ocp")
+    C1 = f.matmul(dA, dB).clone()
+    f.encode(dA, dB)
+    C2 = f.multiply()
+    assert torch.equal(C1, C2)
