@@ -1,0 +1,197 @@
+"""Throughput of the block-scaled e4m3 Strassen-type product on one MI355X.
+
+One step = one fmm_matmul call: encode + quantize both operands, the T fp8
+sub-products with the fused W-combine, C written once; fp32 A and B are
+resident in HBM before the timed region.  Default workload: 8192^3, one
+level, the Phi-optimal realization T*, e4m3 block 32 along K, power-of-two
+(E8M0) block scales, A and B iid N(0,1) (synthetic, seeded).
+
+Prints one JSON line with the effective rate 2MNK / t, the relative RMS error
+of C against the fp64 product (measured after the timed region), the
+roofline of the dominant kernel (the sub-product GEMM, against the fp8 dense
+MFMA peak) with HIP-event kernel times taken on the launch stream, and the
+oracle timed on this host's cores on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+FP8_DENSE_PEAK_TFLOPS = 5000.0      # MI355X dense fp8 (MX) matrix peak
+BF16_DENSE_PEAK_TFLOPS = 2500.0
+HBM_PEAK_GBS = 8000.0
+
+METRIC = "effective fp8 TFLOP/s (2mnk/t) at 8192³ 1-level; relative RMS error vs fp64"
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--size", type=int, default=8192, help="M = K = N")
+    p.add_argument("--depth", type=int, default=1)
+    p.add_argument("--block", type=int, default=32)
+    p.add_argument("--rule", default="pow2_ceil")
+    p.add_argument("--realization", default="tstar")
+    p.add_argument("--family", default="gaussian")
+    p.add_argument("--exact-dot", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample", type=int, default=4096,
+                   help="edge of the cubic products the oracle is timed on")
+    p.add_argument("--cpu-trials", type=int, default=2)
+    return p.parse_args()
+
+
+def cpu_baseline(args):
+    """The oracle, unchanged, timed end to end on one bounded sample."""
+    from oracle import e4m3, fmm
+    from oracle import realizations as R
+    import fmm_inputs as gen
+    n = args.cpu_sample
+    tabs = R.tables_f32(R.builtin_f64(args.realization), args.depth)
+    rule = e4m3.RULES[args.rule]
+    t = 0.0
+    for trial in range(args.cpu_trials):
+        A, B = gen.operands(args.family, 1, n, n, n, seed=0, cfg=90, trial=trial)
+        t0 = time.perf_counter()
+        fmm.fmm(A[0], B[0], tabs, args.depth, args.block, rule, keep=False)
+        t += time.perf_counter() - t0
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"value": args.cpu_trials * 2.0 * n ** 3 / t / 1e12, "unit": "TFLOP/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{args.cpu_trials} x {n}x{n}x{n} products ({args.realization}, depth {args.depth}, block "
+                      f"{args.block}, {args.rule}, {args.family}): numpy fp32 encode + e4m3 codec, "
+                      f"fp64 BLAS sub-products, W-combine; {t:.2f} s wall",
+            "seconds": t, "cpu_model": cpu}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the path has no cross-GPU step); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import fmm_inputs as gen
+    from paper_2609_26077_amd import fmm_realization_metrics
+    from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
+
+    dev = torch.device("cuda:0")
+    n = args.size
+    M = K = N = n
+    A, B = gen.operands(args.family, 1, M, K, N, seed=0, cfg=0, trial=0)
+    dA = torch.from_numpy(A).to(dev)
+    dB = torch.from_numpy(B).to(dev)
+    del A, B
+    f = FMM(args.realization, 1, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
+    C = torch.empty((1, M, N), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        f.matmul(dA, dB, C, stream)
+    torch.cuda.synchronize(dev)
+
+    # timed region: K whole steps, events around each launch on the launch stream
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        ev[s][0].record(stream)
+        f.encode(dA, dB, stream)
+        ev[s][1].record(stream)
+        f.multiply(C, stream)
+        ev[s][2].record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    mul_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    ms_per_step = wall * 1e3 / args.steps
+
+    # error of the last step's C against the fp64 product (not timed)
+    Cref = reference_f64(dA, dB)
+    err2, ref2 = error_stats(C, Cref)
+    rel_mse = float(err2.sum() / ref2.sum())
+    del Cref
+
+    real = f.real
+    R_, T = 0, 0
+    from paper_2609_26077_amd import fmm_realization_terms
+    R_, T = fmm_realization_terms(real, args.depth)
+    phi = fmm_realization_metrics(real, args.depth)["phi"]
+    mkn = 2.0 * M * N * K
+    mfma_flop = mkn * T / 8.0 ** args.depth
+    mp, kp, np_ = M // 2 ** args.depth, K // 2 ** args.depth, N // 2 ** args.depth
+    sb = 4 if args.rule == "fp32_amax" else 1
+    code_bytes = T * (mp + np_) * kp
+    scale_bytes = T * (mp + np_) * (kp // args.block) * sb
+    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes
+    gemm_bytes = code_bytes + scale_bytes + 4 * M * N
+    peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \
+        else FP8_DENSE_PEAK_TFLOPS
+    achieved = mfma_flop / (mul_ms * 1e-3) / 1e12
+
+    line = {
+        "metric": METRIC,
+        "value": mkn / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8",
+        "data": "synthetic",
+        "config": {"workload": f"{M}x{K}x{N} product, depth {args.depth}, realization "
+                               f"{args.realization} (Phi={phi:.4f}), e4m3 block {args.block} along K, "
+                               f"{args.rule} scales, {args.family} operands"
+                               + (", exact-dot" if args.exact_dot else ""),
+                   "M": M, "K": K, "N": N, "depth": args.depth, "terms": T, "block": args.block,
+                   "rule": args.rule, "realization": args.realization, "family": args.family,
+                   "exact_dot": bool(args.exact_dot)},
+        "rel_rms_error_vs_fp64": float(np.sqrt(rel_mse)),
+        "rel_mse_vs_fp64": rel_mse,
+        "kernels_ms": {"encode": enc_ms, "multiply": mul_ms},
+        "roofline": {"bound": "mfma", "kernel": "sub-product GEMM (fmm_multiply)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "algorithmic_flop_per_launch": mfma_flop},
+        "encode_roofline": {"bound": "hbm", "achieved": enc_bytes / (enc_ms * 1e-3) / 1e9,
+                            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                            "algorithmic_bytes_per_launch": enc_bytes},
+        "gemm_compulsory_bytes": gemm_bytes,
+        "device": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        del dA, dB, C
+        torch.cuda.empty_cache()
+        line["cpu_baseline"] = cpu_baseline(args)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
