@@ -257,6 +257,231 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_kernel(GemmArgs g) {
         store_tile(g, bt, ro, q, rowa0 + 32 * i, rowb0 + 32 * j, quad[q][i][j]);
 }
 
+
+// ---------------------------------------------------------------------------
+// Fast MX path for tile-aligned shapes (m', n' multiples of 128; k' a multiple
+// of 128 for block 32, of 512 for block 128).
+//
+// One workgroup of four waves owns a 128 x 128 tile of the m' x n' grid; each
+// wave a 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  The codes and E8M0
+// scales of each 128-byte K step go from HBM straight into LDS
+// (global_load_lds: no staging registers) through a three-slot ring, two
+// steps ahead of the step being multiplied; each wave issues exactly nine
+// such transfers per step (four 1 KB of A codes, four of B codes, one 256 B of
+// scales) and waits for them with an explicit vmcnt, so the steady state holds
+// two steps of loads in flight.  LDS code rows are 128 bytes with 16-byte
+// chunk c stored at c ^ (row & 7) (conflict-free fragment reads).
+//
+// The quadrant accumulators of the fused W-combine live in AGPRs for the
+// whole kernel (the four 64 x 64 sets fill the 256 accumulation registers),
+// leaving the architectural VGPRs to the MFMA accumulator, the operand
+// fragments and addressing; they are touched only through the helpers below.
+// ---------------------------------------------------------------------------
+constexpr int FBK = 128;
+constexpr int kSlot = 2 * BM * FBK + 2 * BM * 4;   // codes A, B + scale words A, B
+constexpr int kSlots = 3;
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+__device__ __forceinline__ void agpr_zero(float &q) {
+  asm volatile("v_accvgpr_write_b32 %0, 0" : "=a"(q));
+}
+__device__ __forceinline__ void agpr_fma(float &q, float w, float p) {
+  float t;
+  asm volatile(
+      "v_accvgpr_read_b32 %0, %1\n\t"
+      "v_fmac_f32_e32 %0, %2, %3\n\t"
+      "v_accvgpr_write_b32 %1, %0"
+      : "=&v"(t), "+a"(q)
+      : "s"(w), "v"(p));
+}
+__device__ __forceinline__ float agpr_read(const float &q) {
+  float v;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(q));
+  return v;
+}
+
+// One wave-wide transfer HBM -> LDS: lane l moves 16 (or 4) bytes from
+// base + off to LDS byte m0 + 16 l (or 4 l).
+__device__ __forceinline__ void dma16(uint32_t off, const uint8_t *base, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(m0)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(uint32_t off, const uint8_t *base, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "s"(m0)
+               : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// XCD-aware tile order: workgroups are dispatched round-robin over the eight
+// XCDs, so consecutive workgroups of one XCD (bid, bid + 8, ...) are given a
+// contiguous range of tiles, walked in groups of eight tile-rows so that the
+// workgroups resident on an XCD share A rows and B columns in its L2.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int &tm, int &tn) {
+  const int ntiles = tiles_m * tiles_n;
+  int id = bid;
+  if ((ntiles & 7) == 0) id = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+  constexpr int GM = 8;
+  const int per_group = GM * tiles_n;
+  const int group = id / per_group;
+  const int first_m = group * GM;
+  const int gm = min(tiles_m - first_m, GM);
+  const int in = id - group * per_group;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
+
+template <int BS>
+__global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, int tiles_m) {
+  __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+  uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_u8 *)lds_raw;
+  const int t = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int lane = t & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int r32 = lane & 31, h = lane >> 5;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, g.tiles_n, tm, tn);
+  const int64_t ro = blockIdx.y, bt = blockIdx.z;
+  const int64_t pm0 = (int64_t)tm * BM, pn0 = (int64_t)tn * BN;
+  const uint32_t kp = (uint32_t)g.kp, kblocks = (uint32_t)g.kblocks;
+  const int nk = (int)(g.kp / FBK);
+  const int total = g.R * nk;
+  const int wrow_a = wm * 64, wrow_b = wn * 64;
+
+  // per-lane DMA offsets: code region of 8 rows x 128 B, lane -> (row l/8, chunk (l%8) ^ (l/8))
+  const uint32_t code_off = (uint32_t)(lane >> 3) * kp + 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+  // scale words: wave 0/1 -> A rows 64w.., wave 2/3 -> B rows 64(w-2)..
+  const int srow = (wave & 1) * 64 + lane;
+  const uint32_t scale_off = (uint32_t)srow * kblocks;
+  const bool scale_is_b = wave >= 2;
+
+  auto issue = [&](int ri, int ks, int slot) {
+    const int64_t r = ro * g.R + ri;
+    const uint32_t k0 = (uint32_t)ks * FBK;
+    const uint8_t *xa = g.xa + ((bt * g.T + r) * g.mp + pm0) * g.kp + k0;
+    const uint8_t *xb = g.xb + ((bt * g.T + r) * g.np + pn0) * g.kp + k0;
+    const uint32_t m0 = lds_base + (uint32_t)slot * kSlot;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int region = wave * 4 + j;                     // rows 8 region .. +8
+      dma16(code_off, xa + (int64_t)region * 8 * g.kp, m0 + region * 1024);
+      dma16(code_off, xb + (int64_t)region * 8 * g.kp, m0 + BM * FBK + region * 1024);
+    }
+    const uint8_t *sbase = scale_is_b ? g.sb + ((bt * g.T + r) * g.np + pn0) * g.kblocks
+                                      : g.sa + ((bt * g.T + r) * g.mp + pm0) * g.kblocks;
+    const uint32_t kw = BS == 32 ? k0 / 32 : (k0 / 128) & ~3u;   // 4-byte aligned word
+    dma4(scale_off + kw, sbase, m0 + 2 * BM * FBK + (scale_is_b ? BM * 4 : 0) + (wave & 1) * 256);
+  };
+
+  v16f acc[2][2];
+  float quad[4][2][2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = (v16f){};
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) agpr_zero(quad[q][i][j][e]);
+    }
+
+  // prologue: steps 0 and 1 in flight
+  int ri_l = 0, ks_l = 0;            // next step to issue
+  auto advance = [&](int &ri, int &ks) {
+    if (++ks == nk) { ks = 0; ++ri; }
+  };
+  issue(ri_l, ks_l, 0);
+  advance(ri_l, ks_l);
+  if (total > 1) {
+    issue(ri_l, ks_l, 1);
+    advance(ri_l, ks_l);
+  }
+
+  int ri = 0, ks = 0, slot = 0;
+  for (int it = 0; it < total; ++it) {
+    if (it + 1 < total) wait_vmcnt<9>(); else wait_vmcnt<0>();
+    __syncthreads();
+    if (it + 2 < total) {
+      issue(ri_l, ks_l, slot == 0 ? 2 : slot - 1);
+      advance(ri_l, ks_l);
+    }
+    const uint8_t *la = lds + slot * kSlot;
+    const uint8_t *lb = la + BM * FBK;
+    const uint32_t *lsa = reinterpret_cast<const uint32_t *>(la + 2 * BM * FBK);
+    const uint32_t *lsb = lsa + BM;
+    int sA[2], sB[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t wa = lsa[wrow_a + 32 * i + r32];
+      const uint32_t wb = lsb[wrow_b + 32 * i + r32];
+      if (BS == 32) {           // block 2s + h of this step at byte 2s after the shift
+        sA[i] = (int)(wa >> (8 * h));
+        sB[i] = (int)(wb >> (8 * h));
+      } else {                  // one block per step: byte ks % 4 of the word
+        sA[i] = (int)(wa >> (8 * (ks & 3)));
+        sB[i] = (int)(wb >> (8 * (ks & 3)));
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      v8i fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = frag_mx(la, wrow_a + 32 * i + r32, s, h);
+        fb[i] = frag_mx(lb, wrow_b + 32 * i + r32, s, h);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          if (BS == 32 && s == 1)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0, 2, sA[i], 2, sB[j]);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0, 0, sA[i], 0, sB[j]);
+        }
+    }
+    if (ks + 1 == nk) {
+      // end of term ri: quadrant q += w[ri][q] * P
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float wq = g.w[4 * ri + q];
+        if (wq != 0.0f) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) agpr_fma(quad[q][i][j][e], wq, acc[i][j][e]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+    }
+    advance(ri, ks);
+    slot = slot == 2 ? 0 : slot + 1;
+  }
+
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        v16f v;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) v[e] = agpr_read(quad[q][i][j][e]);
+        store_tile(g, bt, ro, q, pm0 + wrow_a + 32 * i, pn0 + wrow_b + 32 * j, v);
+      }
+}
+
 // ---------------------------------------------------------------------------
 // Promotion path: fp32 block scales (or block 16)
 // ---------------------------------------------------------------------------
@@ -448,7 +673,14 @@ int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *w
   g.w = tab.w_inner;
   const dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)pb.To, (unsigned)pb.batch);
   const bool mx = !pb.exact_dot && pb.rule != dev::RULE_FP32_AMAX && (pb.block == 32 || pb.block == 128);
-  if (mx)
+  const bool aligned = pb.mp % BM == 0 && pb.np % BN == 0 && pb.kp > 0 &&
+                       pb.kp % (pb.block == 32 ? FBK : 4 * FBK) == 0 &&
+                       pb.mp * pb.kp < (int64_t(1) << 31) && pb.np * pb.kp < (int64_t(1) << 31);
+  if (mx && aligned && pb.block == 32)
+    hipLaunchKernelGGL(gemm_mx_fast_kernel<32>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  else if (mx && aligned && pb.block == 128)
+    hipLaunchKernelGGL(gemm_mx_fast_kernel<128>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  else if (mx)
     hipLaunchKernelGGL(gemm_mx_kernel, grid, dim3(kThreads), 0, st, g);
   else
     hipLaunchKernelGGL(gemm_promote_kernel, grid, dim3(kThreads), 0, st, g, pb.scale_bytes);

@@ -142,3 +142,19 @@ def test_encode_then_multiply_equals_matmul():
     f.encode(dA, dB)
     C2 = f.multiply()
     assert torch.equal(C1, C2)
+
+
+@pytest.mark.parametrize("case", [
+    ("tstar", 1, 256, 256, 256, 1, 32, 1),       # one 128 x 128 tile, one k-step
+    ("tstar", 1, 512, 1024, 768, 1, 32, 1),      # 2 x 3 tiles, four k-steps
+    ("cubic8", 2, 512, 512, 512, 1, 32, 2),      # eight terms, OCP rule
+    ("strassen", 1, 512, 2048, 256, 1, 128, 1),  # block 128 (k' = 1024)
+    ("tstar", 1, 1024, 1024, 512, 2, 32, 1),     # depth 2: m' = 256, k' = 256
+    ("winograd", 3, 256, 512, 256, 1, 32, 1),    # batch of three
+])
+def test_tile_aligned_fast_path(case):
+    """Shapes the tile-aligned kernel takes (m', n' multiples of 128; k' of 128,
+    or of 512 at block 128)."""
+    name, b, M, K, N, depth, bs, rule = case
+    r = check_case(name, "gaussian", b, M, K, N, depth, bs, rule, seed=13, cfg=9)
+    print(case, r, flush=True)
