@@ -10,11 +10,15 @@
 //      contiguous (the B side transposes on the way in);
 //   2. combine: a wave takes 64 items (row, 4 consecutive l) of one term; each
 //      lane forms x = sum_b c_b a_b over the term's nonzero coefficients in
-//      ascending b, as separate fp32 multiplies and adds;
+//      ascending b, as separate fp32 multiplies and adds (the coefficients of a
+//      term are read once into scalar registers when a tile holds enough
+//      positions per term);
 //   3. quantize: the block maximum over `block` consecutive l is reduced
 //      across the block/4 lanes that hold it, the rule gives the scale, the
 //      lane divides and casts its four values and stores one word of codes.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "device.h"
 #include "internal.h"
@@ -26,13 +30,14 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kTL = 128;            // contracted positions per tile (>= every block size)
 constexpr int kStride = kTL + 4;    // LDS row stride in floats (conflict-free transposed writes)
-constexpr int kLdsFloats = 16896;   // 4^l * TR * kStride for every depth (67.6 KB)
 
 template <int DEPTH>
 struct Tile {
   static constexpr int nblk = 1 << (2 * DEPTH);
-  static constexpr int TR = 128 / nblk;      // 32, 8, 2 rows
-  static_assert(nblk * TR * kStride == kLdsFloats, "LDS size");
+  static constexpr int TR = DEPTH == 3 ? 2 : 64 / nblk;   // 16, 4, 2 rows
+  static constexpr int lds_floats = nblk * TR * kStride;  // 33.8, 33.8, 67.6 KB
+  // a wave's 64 consecutive items must belong to one term
+  static_assert((TR * (kTL / 4)) % 64 == 0, "positions per term must fill whole waves");
 };
 
 template <int SIDE, int DEPTH>
@@ -44,7 +49,7 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
   constexpr int TR = TT::TR;
   constexpr int NB = TT::nblk;
   constexpr int n = 1 << DEPTH;
-  __shared__ float4 lds4[kLdsFloats / 4];
+  __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
 
   const int t = threadIdx.x;
@@ -97,30 +102,38 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
   __syncthreads();
 
   // ---- 2./3. combine and quantize ----------------------------------------------
-  constexpr int P = TR * (kTL / 4);          // positions per term (multiple of 64)
+  constexpr int P = TR * (kTL / 4);          // positions (row, 4 consecutive l) per term
   const int64_t T = pb.T;
   const int gl = pb.block / 4;               // lanes per block
   const int64_t kb_count = pb.kblocks;
-  for (int64_t item = t; item < T * P; item += kThreads) {
-    const int64_t r = __builtin_amdgcn_readfirstlane((int)(item / P));   // wave-uniform term
-    const int pos = (int)(item % P);
+
+  // one (term, position) item: combine, block maximum, scale, cast, store
+  // x += c * tile[b][row][4 c4 .. +3] in the pinned order (the first term is a plain product)
+  auto accumulate = [&](bool first, int b, float c, int row, int c4, float &x0, float &x1, float &x2,
+                        float &x3) {
+    const float4 v = *reinterpret_cast<const float4 *>(lds + (b * TR + row) * kStride + 4 * c4);
+    const float t0 = __fmul_rn(c, v.x), t1 = __fmul_rn(c, v.y);
+    const float t2 = __fmul_rn(c, v.z), t3 = __fmul_rn(c, v.w);
+    if (first) {
+      x0 = t0; x1 = t1; x2 = t2; x3 = t3;
+    } else {
+      x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
+      x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
+    }
+  };
+
+  // one (term, position) item: combine, block maximum, scale, cast, store.
+  // REG: the term's coefficients sit in a register array indexed by compile-time e.
+  auto item = [&](int64_t r, int pos, int n, const CoefEntry *ce, auto reg) {
     const int row = pos / (kTL / 4);
     const int c4 = pos % (kTL / 4);
-    const int beg = __builtin_amdgcn_readfirstlane(off[r]);
-    const int end = __builtin_amdgcn_readfirstlane(off[r + 1]);
     float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
-    for (int e = beg; e < end; ++e) {
-      const int b = ent[e].block;
-      const float c = ent[e].coef;
-      const float4 v = *reinterpret_cast<const float4 *>(lds + (b * TR + row) * kStride + 4 * c4);
-      const float t0 = __fmul_rn(c, v.x), t1 = __fmul_rn(c, v.y);
-      const float t2 = __fmul_rn(c, v.z), t3 = __fmul_rn(c, v.w);
-      if (e == beg) {
-        x0 = t0; x1 = t1; x2 = t2; x3 = t3;
-      } else {
-        x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
-        x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
-      }
+    if constexpr (decltype(reg)::value) {
+#pragma unroll
+      for (int e = 0; e < NB; ++e)
+        if (e < n) accumulate(e == 0, ce[e].block, ce[e].coef, row, c4, x0, x1, x2, x3);
+    } else {
+      for (int e = 0; e < n; ++e) accumulate(e == 0, ce[e].block, ce[e].coef, row, c4, x0, x1, x2, x3);
     }
     // block maximum across the gl lanes of this block (all lanes take part)
     float m = fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3)));
@@ -140,6 +153,28 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
         else
           reinterpret_cast<uint32_t *>(scales)[rowid * kb_count + kb] = sc.stored;
       }
+    }
+  };
+
+  if constexpr (P >= kThreads) {
+    // term-outer: the term's nonzero coefficients are read once into SGPRs
+    for (int64_t r = 0; r < T; ++r) {
+      const int beg = __builtin_amdgcn_readfirstlane(off[r]);
+      const int n = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
+      CoefEntry ce[NB];
+#pragma unroll
+      for (int e = 0; e < NB; ++e)
+        if (e < n) ce[e] = ent[beg + e];
+#pragma unroll
+      for (int pp = 0; pp < P / kThreads; ++pp) item(r, t + kThreads * pp, n, ce, std::true_type{});
+    }
+  } else {
+    // few positions per term: a wave takes 64 consecutive items (one term)
+    for (int64_t it = t; it < T * P; it += kThreads) {
+      const int64_t r = __builtin_amdgcn_readfirstlane((int)(it / P));
+      const int beg = __builtin_amdgcn_readfirstlane(off[r]);
+      const int n = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
+      item(r, (int)(it % P), n, ent + beg, std::false_type{});
     }
   }
 }
