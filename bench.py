@@ -1,16 +1,17 @@
 """Throughput of the block-scaled e4m3 Strassen-type product on one MI355X.
 
-One step = one fmm_matmul call: encode + quantize both operands, the T fp8
-sub-products with the fused W-combine, C written once; fp32 A and B are
-resident in HBM before the timed region.  Default workload: 8192^3, one
+One step = encode + quantize both operands, the T fp8 sub-products, the
+W-combine, C written once (fmm_encode, fmm_products, fmm_combine: together
+fmm_matmul); fp32 A and B are resident in HBM before the timed region.  Default workload: 8192^3, one
 level, the Phi-optimal realization T*, e4m3 block 32 along K, power-of-two
 (E8M0) block scales, A and B iid N(0,1) (synthetic, seeded).
 
 Prints one JSON line with the effective rate 2MNK / t, the relative RMS error
 of C against the fp64 product (measured after the timed region), the
-roofline of the dominant kernel (the sub-product GEMM, against the fp8 dense
-MFMA peak) with HIP-event kernel times taken on the launch stream, and the
-oracle timed on this host's cores on a bounded sample.
+roofline of the dominant kernel (the sub-product GEMM, fmm_products, against
+the fp8 dense MFMA peak) with HIP-event times of encode, products and combine
+taken on the launch stream, and the oracle timed on this host's cores on a
+bounded sample.
 """
 from __future__ import annotations
 
@@ -48,8 +49,54 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample", type=int, default=4096,
                    help="edge of the cubic products the oracle is timed on")
-    p.add_argument("--cpu-trials", type=int, default=2)
+    p.add_argument("--cpu-trials", type=int, default=6)
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="only run a plain 1 GiB device-to-device copy five times (the known-size "
+                        "kernel that scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     return p.parse_args()
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 28                                   # 2^28 floats = 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 5}))
+
+
+def recorded_traffic(kernel, size, args):
+    """HBM bytes per launch of the sub-product kernel from the committed counter
+    summary (profiles/), if it was taken on this workload and on the kernel
+    source as it is now; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{size}cube_depth{args.depth}_{args.realization}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for l in fh:
+            if l.startswith("- ") and ": " in l:
+                k, v = l[2:].split(": ", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    try:
+        if fields.get("kernel source sha256") != kernel_source_hash():
+            return None
+        return float(fields["HBM bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources of the sub-product kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_26077_amd", "csrc")
+    for name in ("kernels_gemm.hip", "kernels_split.hip", "lds_dma.h", "device.h", "internal.h"):
+        with open(os.path.join(csrc, name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def cpu_baseline(args):
@@ -88,6 +135,9 @@ def cpu_baseline(args):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the path has no cross-GPU step); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
@@ -95,7 +145,8 @@ def main():
 
     import torch
     import fmm_inputs as gen
-    from paper_2609_26077_amd import fmm_realization_metrics
+    from paper_2609_26077_amd import (FMM_LAYOUT_TILE256x64, fmm_operand_views,
+                                      fmm_realization_metrics)
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
 
     dev = torch.device("cuda:0")
@@ -114,19 +165,22 @@ def main():
     torch.cuda.synchronize(dev)
 
     # timed region: K whole steps, events around each launch on the launch stream
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
     for s in range(args.steps):
         ev[s][0].record(stream)
         f.encode(dA, dB, stream)
         ev[s][1].record(stream)
-        f.multiply(C, stream)
+        f.products(C, stream)
         ev[s][2].record(stream)
+        f.combine(C, stream)
+        ev[s][3].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
     enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    mul_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    prod_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    comb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
     ms_per_step = wall * 1e3 / args.steps
 
     # error of the last step's C against the fp64 product (not timed)
@@ -136,21 +190,29 @@ def main():
     del Cref
 
     real = f.real
-    R_, T = 0, 0
     from paper_2609_26077_amd import fmm_realization_terms
     R_, T = fmm_realization_terms(real, args.depth)
     phi = fmm_realization_metrics(real, args.depth)["phi"]
+    a_view, _ = fmm_operand_views(f.plan, f.ws)
+    split = a_view.code_layout == FMM_LAYOUT_TILE256x64
     mkn = 2.0 * M * N * K
     mfma_flop = mkn * T / 8.0 ** args.depth
     mp, kp, np_ = M // 2 ** args.depth, K // 2 ** args.depth, N // 2 ** args.depth
     sb = 4 if args.rule == "fp32_amax" else 1
     code_bytes = T * (mp + np_) * kp
     scale_bytes = T * (mp + np_) * (kp // args.block) * sb
-    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes
-    gemm_bytes = code_bytes + scale_bytes + 4 * M * N
+    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes * (2 if split else 1)
+    prod_bytes = T * mp * np_ * 4 if split else 4 * M * N
+    comb_bytes = prod_bytes + 4 * M * N if split else 0
     peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \
         else FP8_DENSE_PEAK_TFLOPS
-    achieved = mfma_flop / (mul_ms * 1e-3) / 1e12
+    achieved = mfma_flop / (prod_ms * 1e-3) / 1e12
+    traffic = recorded_traffic("gemm_tile256" if split else "gemm_mx_fast", M, args)
+
+    def hbm(nbytes, ms):
+        gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+        return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": gbs / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": nbytes}
 
     line = {
         "metric": METRIC,
@@ -171,21 +233,22 @@ def main():
                                + (", exact-dot" if args.exact_dot else ""),
                    "M": M, "K": K, "N": N, "depth": args.depth, "terms": T, "block": args.block,
                    "rule": args.rule, "realization": args.realization, "family": args.family,
-                   "exact_dot": bool(args.exact_dot)},
+                   "exact_dot": bool(args.exact_dot),
+                   "subproduct_path": "256x256 tiles + separate W-combine" if split
+                   else "128x128 tiles with the W-combine fused"},
         "rel_rms_error_vs_fp64": float(np.sqrt(rel_mse)),
         "rel_mse_vs_fp64": rel_mse,
-        "kernels_ms": {"encode": enc_ms, "multiply": mul_ms},
-        "roofline": {"bound": "mfma", "kernel": "sub-product GEMM (fmm_multiply)",
+        "kernels_ms": {"encode": enc_ms, "products": prod_ms, "combine": comb_ms},
+        "roofline": {"bound": "mfma", "kernel": "fp8 sub-product GEMM (fmm_products)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
-                     "algorithmic_flop_per_launch": mfma_flop},
-        "encode_roofline": {"bound": "hbm", "achieved": enc_bytes / (enc_ms * 1e-3) / 1e9,
-                            "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                            "frac": enc_bytes / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                            "algorithmic_bytes_per_launch": enc_bytes},
-        "gemm_compulsory_bytes": gemm_bytes,
+                     "frac": achieved / peak, "traffic": traffic,
+                     "algorithmic_flop_per_launch": mfma_flop,
+                     "algorithmic_bytes_per_launch": code_bytes + scale_bytes + prod_bytes},
+        "encode_roofline": hbm(enc_bytes, enc_ms),
         "device": torch.cuda.get_device_name(dev),
     }
+    if split:
+        line["combine_roofline"] = hbm(comb_bytes, comb_ms)
     if not args.no_cpu_baseline:
         del dA, dB, C
         torch.cuda.empty_cache()

@@ -106,8 +106,19 @@ typedef struct {
   int32_t flags;   /* FMM_FLAG_* bits; others must be 0 */
 } fmm_plan_desc;
 
+/* Layouts of the codes in a workspace (fmm_view.code_layout). */
+enum {
+  /* [batch][terms][rows][kdim], contracted axis last */
+  FMM_LAYOUT_ROWS = 0,
+  /* [batch][terms][rows / 256][kdim / 64][256][64]: 256-row x 64-byte tiles,
+   * each contiguous; inside a tile, 16-byte chunk c of tile row t sits at chunk
+   * c ^ ((t >> 2) & 3) of that row.  Used by plans whose sub-products run on
+   * 256 x 256 tiles (depth 1, E8M0 scales, M / 2 and N / 2 multiples of 256). */
+  FMM_LAYOUT_TILE256x64 = 1
+};
+
 /* Where the quantized operands of one side sit inside a workspace.
- * codes : uint8 e4m3 codes, [batch][terms][rows][kdim], contracted axis last
+ * codes : uint8 e4m3 codes in layout code_layout, contracted axis last
  *         (A side: rows = M / 2^l; B side: rows = N / 2^l, i.e. y_r transposed)
  * scales: [batch][terms][rows][kblocks], one per block; uint8 E8M0 (e + 127)
  *         when scale_bytes == 1, IEEE binary32 when scale_bytes == 4. */
@@ -116,7 +127,7 @@ typedef struct {
   void *scales;
   int64_t batch, terms, rows, kdim, kblocks;
   int32_t scale_bytes;
-  int32_t reserved;
+  int32_t code_layout; /* FMM_LAYOUT_* */
 } fmm_view;
 
 /* ---- realizations (host only; no device needed) ------------------------ */
@@ -181,10 +192,23 @@ int fmm_encode(const fmm_plan *p, const float *dA, const float *dB, void *dWs, v
 /* Pointers and extents of the quantized operands inside dWs (host call). */
 int fmm_operand_views(const fmm_plan *p, void *dWs, fmm_view *a, fmm_view *b);
 
-/* Steps "fp8 sub-products + W-combine": reads the encoded workspace and writes
- * C (batch x M x N fp32).  At depth >= 2 it also uses the workspace's
- * partial-product region. */
+/* Steps "fp8 sub-products + W-combine" (Algorithm 1, the products P_r of the
+ * quantized operands and C = sum_r w_r (x) P_r): reads the encoded workspace
+ * and writes C (batch x M x N fp32, 4-byte aligned).  Equal to fmm_products
+ * followed by fmm_combine on the same stream. */
 int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream);
+
+/* The first half of fmm_multiply: the T block-scaled fp8 sub-products with
+ * fp32 accumulation.  Plans with the large-tile layout (fmm_view.code_layout
+ * == FMM_LAYOUT_TILE256x64) write every P_r, fp32, to the workspace; the
+ * others fold the base-level w into the sub-product kernel and write C
+ * (depth 1) or the per-outer-term partial sums (depth >= 2, workspace). */
+int fmm_products(const fmm_plan *p, void *dWs, float *dC, void *stream);
+
+/* The second half of fmm_multiply: what remains of the W-combine after
+ * fmm_products (reads the workspace, writes C); nothing for the plans that
+ * fold it into the sub-product kernel at depth 1. */
+int fmm_combine(const fmm_plan *p, void *dWs, float *dC, void *stream);
 
 /* fmm_encode followed by fmm_multiply. */
 int fmm_matmul(const fmm_plan *p, const float *dA, const float *dB, float *dC, void *dWs,

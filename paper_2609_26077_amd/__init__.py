@@ -5,7 +5,7 @@ point it calls and forwards plain pointers and sizes.  Device memory and
 streams come from PyTorch (``torch.Tensor.data_ptr()``,
 ``torch.cuda.Stream.cuda_stream``); every computation runs in the library's
 HIP kernels.  Importing this module loads the library and fails loudly if it
-has not been built (run ``python -m paper_2609_26077_amd._build`` or
+has not been built (run ``python paper_2609_26077_amd/_build.py`` or
 ``__graft_entry__.build()``).
 """
 from __future__ import annotations
@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libfmm8.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(
         f"{LIB_PATH} is missing: the HIP library has not been built "
-        "(python -m paper_2609_26077_amd._build)")
+        f"(python {os.path.join(_HERE, '_build.py')})")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -43,6 +43,8 @@ BUILTINS = {"cubic8": FMM_CUBIC8, "strassen": FMM_STRASSEN, "winograd": FMM_WINO
             "tstar": FMM_TSTAR}
 
 FMM_FLAG_EXACT_DOT = 1
+FMM_LAYOUT_ROWS = 0
+FMM_LAYOUT_TILE256x64 = 1
 
 FMM_RULE_FP32_AMAX = 0
 FMM_RULE_POW2_CEIL = 1
@@ -66,7 +68,7 @@ class fmm_view(ctypes.Structure):
     _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p),
                 ("batch", ctypes.c_int64), ("terms", ctypes.c_int64), ("rows", ctypes.c_int64),
                 ("kdim", ctypes.c_int64), ("kblocks", ctypes.c_int64),
-                ("scale_bytes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("scale_bytes", ctypes.c_int32), ("code_layout", ctypes.c_int32)]
 
 
 _SIGS = {
@@ -87,6 +89,8 @@ _SIGS = {
     "fmm_operand_views": (ctypes.c_int, [_vp, _vp, ctypes.POINTER(fmm_view),
                                          ctypes.POINTER(fmm_view)]),
     "fmm_multiply": (ctypes.c_int, [_vp, _vp, _vp, _vp]),
+    "fmm_products": (ctypes.c_int, [_vp, _vp, _vp, _vp]),
+    "fmm_combine": (ctypes.c_int, [_vp, _vp, _vp, _vp]),
     "fmm_matmul": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp]),
     "fmm_plan_destroy": (None, [_vp]),
     "fmm_reference_f64": (ctypes.c_int, [_i64, _i64, _i64, _i64, _vp, _vp, _vp, _vp]),
@@ -297,6 +301,14 @@ def fmm_operand_views(p: Plan, ws):
 
 def fmm_multiply(p: Plan, ws, C, stream=None) -> None:
     _check(_lib.fmm_multiply(p.handle, _ptr(ws), _ptr(C), _stream(stream)), "fmm_multiply")
+
+
+def fmm_products(p: Plan, ws, C, stream=None) -> None:
+    _check(_lib.fmm_products(p.handle, _ptr(ws), _ptr(C), _stream(stream)), "fmm_products")
+
+
+def fmm_combine(p: Plan, ws, C, stream=None) -> None:
+    _check(_lib.fmm_combine(p.handle, _ptr(ws), _ptr(C), _stream(stream)), "fmm_combine")
 
 
 def fmm_matmul(p: Plan, A, B, C, ws, stream=None) -> None:

@@ -14,12 +14,15 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 SOURCES = ["realization.cpp", "plan.cpp", "kernels_encode.hip", "kernels_gemm.hip",
-           "kernels_measure.hip"]
+           "kernels_split.hip", "kernels_measure.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
           "-Wno-unused-function", "-Wno-unused-variable"]
 DEVICE = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-munsafe-fp-atomics", "-mllvm", "-amdgpu-mfma-vgpr-form"]
+          "-munsafe-fp-atomics"]
+# the 128 x 128 kernels keep the MFMA accumulator in VGPRs (the AGPRs hold the
+# W-combine quadrants); the 256 x 256 kernel keeps its 256 accumulators in AGPRs
+PER_FILE = {"kernels_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
@@ -27,7 +30,7 @@ def _compile(src: str) -> str:
     obj = os.path.join(OBJ, src + ".o")
     cmd = [HIPCC] + COMMON
     if src.endswith(".hip"):
-        cmd += ["-x", "hip"] + DEVICE
+        cmd += ["-x", "hip"] + DEVICE + PER_FILE.get(src, [])
     else:
         cmd += ["-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROCM, "include")]
     cmd += ["-c", path, "-o", obj]

@@ -10,6 +10,7 @@ namespace fmm {
 
 constexpr int kMaxRank = 8;    // <2,2,2;R>, R <= 8 (cubic has 8 terms)
 constexpr int kMaxDepth = 3;
+constexpr int kSplitTile = 256; // tile edge of the large-tile sub-product path
 
 struct Realization {
   int R;
@@ -47,11 +48,14 @@ struct Problem {
   int64_t kblocks;         // kp / block
   int scale_bytes;         // 1 (E8M0) or 4 (fp32)
   int exact_dot;           // FMM_FLAG_EXACT_DOT requested
+  int split;               // large-tile sub-products + separate W-combine (depth 1, tile-aligned MX)
 };
 
 // Layout of a workspace: byte offsets from its base.
 struct Workspace {
   size_t a_codes, b_codes, a_scales, b_scales, partial, total;
+  // split path only: K-block-major scale copies and the fp32 sub-products
+  size_t a_scales_t, b_scales_t, products;
 };
 
 // Device copies of the plan's tables (one allocation).
@@ -60,14 +64,23 @@ struct DeviceTables {
   const CoefEntry *a_ent;
   const int32_t *b_off;
   const CoefEntry *b_ent;
-  const float *w_inner;        // R x 4 fp32 base w (the inner-level decoder)
+  const float *w_inner;        // R x 4 fp32 base w (the inner-level decoder), zero-padded to kMaxRank x 4
   const float *w_outer;        // To x 4^(l-1) fp32 flattened depth-(l-1) w (depth >= 2)
 };
 
 // ---- launchers (kernels_*.hip); return a hipError_t as int ---------------
 int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
                   uint8_t *ws, const Workspace &wl, void *stream);
-int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl, float *C, void *stream);
+// sub-products (split plans: into the product region; otherwise with the fused
+// inner W-combine, into C at depth 1 or the partial region at depth >= 2)
+int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
+                    float *C, void *stream);
+// what remains of the W-combine after launch_products (nothing for fused depth-1 plans)
+int launch_combine(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
+                   float *C, void *stream);
+int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace &wl, void *stream);
+int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
+                         float *C, void *stream);
 int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *A,
                          const float *B, double *Cref, void *stream);
 size_t error_stats_scratch_bytes(int64_t batch, int64_t M, int64_t N);

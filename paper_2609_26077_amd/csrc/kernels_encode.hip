@@ -44,7 +44,7 @@ template <int SIDE, int DEPTH>
 __global__ __launch_bounds__(kThreads) void encode_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
-    int64_t tiles_l) {
+    uint8_t *__restrict__ scales_t, int64_t tiles_l) {
   using TT = Tile<DEPTH>;
   constexpr int TR = TT::TR;
   constexpr int NB = TT::nblk;
@@ -145,13 +145,27 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
     const int64_t l = l0 + 4 * c4;
     if (p < rows && l < kp) {
       const int64_t rowid = (bt * T + r) * rows + p;
-      *reinterpret_cast<uint32_t *>(codes + rowid * kp + l) = w;
+      int64_t at = rowid * kp + l;
+      if (scales_t) {
+        // tiled codes of the large-tile path: 256-row x 64-byte tiles, each the
+        // LDS image the GEMM copies (chunk c of tile row t at c ^ ((t >> 2) & 3))
+        const int64_t t = p & 255, c = (l >> 4) & 3;
+        at = ((((bt * T + r) * (rows >> 8) + (p >> 8)) * (kp >> 6) + (l >> 6)) << 14) + t * 64 +
+             16 * (c ^ ((t >> 2) & 3)) + (l & 15);
+      }
+      *reinterpret_cast<uint32_t *>(codes + at) = w;
       if ((c4 % gl) == 0) {
         const int64_t kb = l / pb.block;
         if (pb.scale_bytes == 1)
           scales[rowid * kb_count + kb] = (uint8_t)sc.stored;
         else
           reinterpret_cast<uint32_t *>(scales)[rowid * kb_count + kb] = sc.stored;
+        if (scales_t) {
+          // K-block-major copy for the large-tile path, rows permuted inside each
+          // 256-row tile: row 128 wm + 32 i + r at byte 4 (32 wm + r) + i
+          const int64_t pt = (p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3));
+          scales_t[((bt * T + r) * kb_count + kb) * rows + pt] = (uint8_t)sc.stored;
+        }
       }
     }
   };
@@ -181,23 +195,25 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
 
 template <int SIDE, int DEPTH>
 hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
-                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
+                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, uint8_t *scales_t,
+                       hipStream_t st) {
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
   const int64_t tiles_r = (rows + Tile<DEPTH>::TR - 1) / Tile<DEPTH>::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
   hipLaunchKernelGGL((encode_kernel<SIDE, DEPTH>), grid, dim3(kThreads), 0, st, src, pb, off,
-                     ent, codes, scales, tiles_l);
+                     ent, codes, scales, scales_t, tiles_l);
   return hipGetLastError();
 }
 
 template <int SIDE>
 hipError_t launch_depth(const Problem &pb, const float *src, const int32_t *off,
-                        const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
+                        const CoefEntry *ent, uint8_t *codes, uint8_t *scales, uint8_t *scales_t,
+                        hipStream_t st) {
   switch (pb.depth) {
-    case 1: return launch_side<SIDE, 1>(pb, src, off, ent, codes, scales, st);
-    case 2: return launch_side<SIDE, 2>(pb, src, off, ent, codes, scales, st);
-    case 3: return launch_side<SIDE, 3>(pb, src, off, ent, codes, scales, st);
+    case 1: return launch_side<SIDE, 1>(pb, src, off, ent, codes, scales, scales_t, st);
+    case 2: return launch_side<SIDE, 2>(pb, src, off, ent, codes, scales, scales_t, st);
+    case 3: return launch_side<SIDE, 3>(pb, src, off, ent, codes, scales, scales_t, st);
   }
   return hipErrorInvalidValue;
 }
@@ -208,9 +224,11 @@ int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, co
                   uint8_t *ws, const Workspace &wl, void *stream) {
   if (pb.batch == 0 || pb.M == 0 || pb.N == 0 || pb.K == 0) return hipSuccess;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = launch_depth<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, st);
+  uint8_t *at = pb.split ? ws + wl.a_scales_t : nullptr;
+  uint8_t *btp = pb.split ? ws + wl.b_scales_t : nullptr;
+  hipError_t e = launch_depth<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, at, st);
   if (e != hipSuccess) return e;
-  return launch_depth<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, st);
+  return launch_depth<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, btp, st);
 }
 
 }  // namespace fmm

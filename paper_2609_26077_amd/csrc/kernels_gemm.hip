@@ -31,6 +31,7 @@
 
 #include "device.h"
 #include "internal.h"
+#include "lds_dma.h"
 
 namespace fmm {
 
@@ -65,8 +66,13 @@ struct GemmArgs {
   const float *w;                // R x 4 inner decoder weights (device)
 };
 
-// LDS tile: 128 rows x 128 bytes; 16-byte chunk c of row r sits at chunk c ^ (r & 7)
-__device__ __forceinline__ int swz(int row, int chunk) { return row * BK + 16 * (chunk ^ (row & 7)); }
+// LDS tile: 128 rows x 128 bytes; 16-byte chunk c of row r sits at chunk
+// c ^ (r & 7) ^ ((r >> 3) & 1).  A 16-byte read is served in groups of 16
+// lanes over 64 four-byte banks; the fragment rows r and r + 8 of one group
+// would share banks under c ^ (r & 7) alone.
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * BK + 16 * (chunk ^ (row & 7) ^ ((row >> 3) & 1));
+}
 
 // Global -> registers for one (term, k-step): each thread moves four 16-byte chunks
 // of A and four of B.  Rows past the end and chunks past kp read as zero.
@@ -265,23 +271,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_kernel(GemmArgs g) {
 // One workgroup of four waves owns a 128 x 128 tile of the m' x n' grid; each
 // wave a 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  The codes and E8M0
 // scales of each 128-byte K step go from HBM straight into LDS
-// (global_load_lds: no staging registers) through a three-slot ring, two
-// steps ahead of the step being multiplied; each wave issues exactly nine
-// such transfers per step (four 1 KB of A codes, four of B codes, one 256 B of
-// scales) and waits for them with an explicit vmcnt, so the steady state holds
-// two steps of loads in flight.  LDS code rows are 128 bytes with 16-byte
-// chunk c stored at c ^ (row & 7) (conflict-free fragment reads).
+// (global_load_lds: no staging registers) through a four-slot ring; each wave
+// issues exactly nine such transfers per step (four 1 KB of A codes, four of
+// B codes, one 256 B of scales) and waits for them with an explicit vmcnt.
+// While the MFMAs of step s run on fragments already in registers, the
+// fragments of step s + 1 are read from LDS into a second register set and the
+// transfers of steps s + 2 and s + 3 are in flight.  LDS code rows are 128
+// bytes; 16-byte chunk c of row r is stored at c ^ (r & 7) ^ ((r >> 3) & 1),
+// which keeps every 16-lane group of a fragment read on distinct banks.
 //
 // The quadrant accumulators of the fused W-combine live in AGPRs for the
 // whole kernel (the four 64 x 64 sets fill the 256 accumulation registers),
-// leaving the architectural VGPRs to the MFMA accumulator, the operand
-// fragments and addressing; they are touched only through the helpers below.
+// leaving the architectural VGPRs to the MFMA accumulator, the two fragment
+// sets and addressing; they are touched only through the helpers below.  The
+// decoder weights are copied to LDS once, so the term-end combine never waits
+// on vector memory (which would drain the transfer ring).
 // ---------------------------------------------------------------------------
 constexpr int FBK = 128;
 constexpr int kSlot = 2 * BM * FBK + 2 * BM * 4;   // codes A, B + scale words A, B
-constexpr int kSlots = 3;
+constexpr int kSlots = 4;
 
-typedef __attribute__((address_space(3))) uint8_t lds_u8;
+using dma::copy16;
+using dma::copy4;
+using dma::wait_vmcnt;
 
 __device__ __forceinline__ void agpr_zero(float &q) {
   asm volatile("v_accvgpr_write_b32 %0, 0" : "=a"(q));
@@ -299,21 +311,6 @@ __device__ __forceinline__ float agpr_read(const float &q) {
   float v;
   asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(q));
   return v;
-}
-
-// One wave-wide transfer HBM -> LDS: lane l moves 16 (or 4) bytes from
-// base + off to LDS byte m0 + 16 l (or 4 l).
-__device__ __forceinline__ void dma16(uint32_t off, const uint8_t *base, uint32_t m0) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(m0)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void dma4(uint32_t off, const uint8_t *base, uint32_t m0) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "s"(m0)
-               : "memory", "m0");
-}
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // XCD-aware tile order: workgroups are dispatched round-robin over the eight
@@ -334,11 +331,19 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int &
   tn = in / gm;
 }
 
+// Operands of one K step for one wave: fragments [substep s][tile i] and the
+// raw E8M0 scale word (four K blocks) of each of its A and B row tiles.
+struct MxFrags {
+  v8i a[2][2], b[2][2];
+  uint32_t wa[2], wb[2];
+};
+
 template <int BS>
 __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, int tiles_m) {
   __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+  __shared__ float lds_w[4 * kMaxRank];
   uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
-  const uint32_t lds_base = (uint32_t)(uintptr_t)(lds_u8 *)lds_raw;
+  const uint32_t lds_base = dma::lds_addr(lds_raw);
   const int t = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int lane = t & 63;
@@ -352,30 +357,58 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
   const int nk = (int)(g.kp / FBK);
   const int total = g.R * nk;
   const int wrow_a = wm * 64, wrow_b = wn * 64;
+  if (t == 0) {   // uniform loads of the zero-padded table; read only after the first barrier
+#pragma unroll
+    for (int i = 0; i < 4 * kMaxRank; ++i) lds_w[i] = g.w[i];
+  }
 
-  // per-lane DMA offsets: code region of 8 rows x 128 B, lane -> (row l/8, chunk (l%8) ^ (l/8))
-  const uint32_t code_off = (uint32_t)(lane >> 3) * kp + 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+  // per-lane DMA offsets into a region of 8 rows x 128 B: lane l fills LDS row
+  // l / 8, chunk l % 8, which holds global chunk (l % 8) ^ (l / 8) ^ (region & 1)
+  const uint32_t code_off0 = (uint32_t)(lane >> 3) * kp + 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+  const uint32_t code_off1 = code_off0 ^ 16u;
   // scale words: wave 0/1 -> A rows 64w.., wave 2/3 -> B rows 64(w-2)..
   const int srow = (wave & 1) * 64 + lane;
   const uint32_t scale_off = (uint32_t)srow * kblocks;
   const bool scale_is_b = wave >= 2;
 
-  auto issue = [&](int ri, int ks, int slot) {
+  auto issue = [&](int step) {
+    const int ri = step / nk, ks = step - ri * nk;
     const int64_t r = ro * g.R + ri;
     const uint32_t k0 = (uint32_t)ks * FBK;
     const uint8_t *xa = g.xa + ((bt * g.T + r) * g.mp + pm0) * g.kp + k0;
     const uint8_t *xb = g.xb + ((bt * g.T + r) * g.np + pn0) * g.kp + k0;
-    const uint32_t m0 = lds_base + (uint32_t)slot * kSlot;
+    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int region = wave * 4 + j;                     // rows 8 region .. +8
-      dma16(code_off, xa + (int64_t)region * 8 * g.kp, m0 + region * 1024);
-      dma16(code_off, xb + (int64_t)region * 8 * g.kp, m0 + BM * FBK + region * 1024);
+      const uint32_t off = (j & 1) ? code_off1 : code_off0;
+      copy16(off, xa + (int64_t)region * 8 * g.kp, m0 + region * 1024);
+      copy16(off, xb + (int64_t)region * 8 * g.kp, m0 + BM * FBK + region * 1024);
     }
     const uint8_t *sbase = scale_is_b ? g.sb + ((bt * g.T + r) * g.np + pn0) * g.kblocks
                                       : g.sa + ((bt * g.T + r) * g.mp + pm0) * g.kblocks;
     const uint32_t kw = BS == 32 ? k0 / 32 : (k0 / 128) & ~3u;   // 4-byte aligned word
-    dma4(scale_off + kw, sbase, m0 + 2 * BM * FBK + (scale_is_b ? BM * 4 : 0) + (wave & 1) * 256);
+    copy4(scale_off + kw, sbase, m0 + 2 * BM * FBK + (scale_is_b ? BM * 4 : 0) + (wave & 1) * 256);
+  };
+
+  // LDS -> registers for one step (slot step % 4; any step index reads in bounds)
+  auto load = [&](int step, MxFrags &f) {
+    const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *lb = la + BM * FBK;
+    const uint32_t *lsa = reinterpret_cast<const uint32_t *>(la + 2 * BM * FBK);
+    const uint32_t *lsb = lsa + BM;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      f.wa[i] = lsa[wrow_a + 32 * i + r32];
+      f.wb[i] = lsb[wrow_b + 32 * i + r32];
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        f.a[s][i] = frag_mx(la, wrow_a + 32 * i + r32, s, h);
+        f.b[s][i] = frag_mx(lb, wrow_b + 32 * i + r32, s, h);
+      }
   };
 
   v16f acc[2][2];
@@ -391,66 +424,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
         for (int e = 0; e < 16; ++e) agpr_zero(quad[q][i][j][e]);
     }
 
-  // prologue: steps 0 and 1 in flight
-  int ri_l = 0, ks_l = 0;            // next step to issue
-  auto advance = [&](int &ri, int &ks) {
-    if (++ks == nk) { ks = 0; ++ri; }
-  };
-  issue(ri_l, ks_l, 0);
-  advance(ri_l, ks_l);
-  if (total > 1) {
-    issue(ri_l, ks_l, 1);
-    advance(ri_l, ks_l);
-  }
-
-  int ri = 0, ks = 0, slot = 0;
-  for (int it = 0; it < total; ++it) {
-    if (it + 1 < total) wait_vmcnt<9>(); else wait_vmcnt<0>();
-    __syncthreads();
-    if (it + 2 < total) {
-      issue(ri_l, ks_l, slot == 0 ? 2 : slot - 1);
-      advance(ri_l, ks_l);
+  // one step: wait for step + 1, start step + 3, read step + 1 into `nxt`
+  // while the MFMAs of `cur` (step) run, and at the end of a term fold P_r
+  // into the quadrants.  The scale bytes of `cur` are selected here, a step after
+  // their words were read, so no MFMA waits on a scale read.
+  auto body = [&](int step, MxFrags &cur, MxFrags &nxt) {
+    if (step + 1 < total) {
+      if (step + 2 < total) wait_vmcnt<9>(); else wait_vmcnt<0>();
+      __syncthreads();
     }
-    const uint8_t *la = lds + slot * kSlot;
-    const uint8_t *lb = la + BM * FBK;
-    const uint32_t *lsa = reinterpret_cast<const uint32_t *>(la + 2 * BM * FBK);
-    const uint32_t *lsb = lsa + BM;
-    int sA[2], sB[2];
+    if (step + 3 < total) issue(step + 3);
+    const int ks = step % nk;
+    const int sh = BS == 32 ? 8 * h : 8 * (ks & 3);   // block 2s + h at byte 2s / block ks % 4 at byte 0
+    int sa[2], sb[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const uint32_t wa = lsa[wrow_a + 32 * i + r32];
-      const uint32_t wb = lsb[wrow_b + 32 * i + r32];
-      if (BS == 32) {           // block 2s + h of this step at byte 2s after the shift
-        sA[i] = (int)(wa >> (8 * h));
-        sB[i] = (int)(wb >> (8 * h));
-      } else {                  // one block per step: byte ks % 4 of the word
-        sA[i] = (int)(wa >> (8 * (ks & 3)));
-        sB[i] = (int)(wb >> (8 * (ks & 3)));
-      }
+      sa[i] = (int)(cur.wa[i] >> sh);
+      sb[i] = (int)(cur.wb[i] >> sh);
     }
+    load(step + 1, nxt);
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      v8i fa[2], fb[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        fa[i] = frag_mx(la, wrow_a + 32 * i + r32, s, h);
-        fb[i] = frag_mx(lb, wrow_b + 32 * i + r32, s, h);
-      }
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           if (BS == 32 && s == 1)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0, 2, sA[i], 2, sB[j]);
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[s][i], cur.b[s][j], acc[i][j],
+                                                                          0, 0, 2, sa[i], 2, sb[j]);
           else
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], 0, 0, 0, sA[i], 0, sB[j]);
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[s][i], cur.b[s][j], acc[i][j],
+                                                                          0, 0, 0, sa[i], 0, sb[j]);
         }
+    // MFMA and LDS reads alternate: 1 MFMA, then 3 reads (20 reads over 7 gaps)
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     if (ks + 1 == nk) {
+      const int ri = step / nk;
       // end of term ri: quadrant q += w[ri][q] * P
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float wq = g.w[4 * ri + q];
+        const float wq = __builtin_bit_cast(
+            float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, lds_w[4 * ri + q])));
         if (wq != 0.0f) {
 #pragma unroll
           for (int i = 0; i < 2; ++i)
@@ -465,8 +486,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
     }
-    advance(ri, ks);
-    slot = slot == 2 ? 0 : slot + 1;
+  };
+
+  // prologue: steps 0, 1, 2 in flight, step 0 read into registers
+  issue(0);
+  if (total > 1) issue(1);
+  if (total > 2) issue(2);
+  if (total > 2) wait_vmcnt<18>(); else if (total > 1) wait_vmcnt<9>(); else wait_vmcnt<0>();
+  __syncthreads();
+  MxFrags f0, f1;
+  load(0, f0);
+  for (int step = 0; step < total; step += 2) {
+    body(step, f0, f1);
+    if (step + 1 < total) body(step + 1, f1, f0);
   }
 
 #pragma unroll
@@ -655,9 +687,10 @@ __global__ __launch_bounds__(256) void outer_combine_kernel(const float *__restr
 
 }  // namespace
 
-int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *ws,
+int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *ws,
                     const Workspace &wl, float *C, void *stream) {
   if (pb.batch == 0 || pb.M == 0 || pb.N == 0) return hipSuccess;
+  if (pb.split) return launch_products_split(pb, ws, wl, stream);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   GemmArgs g;
   g.xa = ws + wl.a_codes;
@@ -684,14 +717,22 @@ int launch_multiply(const Problem &pb, const DeviceTables &tab, const uint8_t *w
     hipLaunchKernelGGL(gemm_mx_kernel, grid, dim3(kThreads), 0, st, g);
   else
     hipLaunchKernelGGL(gemm_promote_kernel, grid, dim3(kThreads), 0, st, g, pb.scale_bytes);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || pb.depth == 1) return e;
+  return hipGetLastError();
+}
+
+int launch_combine(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
+                   float *C, void *stream) {
+  if (pb.batch == 0 || pb.M == 0 || pb.N == 0) return hipSuccess;
+  if (pb.split) return launch_combine_split(pb, tab, ws, wl, C, stream);
+  if (pb.depth == 1) return hipSuccess;     // fused into the sub-product kernel
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const float *Q = reinterpret_cast<const float *>(ws + wl.partial);
   const int64_t npos = pb.mp * pb.np;
   const dim3 g2((unsigned)((npos + 255) / 256), 4, (unsigned)pb.batch);
   if (pb.depth == 2)
-    hipLaunchKernelGGL(outer_combine_kernel<4>, g2, dim3(256), 0, st, g.out, tab.w_outer, C, pb);
+    hipLaunchKernelGGL(outer_combine_kernel<4>, g2, dim3(256), 0, st, Q, tab.w_outer, C, pb);
   else
-    hipLaunchKernelGGL(outer_combine_kernel<16>, g2, dim3(256), 0, st, g.out, tab.w_outer, C, pb);
+    hipLaunchKernelGGL(outer_combine_kernel<16>, g2, dim3(256), 0, st, Q, tab.w_outer, C, pb);
   return hipGetLastError();
 }
 

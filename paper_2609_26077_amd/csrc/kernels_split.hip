@@ -1,0 +1,306 @@
+// Large-tile sub-products for tile-aligned block-scaled problems at depth 1.
+//
+// The sub-products are the dominant cost; each is a plain block-scaled fp8
+// GEMM P_r = A_r B_r^T with fp32 accumulation.  A 256 x 256 tile of P_r
+// halves the operand bytes per MFMA flop of a 128 x 128 tile, which is what
+// bounds the feed from L2 into LDS; the price is that P_r leaves the
+// workgroup, so the W-combine becomes its own bandwidth-bound pass:
+//
+//   1. gemm_tile256_kernel: one workgroup per (batch, term r, 256 x 256 tile),
+//      eight waves of 128 x 64 (4 x 2 MFMA tiles of 32 x 32, 128 accumulation
+//      registers each), two per SIMD, run in alternating phases so that one
+//      wave's MFMAs cover the other's LDS reads; 64-byte K steps through a
+//      four-slot LDS ring filled by global_load_lds three steps ahead; P_r is
+//      stored in fp32.
+//   2. combine1_kernel: C block (i, k) = sum_r w[r][2k + i] P_r, ascending r,
+//      one fused multiply-add per nonzero weight (the order of the fused
+//      W-combine of the 128 x 128 path).
+//
+// Scales come from the encoder's second, K-block-major copy: for each
+// (term, K block) the E8M0 bytes of all rows, permuted inside every 256-row
+// tile so that row 128 wm + 32 i + r sits at byte 4 (32 wm + r) + i.  One
+// 32-bit LDS read then gives a lane the scales of its four A row tiles (or,
+// shifted by 16 (wn & 1) bits, of its two B row tiles), and the MFMA's op_sel
+// picks the byte of each tile.
+#include <hip/hip_runtime.h>
+
+#include "device.h"
+#include "internal.h"
+#include "lds_dma.h"
+
+namespace fmm {
+
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int TT = kSplitTile;        // tile edge in rows of A_r and of B_r
+constexpr int SK = 64;                // contracted bytes per step
+constexpr int kThreads = 512;
+constexpr int kSlots = 4;
+constexpr int kCode = TT * SK;        // 16 KB of codes per operand per step
+constexpr int kScale = 2 * TT;        // two K blocks x 256 rows of scale bytes per operand
+constexpr int kSlot = 2 * kCode + 2 * kScale;
+
+struct SplitArgs {
+  const uint8_t *xa, *xb;      // codes [batch][T][rows / 256][kp / 64][256 x 64 tile image]
+  const uint8_t *sat, *sbt;    // scales [batch][T][kblocks][rows] (rows permuted per tile)
+  float *P;                    // products [batch][T][mp][np]
+  int64_t mp, np, kp, kblocks, T;
+  int tiles_m, tiles_n;
+};
+
+// LDS tile of one operand: 256 rows x 64 bytes; 16-byte chunk c of row r sits
+// at chunk c ^ ((r >> 2) & 3), so the 16 rows of a 16-lane fragment read fall
+// on 16 distinct bank groups of the 64 banks.  The encoder writes the codes of
+// these plans in exactly this image, one contiguous 16 KB block per
+// (term, 256-row tile, 64-byte k-step).
+__device__ __forceinline__ int swz64(int row, int chunk) {
+  return row * SK + 16 * (chunk ^ ((row >> 2) & 3));
+}
+
+// 32 rows x 64 bytes of one operand for v_mfma_scale_f32_32x32x64_f8f6f4:
+// lane (r, h) holds bytes [16h, 16h+16) and [32+16h, 32+16h+16) of row r.
+__device__ __forceinline__ v8i frag64(const uint8_t *lt, int row, int h) {
+  const uint4 lo = *reinterpret_cast<const uint4 *>(lt + swz64(row, h));
+  const uint4 hi = *reinterpret_cast<const uint4 *>(lt + swz64(row, 2 + h));
+  v8i f;
+  f[0] = (int)lo.x; f[1] = (int)lo.y; f[2] = (int)lo.z; f[3] = (int)lo.w;
+  f[4] = (int)hi.x; f[5] = (int)hi.y; f[6] = (int)hi.z; f[7] = (int)hi.w;
+  return f;
+}
+
+struct Frags {
+  v8i a[4], b[2];
+  uint32_t sa, sb;     // scale bytes of the row tiles (byte i = A tile i, byte j = B tile j)
+};
+
+// Work order: workgroups are dispatched round-robin over the eight XCDs, so
+// the ids of one XCD (bid, bid + 8, ...) are given a contiguous range of work
+// items; items run term-major, and the tiles of a term in groups of eight
+// tile-rows, so the workgroups resident on an XCD share A and B rows in L2.
+__device__ __forceinline__ void work_of(int bid, int64_t nitems, int64_t T, int tiles_m, int tiles_n,
+                                        int64_t &bt, int64_t &r, int &tm, int &tn) {
+  int64_t id = bid;
+  if ((nitems & 7) == 0) id = (int64_t)(bid & 7) * (nitems >> 3) + (bid >> 3);
+  const int64_t ntiles = (int64_t)tiles_m * tiles_n;
+  bt = id / (T * ntiles);
+  const int64_t rem = id - bt * T * ntiles;
+  r = rem / ntiles;
+  const int tile = (int)(rem - r * ntiles);
+  constexpr int GM = 8;
+  const int per_group = GM * tiles_n;
+  const int group = tile / per_group;
+  const int first_m = group * GM;
+  const int gm = min(tiles_m - first_m, GM);
+  const int in = tile - group * per_group;
+  tm = first_m + in % gm;
+  tn = in / gm;
+}
+
+template <int BS>
+__global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(SplitArgs g) {
+  __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+  const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
+  const uint32_t lds_base = dma::lds_addr(lds_raw);
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = wave >> 2, wn = wave & 3;       // A rows 128 wm.., B rows 64 wn..
+  const int r32 = lane & 31, h = lane >> 5;
+  const int64_t nitems = (int64_t)gridDim.x;
+  int64_t bt, r;
+  int tm, tn;
+  work_of(blockIdx.x, nitems, g.T, g.tiles_m, g.tiles_n, bt, r, tm, tn);
+  const int64_t pm0 = (int64_t)tm * TT, pn0 = (int64_t)tn * TT;
+  const int nk = (int)(g.kp / SK);
+  // codes arrive tiled: the 16 KB image of (tile, k-step) is contiguous, so a
+  // transfer is a straight 1 KB copy (lane l moves bytes 16 l .. 16 l + 15)
+  const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kCode;
+  const uint8_t *xb = g.xb + ((bt * g.T + r) * g.tiles_n + tn) * (int64_t)nk * kCode;
+  const uint32_t code_off = 16u * (uint32_t)lane;
+  // scale transfer of this wave: operand (wave & 3) / 2 (A, B), K block
+  // 2 step + (wave & 1) (block 32) or step / 2 (block 128); waves w and w + 4,
+  // and at block 128 also w and w + 1, move the same bytes
+  const bool s_is_b = (wave & 3) >= 2;
+  const int seg = BS == 32 ? (wave & 1) : 0;
+  const int64_t srows = s_is_b ? g.np : g.mp;
+  const uint8_t *sbase = s_is_b ? g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0
+                                : g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0;
+
+  auto issue = [&](int step) {
+    const int64_t src = (int64_t)step * kCode;
+    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int region = wave * 2 + j;             // 1 KB = tile rows 16 region .. + 15
+      dma::copy16(code_off, xa + src + region * 1024, m0 + region * 1024);
+      dma::copy16(code_off, xb + src + region * 1024, m0 + kCode + region * 1024);
+    }
+    const int64_t kb = BS == 32 ? 2 * (int64_t)step + seg : step / 2;
+    dma::copy4(4u * (uint32_t)lane, sbase + kb * srows,
+               m0 + 2 * kCode + (s_is_b ? kScale : 0) + seg * TT);
+  };
+
+  // LDS -> registers for one step (slot step % 4; any step index reads in bounds)
+  auto load = [&](int step, Frags &f) {
+    const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *lb = la + kCode;
+    const int sseg = BS == 32 ? h * TT : 0;     // block 2 step + h, or step / 2
+    f.sa = *reinterpret_cast<const uint32_t *>(la + 2 * kCode + sseg + 4 * (wm * 32 + r32));
+    // B row 64 wn + 32 j + r is row 128 (wn / 2) + 32 (2 (wn & 1) + j) + r of the tile
+    f.sb = *reinterpret_cast<const uint32_t *>(la + 2 * kCode + kScale + sseg + 4 * ((wn >> 1) * 32 + r32)) >>
+           (16 * (wn & 1));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.a[i] = frag64(la, wm * 128 + 32 * i + r32, h);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) f.b[j] = frag64(lb, wn * 64 + 32 * j + r32, h);
+  };
+
+  v16f acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+
+  auto mfma = [&](const Frags &f) {
+#define FMM_MFMA_IJ(I, J)                                                                     \
+  acc[I][J] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(f.a[I], f.b[J], acc[I][J], 0, 0, \
+                                                              I, (int)f.sa, J, (int)f.sb)
+    FMM_MFMA_IJ(0, 0); FMM_MFMA_IJ(0, 1); FMM_MFMA_IJ(1, 0); FMM_MFMA_IJ(1, 1);
+    FMM_MFMA_IJ(2, 0); FMM_MFMA_IJ(2, 1); FMM_MFMA_IJ(3, 0); FMM_MFMA_IJ(3, 1);
+#undef FMM_MFMA_IJ
+  };
+
+  // Two phases per step, separated by barriers.  Waves w and w + 4 share a
+  // SIMD and sit in different groups: in every phase one group reads a
+  // step's fragments from LDS while the other runs its MFMAs on the fragments
+  // it read in the phase before, so each SIMD always has a wave issuing MFMAs.
+  //   phase 2s:     group 0 reads step s;   group 1 multiplies step s - 1
+  //   phase 2s + 1: group 0 multiplies s;   group 1 reads step s
+  // Steps 0, 1, 2 are in flight at the start; at phase 2s every wave waits for
+  // its own transfers of step s (five a step) and, after the barrier, starts
+  // step s + 3 into the slot of step s - 1, which group 1 finished reading in
+  // phase 2s - 1.
+  // Every wave runs the same sequence (phase, read s, phase, multiply s);
+  // group 1 starts one phase late and group 0 ends one phase late, so both
+  // pass 2 nk + 1 barriers.  An even phase 2s begins with the wait for the
+  // wave's own transfers of step s (five a step) and, after its barrier,
+  // starts step s + 3.
+  auto phase = [&](int ph) {
+    if ((ph & 1) == 0) {
+      const int s = ph >> 1;
+      if (s + 2 < nk) dma::wait_vmcnt<10>(); else if (s + 1 < nk) dma::wait_vmcnt<5>(); else dma::wait_vmcnt<0>();
+    }
+    __syncthreads();
+    if ((ph & 1) == 0 && (ph >> 1) + 3 < nk) issue((ph >> 1) + 3);
+  };
+  const int grp = wave >> 2;
+  issue(0);
+  if (nk > 1) issue(1);
+  if (nk > 2) issue(2);
+  int ph = 0;
+  if (grp == 1) phase(ph++);
+  for (int step = 0; step < nk; ++step) {
+    Frags f;
+    phase(ph++);
+    load(step, f);
+    phase(ph++);
+    mfma(f);
+  }
+  if (grp == 0) phase(ph++);
+
+  // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32
+  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 128) * g.np + pn0 + wn * 64 + r32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+        out[(int64_t)row * g.np + 32 * j] = acc[i][j][e];
+      }
+}
+
+// C block (i, k) of batch element bt, rows i m' + p, columns k n' + 4 q4 .. + 3:
+//   sum over r of w[r][2k + i] P_r[p][4 q4 ..], ascending r, fma per nonzero weight.
+template <bool VEC>
+__global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__ P, const float *__restrict__ w,
+                                                       float *__restrict__ C, Problem pb) {
+  const int64_t n4 = pb.np / 4;
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // p * n4 + q4
+  const int64_t bt = blockIdx.y;
+  if (pos >= pb.mp * n4) return;
+  const int64_t p = pos / n4, q4 = pos - p * n4;
+  float wr[kMaxRank][4];
+#pragma unroll
+  for (int r = 0; r < kMaxRank; ++r)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wr[r][q] = w[4 * r + q];   // zero-padded table
+  float4 acc[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) acc[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int r = 0; r < kMaxRank; ++r) {
+    if (r < pb.T) {
+      const float4 v = *reinterpret_cast<const float4 *>(P + ((bt * pb.T + r) * pb.mp + p) * pb.np + 4 * q4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float wq = wr[r][q];
+        if (wq != 0.0f) {
+          acc[q].x = __fmaf_rn(wq, v.x, acc[q].x);
+          acc[q].y = __fmaf_rn(wq, v.y, acc[q].y);
+          acc[q].z = __fmaf_rn(wq, v.z, acc[q].z);
+          acc[q].w = __fmaf_rn(wq, v.w, acc[q].w);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = q & 1, k = q >> 1;
+    float *dst = C + bt * pb.M * pb.N + (i * pb.mp + p) * pb.N + k * pb.np + 4 * q4;
+    if (VEC) {
+      *reinterpret_cast<float4 *>(dst) = acc[q];
+    } else {
+      dst[0] = acc[q].x; dst[1] = acc[q].y; dst[2] = acc[q].z; dst[3] = acc[q].w;
+    }
+  }
+}
+
+}  // namespace
+
+int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace &wl, void *stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  SplitArgs g;
+  g.xa = ws + wl.a_codes;
+  g.xb = ws + wl.b_codes;
+  g.sat = ws + wl.a_scales_t;
+  g.sbt = ws + wl.b_scales_t;
+  g.P = reinterpret_cast<float *>(const_cast<uint8_t *>(ws) + wl.products);
+  g.mp = pb.mp; g.np = pb.np; g.kp = pb.kp; g.kblocks = pb.kblocks; g.T = pb.T;
+  g.tiles_m = (int)(pb.mp / TT);
+  g.tiles_n = (int)(pb.np / TT);
+  const int64_t items = pb.batch * pb.T * g.tiles_m * g.tiles_n;
+  if (pb.block == 32)
+    hipLaunchKernelGGL(gemm_tile256_kernel<32>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+  else
+    hipLaunchKernelGGL(gemm_tile256_kernel<128>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+  return hipGetLastError();
+}
+
+int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
+                         float *C, void *stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const float *P = reinterpret_cast<const float *>(ws + wl.products);
+  const int64_t npos = pb.mp * (pb.np / 4);
+  const dim3 g2((unsigned)((npos + 255) / 256), (unsigned)pb.batch);
+  if ((reinterpret_cast<uintptr_t>(C) & 15) == 0)
+    hipLaunchKernelGGL(combine1_kernel<true>, g2, dim3(256), 0, st, P, tab.w_inner, C, pb);
+  else
+    hipLaunchKernelGGL(combine1_kernel<false>, g2, dim3(256), 0, st, P, tab.w_inner, C, pb);
+  return hipGetLastError();
+}
+
+}  // namespace fmm

@@ -93,6 +93,12 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.kblocks = pb.kp / q.block;
   pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
   pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
+  // large-tile path: E8M0 scales applied by the MFMA, one level, 256-row tiles,
+  // whole 64-byte (block 32) or 128-byte (block 128) K steps
+  pb.split = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
+             q.depth == 1 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
+             pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
+             q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTile) < (int64_t(1) << 31);
 
   // workspace layout
   fmm::Workspace &wl = p->wl;
@@ -104,6 +110,12 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   wl.b_scales = off; off = align256(off + B * T * pb.np * pb.kblocks * pb.scale_bytes);
   wl.partial = off;
   if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
+  wl.a_scales_t = wl.b_scales_t = wl.products = off;
+  if (pb.split) {
+    wl.a_scales_t = off; off = align256(off + B * T * pb.mp * pb.kblocks);
+    wl.b_scales_t = off; off = align256(off + B * T * pb.np * pb.kblocks);
+    wl.products = off; off = align256(off + B * T * pb.mp * pb.np * sizeof(float));
+  }
   wl.total = off;
 
   // host tables: fp32 flattened U, V (nonzeros in ascending block order), base w, outer w
@@ -137,7 +149,7 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   const size_t s_boff = s_aoff;
   const size_t s_aent = align256(std::max<size_t>(1, aent.size()) * sizeof(fmm::CoefEntry));
   const size_t s_bent = align256(std::max<size_t>(1, bent.size()) * sizeof(fmm::CoefEntry));
-  const size_t s_wi = align256(wbase.size() * sizeof(float));
+  const size_t s_wi = align256((size_t)fmm::kMaxRank * 4 * sizeof(float));   // zero-padded to 8 x 4
   const size_t s_wo = align256(std::max<size_t>(1, wouter.size()) * sizeof(float));
   const size_t tot = s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo;
   std::vector<uint8_t> host(tot, 0);
@@ -195,13 +207,15 @@ int fmm_operand_views(const fmm_plan *p, void *dWs, fmm_view *a, fmm_view *b) {
     a->codes = ws ? ws + p->wl.a_codes : nullptr;
     a->scales = ws ? ws + p->wl.a_scales : nullptr;
     a->batch = pb.batch; a->terms = pb.T; a->rows = pb.mp; a->kdim = pb.kp;
-    a->kblocks = pb.kblocks; a->scale_bytes = pb.scale_bytes; a->reserved = 0;
+    a->kblocks = pb.kblocks; a->scale_bytes = pb.scale_bytes;
+    a->code_layout = pb.split ? FMM_LAYOUT_TILE256x64 : FMM_LAYOUT_ROWS;
   }
   if (b) {
     b->codes = ws ? ws + p->wl.b_codes : nullptr;
     b->scales = ws ? ws + p->wl.b_scales : nullptr;
     b->batch = pb.batch; b->terms = pb.T; b->rows = pb.np; b->kdim = pb.kp;
-    b->kblocks = pb.kblocks; b->scale_bytes = pb.scale_bytes; b->reserved = 0;
+    b->kblocks = pb.kblocks; b->scale_bytes = pb.scale_bytes;
+    b->code_layout = pb.split ? FMM_LAYOUT_TILE256x64 : FMM_LAYOUT_ROWS;
   }
   return FMM_OK;
 }
@@ -223,15 +237,32 @@ int fmm_encode(const fmm_plan *p, const float *dA, const float *dB, void *dWs, v
   return hip_status(fmm::launch_encode(pb, p->tab, dA, dB, reinterpret_cast<uint8_t *>(dWs), p->wl, stream));
 }
 
-int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream) {
+static int check_multiply(const fmm_plan *p, const void *dWs, const float *dC) {
   if (!p) return FMM_ERR_ARG;
   const fmm::Problem &pb = p->pb;
   const bool empty = pb.batch == 0 || pb.M == 0 || pb.N == 0;
   if (!empty && !dC) return FMM_ERR_ARG;
-  int st = check_ws(p, dWs);
+  return check_ws(p, dWs);
+}
+
+int fmm_products(const fmm_plan *p, void *dWs, float *dC, void *stream) {
+  int st = check_multiply(p, dWs, dC);
   if (st != FMM_OK) return st;
-  return hip_status(fmm::launch_multiply(pb, p->tab, reinterpret_cast<const uint8_t *>(dWs),
-                                         p->wl, dC, stream));
+  return hip_status(fmm::launch_products(p->pb, p->tab, reinterpret_cast<const uint8_t *>(dWs), p->wl,
+                                         dC, stream));
+}
+
+int fmm_combine(const fmm_plan *p, void *dWs, float *dC, void *stream) {
+  int st = check_multiply(p, dWs, dC);
+  if (st != FMM_OK) return st;
+  return hip_status(fmm::launch_combine(p->pb, p->tab, reinterpret_cast<const uint8_t *>(dWs), p->wl,
+                                        dC, stream));
+}
+
+int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream) {
+  int st = fmm_products(p, dWs, dC, stream);
+  if (st != FMM_OK) return st;
+  return fmm_combine(p, dWs, dC, stream);
 }
 
 int fmm_matmul(const fmm_plan *p, const float *dA, const float *dB, float *dC, void *dWs,

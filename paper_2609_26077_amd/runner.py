@@ -8,8 +8,9 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (Realization, fmm_encode, fmm_error_stats, fmm_error_stats_scratch_size,
-               fmm_matmul, fmm_multiply, fmm_operand_views, fmm_plan_create,
+from . import (FMM_LAYOUT_TILE256x64, Realization, fmm_combine, fmm_encode, fmm_error_stats,
+               fmm_error_stats_scratch_size, fmm_matmul, fmm_multiply, fmm_operand_views,
+               fmm_plan_create, fmm_products,
                fmm_plan_workspace_size, fmm_realization_builtin, fmm_reference_f64, make_desc)
 
 
@@ -48,8 +49,23 @@ class FMM:
         fmm_multiply(self.plan, self.ws, C, stream)
         return C
 
+    def products(self, C=None, stream=None):
+        """First half of multiply (the sub-products); returns C, which it may or may not have written."""
+        b, M, K, N = self.shape
+        if C is None:
+            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        fmm_products(self.plan, self.ws, C, stream)
+        return C
+
+    def combine(self, C, stream=None):
+        """Second half of multiply (the rest of the W-combine); writes C."""
+        fmm_combine(self.plan, self.ws, C, stream)
+        return C
+
     def operands(self):
-        """torch views of (a_codes, a_scales, b_codes, b_scales) in the workspace."""
+        """(a_codes, a_scales, b_codes, b_scales) as [batch][terms][rows][kdim]
+        and [batch][terms][rows][kblocks] tensors: views of the workspace, except
+        codes held in the tiled layout, which are returned as a row-major copy."""
         a, b = fmm_operand_views(self.plan, self.ws)
         base = self.ws.data_ptr()
         out = []
@@ -58,7 +74,11 @@ class FMM:
             ns = v.batch * v.terms * v.rows * v.kblocks
             c0 = v.codes - base
             s0 = v.scales - base
-            codes = self.ws[c0:c0 + nc].view(v.batch, v.terms, v.rows, v.kdim)
+            raw = self.ws[c0:c0 + nc]
+            if v.code_layout == FMM_LAYOUT_TILE256x64:
+                codes = _untile256x64(raw, v.batch, v.terms, v.rows, v.kdim)
+            else:
+                codes = raw.view(v.batch, v.terms, v.rows, v.kdim)
             sraw = self.ws[s0:s0 + ns * v.scale_bytes]
             if v.scale_bytes == 4:
                 scales = sraw.view(torch.float32).view(v.batch, v.terms, v.rows, v.kblocks)
@@ -66,6 +86,15 @@ class FMM:
                 scales = sraw.view(v.batch, v.terms, v.rows, v.kblocks)
             out += [codes, scales]
         return tuple(out)
+
+
+def _untile256x64(raw, batch, terms, rows, kdim):
+    """Row-major copy of codes in FMM_LAYOUT_TILE256x64 (see include/fmm8.h)."""
+    t = raw.view(batch, terms, rows // 256, kdim // 64, 256, 4, 16)
+    row = torch.arange(256, device=raw.device)[:, None]
+    chunk = torch.arange(4, device=raw.device)[None, :]
+    t = t[:, :, :, :, row, chunk ^ ((row >> 2) & 3), :]      # logical chunk c of tile row
+    return t.permute(0, 1, 2, 4, 3, 5, 6).reshape(batch, terms, rows, kdim)
 
 
 def reference_f64(A, B, stream=None):

@@ -158,3 +158,55 @@ def test_tile_aligned_fast_path(case):
     name, b, M, K, N, depth, bs, rule = case
     r = check_case(name, "gaussian", b, M, K, N, depth, bs, rule, seed=13, cfg=9)
     print(case, r, flush=True)
+
+
+@pytest.mark.parametrize("case", [
+    ("tstar", 1, 512, 128, 512, 32, 1),        # one 256 x 256 tile, one 64-byte k-step
+    ("tstar", 1, 1024, 256, 512, 32, 1),       # 2 x 1 tiles, two k-steps
+    ("strassen", 2, 512, 384, 1024, 32, 2),    # batch of two, 1 x 2 tiles, three k-steps, OCP
+    ("cubic8", 1, 1024, 640, 1024, 32, 1),     # eight terms, 2 x 2 tiles, five k-steps
+    ("winograd", 1, 512, 1024, 512, 128, 1),   # block 128, eight k-steps
+    ("tstar", 1, 512, 512, 1536, 128, 2),      # block 128, OCP, 1 x 3 tiles
+])
+def test_large_tile_split_path(case):
+    """Shapes the large-tile path takes (depth 1, E8M0 scales, m' and n'
+    multiples of 256, k' a multiple of 64, or of 128 at block 128): every
+    prologue and tail branch of its transfer ring (one, two, three, five and
+    eight k-steps), several tiles along both edges, batches, eight terms."""
+    name, b, M, K, N, bs, rule = case
+    r = check_case(name, "gaussian", b, M, K, N, 1, bs, rule, seed=14, cfg=10)
+    print(case, r, flush=True)
+
+
+def test_large_tile_split_path_unaligned_output():
+    """C at an address that is 4 but not 16 bytes aligned: the W-combine of
+    the large-tile path stores scalars; the result equals the aligned one."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    A, B = gen.operands("gaussian", 1, 512, 256, 512, seed=15)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM("tstar", 1, 512, 256, 512, 1, 32, "pow2_ceil")
+    C1 = f.matmul(dA, dB).clone()
+    buf = torch.full((1 + 512 * 512,), float("nan"), device="cuda:0")
+    C2 = buf[1:].view(1, 512, 512)
+    assert C2.data_ptr() % 16 == 4
+    f.matmul(dA, dB, C2)
+    assert torch.equal(C1, C2)
+
+
+@pytest.mark.parametrize("shape,depth", [((1, 512, 256, 512), 1),    # large-tile plan
+                                         ((1, 256, 256, 384), 1),    # combine fused into the GEMM
+                                         ((2, 256, 512, 256), 2)])   # outer combine
+def test_products_then_combine_equals_multiply(shape, depth):
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    b, M, K, N = shape
+    A, B = gen.operands("gaussian", b, M, K, N, seed=16)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM("tstar", b, M, K, N, depth, 32, "pow2_ceil")
+    f.encode(dA, dB)
+    C1 = f.multiply().clone()
+    C2 = torch.full_like(C1, float("nan"))
+    f.products(C2)
+    f.combine(C2)
+    assert torch.equal(C1, C2)

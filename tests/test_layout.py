@@ -1,0 +1,52 @@
+"""Host-side checks of the ABI's constants and of the tiled code layout.
+
+The tiled layout FMM_LAYOUT_TILE256x64 is rebuilt here from its definition in
+include/fmm8.h with plain loops; the binding's row-major reconstruction must
+invert it exactly.  No GPU is needed.
+"""
+import os
+import re
+
+import numpy as np
+import torch
+
+import paper_2609_26077_amd as fm
+from paper_2609_26077_amd.runner import _untile256x64
+
+HEADER = os.path.join(os.path.dirname(__file__), "..", "include", "fmm8.h")
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    consts = dict((k, int(v)) for k, v in re.findall(r"\b(FMM_[A-Z0-9_x]+)\s*=\s*(-?\d+)", text))
+    assert "FMM_LAYOUT_TILE256x64" in consts and "FMM_OK" in consts
+    for name, value in consts.items():
+        assert getattr(fm, name) == value, name
+
+
+def _tile_by_definition(codes):
+    """[b][T][rows][kdim] -> the byte image of FMM_LAYOUT_TILE256x64."""
+    b, T, rows, kdim = codes.shape
+    out = np.empty(codes.size, dtype=np.uint8)
+    pos = 0
+    for bi in range(b):
+        for r in range(T):
+            for tile in range(rows // 256):
+                for ks in range(kdim // 64):
+                    img = np.empty((256, 64), dtype=np.uint8)
+                    for t in range(256):
+                        src = codes[bi, r, 256 * tile + t, 64 * ks:64 * ks + 64]
+                        for c in range(4):
+                            s = c ^ ((t >> 2) & 3)
+                            img[t, 16 * s:16 * s + 16] = src[16 * c:16 * c + 16]
+                    out[pos:pos + img.size] = img.ravel()
+                    pos += img.size
+    return out
+
+
+def test_untile_inverts_the_documented_layout():
+    rng = np.random.default_rng(0)
+    codes = rng.integers(0, 256, size=(2, 3, 512, 192), dtype=np.uint8)
+    raw = torch.from_numpy(_tile_by_definition(codes))
+    back = _untile256x64(raw, 2, 3, 512, 192).numpy()
+    assert np.array_equal(back, codes)
