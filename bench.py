@@ -201,7 +201,7 @@ def main():
     sb = 4 if args.rule == "fp32_amax" else 1
     code_bytes = T * (mp + np_) * kp
     scale_bytes = T * (mp + np_) * (kp // args.block) * sb
-    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes * (2 if split else 1)
+    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes
     prod_bytes = T * mp * np_ * 4 if split else 4 * M * N
     comb_bytes = prod_bytes + 4 * M * N if split else 0
     peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \

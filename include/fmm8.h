@@ -106,22 +106,27 @@ typedef struct {
   int32_t flags;   /* FMM_FLAG_* bits; others must be 0 */
 } fmm_plan_desc;
 
-/* Layouts of the codes in a workspace (fmm_view.code_layout). */
+/* Layouts of the quantized operands in a workspace (fmm_view.code_layout). */
 enum {
-  /* [batch][terms][rows][kdim], contracted axis last */
+  /* codes [batch][terms][rows][kdim], scales [batch][terms][rows][kblocks] */
   FMM_LAYOUT_ROWS = 0,
-  /* [batch][terms][rows / 256][kdim / 64][256][64]: 256-row x 64-byte tiles,
-   * each contiguous; inside a tile, 16-byte chunk c of tile row t sits at chunk
-   * c ^ ((t >> 2) & 3) of that row.  Used by plans whose sub-products run on
-   * 256 x 256 tiles (depth 1, E8M0 scales, M / 2 and N / 2 multiples of 256). */
+  /* codes [batch][terms][rows / 256][kdim / 64][256][64]: 256-row x 64-byte
+   * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
+   * at chunk c ^ ((t >> 2) & 3) of that row.
+   * scales [batch][terms][kblocks][rows]: for each block of the contracted
+   * axis, one byte per row, the rows of every 256-row tile permuted so that
+   * tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at byte 4 (32 h + j) + i.
+   * Used by plans whose sub-products run on 256 x 256 tiles (depth 1, E8M0
+   * scales, M / 2 and N / 2 multiples of 256). */
   FMM_LAYOUT_TILE256x64 = 1
 };
 
-/* Where the quantized operands of one side sit inside a workspace.
- * codes : uint8 e4m3 codes in layout code_layout, contracted axis last
- *         (A side: rows = M / 2^l; B side: rows = N / 2^l, i.e. y_r transposed)
- * scales: [batch][terms][rows][kblocks], one per block; uint8 E8M0 (e + 127)
- *         when scale_bytes == 1, IEEE binary32 when scale_bytes == 4. */
+/* Where the quantized operands of one side sit inside a workspace, in layout
+ * code_layout (A side: rows = M / 2^l; B side: rows = N / 2^l, i.e. y_r
+ * transposed; the contracted axis has kdim = K / 2^l codes in kblocks blocks).
+ * codes : uint8 e4m3 codes
+ * scales: one per block; uint8 E8M0 (e + 127) when scale_bytes == 1, IEEE
+ *         binary32 when scale_bytes == 4. */
 typedef struct {
   void *codes;
   void *scales;

@@ -54,8 +54,7 @@ struct Problem {
 // Layout of a workspace: byte offsets from its base.
 struct Workspace {
   size_t a_codes, b_codes, a_scales, b_scales, partial, total;
-  // split path only: K-block-major scale copies and the fp32 sub-products
-  size_t a_scales_t, b_scales_t, products;
+  size_t products;   // split plans only: the fp32 sub-products P_r
 };
 
 // Device copies of the plan's tables (one allocation).

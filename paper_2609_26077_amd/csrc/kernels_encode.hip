@@ -40,11 +40,27 @@ struct Tile {
   static_assert((TR * (kTL / 4)) % 64 == 0, "positions per term must fill whole waves");
 };
 
+// max over each group of gl aligned lanes (gl = block / 4: 4, 8 or 32), every
+// lane receiving its group's maximum: quad permutations (xor 1, xor 2), then
+// the half-row and row mirrors, then across the two rows of 32 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float group_max(float m, int gl) {
+  m = fmaxf(m, dpp<0xB1>(m));        // quad_perm [1, 0, 3, 2]
+  m = fmaxf(m, dpp<0x4E>(m));        // quad_perm [2, 3, 0, 1]
+  if (gl >= 8) m = fmaxf(m, dpp<0x141>(m));   // row_half_mirror: lane i <- 7 - i within 8
+  if (gl >= 16) m = fmaxf(m, dpp<0x140>(m));  // row_mirror: lane i <- 15 - i within 16
+  if (gl >= 32) m = fmaxf(m, __shfl_xor(m, 16, 64));
+  return m;
+}
+
 template <int SIDE, int DEPTH>
 __global__ __launch_bounds__(kThreads) void encode_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
-    uint8_t *__restrict__ scales_t, int64_t tiles_l) {
+    int64_t tiles_l) {
   using TT = Tile<DEPTH>;
   constexpr int TR = TT::TR;
   constexpr int NB = TT::nblk;
@@ -61,42 +77,63 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
   const int64_t kp = pb.kp;
 
   // ---- 1. stage the tile ----------------------------------------------------
+  // every load of the tile is issued before the first LDS write, so the
+  // workgroup waits for HBM once, not once per element
+  constexpr int kPerThread = NB * TR * (kTL / 4) / kThreads;   // float4s per thread
+  static_assert(NB * TR * (kTL / 4) % kThreads == 0, "the tile splits evenly over the threads");
+  float4 stage[kPerThread];
   if (SIDE == 0) {
     // A (M x K): block b = I n + J holds rows I m' + p, columns J k' + l.
     const float *Ab = src + bt * pb.M * pb.K;
-    for (int e = t; e < NB * TR * (kTL / 4); e += kThreads) {
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+      const int e = t + kThreads * k;
       const int b = e / (TR * (kTL / 4));
       const int rem = e % (TR * (kTL / 4));
       const int r = rem / (kTL / 4);
       const int c4 = rem % (kTL / 4);
       const int64_t p = row0 + r, l = l0 + 4 * c4;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (p < rows && l < kp) {
         const int I = b / n, J = b % n;
-        v = *reinterpret_cast<const float4 *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l);
+        stage[k] = *reinterpret_cast<const float4 *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l);
       }
-      *reinterpret_cast<float4 *>(lds + (b * TR + r) * kStride + 4 * c4) = v;
+    }
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+      const int e = t + kThreads * k;
+      const int b = e / (TR * (kTL / 4));
+      const int rem = e % (TR * (kTL / 4));
+      *reinterpret_cast<float4 *>(lds + (b * TR + rem / (kTL / 4)) * kStride + 4 * (rem % (kTL / 4))) = stage[k];
     }
   } else {
     // B (K x N): block b = J n + K holds rows J k' + l, columns K n' + q;
     // lanes run along q so each of the four loads is coalesced.
     const float *Bb = src + bt * pb.K * pb.N;
-    for (int e = t; e < NB * TR * (kTL / 4); e += kThreads) {
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+      const int e = t + kThreads * k;
       const int b = e / (TR * (kTL / 4));
       const int rem = e % (TR * (kTL / 4));
       const int q = rem % TR;
       const int c4 = rem / TR;
       const int64_t qq = row0 + q, l = l0 + 4 * c4;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (qq < rows && l < kp) {
         const int J = b / n, Kb = b % n;
         const float *p = Bb + (J * kp + l) * pb.N + Kb * pb.np + qq;
-        v.x = p[0];
-        v.y = p[pb.N];
-        v.z = p[2 * pb.N];
-        v.w = p[3 * pb.N];
+        stage[k].x = p[0];
+        stage[k].y = p[pb.N];
+        stage[k].z = p[2 * pb.N];
+        stage[k].w = p[3 * pb.N];
       }
-      *reinterpret_cast<float4 *>(lds + (b * TR + q) * kStride + 4 * c4) = v;
+    }
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+      const int e = t + kThreads * k;
+      const int b = e / (TR * (kTL / 4));
+      const int rem = e % (TR * (kTL / 4));
+      *reinterpret_cast<float4 *>(lds + (b * TR + rem % TR) * kStride + 4 * (rem / TR)) = stage[k];
     }
   }
   __syncthreads();
@@ -107,71 +144,93 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
   const int gl = pb.block / 4;               // lanes per block
   const int64_t kb_count = pb.kblocks;
 
-  // one (term, position) item: combine, block maximum, scale, cast, store
-  // x += c * tile[b][row][4 c4 .. +3] in the pinned order (the first term is a plain product)
-  auto accumulate = [&](bool first, int b, float c, int row, int c4, float &x0, float &x1, float &x2,
-                        float &x3) {
-    const float4 v = *reinterpret_cast<const float4 *>(lds + (b * TR + row) * kStride + 4 * c4);
-    const float t0 = __fmul_rn(c, v.x), t1 = __fmul_rn(c, v.y);
-    const float t2 = __fmul_rn(c, v.z), t3 = __fmul_rn(c, v.w);
-    if (first) {
-      x0 = t0; x1 = t1; x2 = t2; x3 = t3;
-    } else {
-      x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
-      x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
+  // one (term, position) item: combine, block maximum, scale, cast, store.
+  // The values of a group of up to four coefficients are all read before any
+  // arithmetic, then x += c * tile[b][row][4 c4 .. +3] in ascending b as
+  // separate multiplies and adds (the first term is a plain product).
+  auto combine = [&](int n, const CoefEntry *ce, int row, int c4, float &x0, float &x1, float &x2,
+                     float &x3, auto reg) {
+    constexpr int G = decltype(reg)::value ? NB : 4;
+    for (int e0 = 0; e0 < n; e0 += G) {
+      float4 v[G];
+#pragma unroll
+      for (int e = 0; e < G; ++e)
+        if (e0 + e < n) v[e] = *reinterpret_cast<const float4 *>(lds + (ce[e0 + e].block * TR + row) * kStride + 4 * c4);
+#pragma unroll
+      for (int e = 0; e < G; ++e) {
+        if (e0 + e < n) {
+          const float c = ce[e0 + e].coef;
+          const float t0 = __fmul_rn(c, v[e].x), t1 = __fmul_rn(c, v[e].y);
+          const float t2 = __fmul_rn(c, v[e].z), t3 = __fmul_rn(c, v[e].w);
+          if (e0 + e == 0) {
+            x0 = t0; x1 = t1; x2 = t2; x3 = t3;
+          } else {
+            x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
+            x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
+          }
+        }
+      }
+      if (decltype(reg)::value) break;   // NB >= n: one group holds every coefficient
     }
   };
 
+  // Where the results of one position go, inside one term's plane: a thread's
+  // positions are the same for every term it handles, so this is computed once.
+  //   codes : row-major p k' + l, or (large-tile plans) the 256-row x 64-byte
+  //           tile image, chunk c of tile row t at c ^ ((t >> 2) & 3)
+  //   scales: row-major p kblocks + kb, or (large-tile plans) K-block-major with
+  //           rows permuted inside each 256-row tile: row 128 wm + 32 i + r at
+  //           byte 4 (32 wm + r) + i of the tile
+  struct Out {
+    int64_t code, scale;
+    bool valid, leader;
+  };
+  auto out_of = [&](int pos) {
+    Out o;
+    const int row = pos / (kTL / 4), c4 = pos % (kTL / 4);
+    const int64_t p = row0 + row, l = l0 + 4 * c4;
+    o.valid = p < rows && l < kp;
+    o.leader = o.valid && (c4 % gl) == 0;
+    const int64_t kb = l / pb.block;
+    if (pb.split) {
+      const int64_t t = p & 255, c = (l >> 4) & 3;
+      o.code = ((((p >> 8) * (kp >> 6) + (l >> 6)) << 14) + t * 64 + 16 * (c ^ ((t >> 2) & 3)) + (l & 15));
+      o.scale = kb * rows + ((p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3)));
+    } else {
+      o.code = p * kp + l;
+      o.scale = p * kb_count + kb;
+    }
+    return o;
+  };
+  const int64_t code_plane = rows * kp, scale_plane = rows * kb_count;
+
   // one (term, position) item: combine, block maximum, scale, cast, store.
   // REG: the term's coefficients sit in a register array indexed by compile-time e.
-  auto item = [&](int64_t r, int pos, int n, const CoefEntry *ce, auto reg) {
+  auto item = [&](int64_t r, int pos, const Out &o, int n, const CoefEntry *ce, auto reg) {
     const int row = pos / (kTL / 4);
     const int c4 = pos % (kTL / 4);
     float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
-    if constexpr (decltype(reg)::value) {
-#pragma unroll
-      for (int e = 0; e < NB; ++e)
-        if (e < n) accumulate(e == 0, ce[e].block, ce[e].coef, row, c4, x0, x1, x2, x3);
-    } else {
-      for (int e = 0; e < n; ++e) accumulate(e == 0, ce[e].block, ce[e].coef, row, c4, x0, x1, x2, x3);
-    }
+    combine(n, ce, row, c4, x0, x1, x2, x3, reg);
     // block maximum across the gl lanes of this block (all lanes take part)
-    float m = fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3)));
-    for (int s = 1; s < gl; s <<= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
+    const float m = group_max(fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3))), gl);
     const dev::Scale sc = dev::block_scale(m, pb.rule);
     const uint32_t w = dev::e4m3_pack4(dev::scaled(x0, sc, pb.rule), dev::scaled(x1, sc, pb.rule),
                                        dev::scaled(x2, sc, pb.rule), dev::scaled(x3, sc, pb.rule));
-    const int64_t p = row0 + row;
-    const int64_t l = l0 + 4 * c4;
-    if (p < rows && l < kp) {
-      const int64_t rowid = (bt * T + r) * rows + p;
-      int64_t at = rowid * kp + l;
-      if (scales_t) {
-        // tiled codes of the large-tile path: 256-row x 64-byte tiles, each the
-        // LDS image the GEMM copies (chunk c of tile row t at c ^ ((t >> 2) & 3))
-        const int64_t t = p & 255, c = (l >> 4) & 3;
-        at = ((((bt * T + r) * (rows >> 8) + (p >> 8)) * (kp >> 6) + (l >> 6)) << 14) + t * 64 +
-             16 * (c ^ ((t >> 2) & 3)) + (l & 15);
-      }
-      *reinterpret_cast<uint32_t *>(codes + at) = w;
-      if ((c4 % gl) == 0) {
-        const int64_t kb = l / pb.block;
-        if (pb.scale_bytes == 1)
-          scales[rowid * kb_count + kb] = (uint8_t)sc.stored;
-        else
-          reinterpret_cast<uint32_t *>(scales)[rowid * kb_count + kb] = sc.stored;
-        if (scales_t) {
-          // K-block-major copy for the large-tile path, rows permuted inside each
-          // 256-row tile: row 128 wm + 32 i + r at byte 4 (32 wm + r) + i
-          const int64_t pt = (p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3));
-          scales_t[((bt * T + r) * kb_count + kb) * rows + pt] = (uint8_t)sc.stored;
-        }
-      }
+    const int64_t plane = bt * T + r;
+    if (o.valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + o.code) = w;
+    if (o.leader) {
+      if (pb.scale_bytes == 1)
+        scales[plane * scale_plane + o.scale] = (uint8_t)sc.stored;
+      else
+        reinterpret_cast<uint32_t *>(scales)[plane * scale_plane + o.scale] = sc.stored;
     }
   };
 
   if constexpr (P >= kThreads) {
     // term-outer: the term's nonzero coefficients are read once into SGPRs
+    Out outs[P / kThreads];
+#pragma unroll
+    for (int pp = 0; pp < P / kThreads; ++pp) outs[pp] = out_of(t + kThreads * pp);
     for (int64_t r = 0; r < T; ++r) {
       const int beg = __builtin_amdgcn_readfirstlane(off[r]);
       const int n = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
@@ -180,40 +239,41 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
       for (int e = 0; e < NB; ++e)
         if (e < n) ce[e] = ent[beg + e];
 #pragma unroll
-      for (int pp = 0; pp < P / kThreads; ++pp) item(r, t + kThreads * pp, n, ce, std::true_type{});
+      for (int pp = 0; pp < P / kThreads; ++pp) item(r, t + kThreads * pp, outs[pp], n, ce, std::true_type{});
     }
   } else {
-    // few positions per term: a wave takes 64 consecutive items (one term)
+    // few positions per term: a wave takes 64 consecutive items (one term);
+    // kThreads is a multiple of P, so a thread's position is t % P throughout
+    static_assert(kThreads % P == 0, "a thread keeps one position");
+    const Out o = out_of(t % P);
     for (int64_t it = t; it < T * P; it += kThreads) {
       const int64_t r = __builtin_amdgcn_readfirstlane((int)(it / P));
       const int beg = __builtin_amdgcn_readfirstlane(off[r]);
       const int n = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
-      item(r, (int)(it % P), n, ent + beg, std::false_type{});
+      item(r, t % P, o, n, ent + beg, std::false_type{});
     }
   }
 }
 
 template <int SIDE, int DEPTH>
 hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
-                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, uint8_t *scales_t,
-                       hipStream_t st) {
+                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
   const int64_t tiles_r = (rows + Tile<DEPTH>::TR - 1) / Tile<DEPTH>::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
   hipLaunchKernelGGL((encode_kernel<SIDE, DEPTH>), grid, dim3(kThreads), 0, st, src, pb, off,
-                     ent, codes, scales, scales_t, tiles_l);
+                     ent, codes, scales, tiles_l);
   return hipGetLastError();
 }
 
 template <int SIDE>
 hipError_t launch_depth(const Problem &pb, const float *src, const int32_t *off,
-                        const CoefEntry *ent, uint8_t *codes, uint8_t *scales, uint8_t *scales_t,
-                        hipStream_t st) {
+                        const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
   switch (pb.depth) {
-    case 1: return launch_side<SIDE, 1>(pb, src, off, ent, codes, scales, scales_t, st);
-    case 2: return launch_side<SIDE, 2>(pb, src, off, ent, codes, scales, scales_t, st);
-    case 3: return launch_side<SIDE, 3>(pb, src, off, ent, codes, scales, scales_t, st);
+    case 1: return launch_side<SIDE, 1>(pb, src, off, ent, codes, scales, st);
+    case 2: return launch_side<SIDE, 2>(pb, src, off, ent, codes, scales, st);
+    case 3: return launch_side<SIDE, 3>(pb, src, off, ent, codes, scales, st);
   }
   return hipErrorInvalidValue;
 }
@@ -224,11 +284,9 @@ int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, co
                   uint8_t *ws, const Workspace &wl, void *stream) {
   if (pb.batch == 0 || pb.M == 0 || pb.N == 0 || pb.K == 0) return hipSuccess;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  uint8_t *at = pb.split ? ws + wl.a_scales_t : nullptr;
-  uint8_t *btp = pb.split ? ws + wl.b_scales_t : nullptr;
-  hipError_t e = launch_depth<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, at, st);
+  hipError_t e = launch_depth<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, st);
   if (e != hipSuccess) return e;
-  return launch_depth<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, btp, st);
+  return launch_depth<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, st);
 }
 
 }  // namespace fmm

@@ -16,7 +16,7 @@
 //      one fused multiply-add per nonzero weight (the order of the fused
 //      W-combine of the 128 x 128 path).
 //
-// Scales come from the encoder's second, K-block-major copy: for each
+// Scales of these plans are stored K-block-major by the encoder: for each
 // (term, K block) the E8M0 bytes of all rows, permuted inside every 256-row
 // tile so that row 128 wm + 32 i + r sits at byte 4 (32 wm + r) + i.  One
 // 32-bit LDS read then gives a lane the scales of its four A row tiles (or,
@@ -276,8 +276,8 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
   SplitArgs g;
   g.xa = ws + wl.a_codes;
   g.xb = ws + wl.b_codes;
-  g.sat = ws + wl.a_scales_t;
-  g.sbt = ws + wl.b_scales_t;
+  g.sat = ws + wl.a_scales;
+  g.sbt = ws + wl.b_scales;
   g.P = reinterpret_cast<float *>(const_cast<uint8_t *>(ws) + wl.products);
   g.mp = pb.mp; g.np = pb.np; g.kp = pb.kp; g.kblocks = pb.kblocks; g.T = pb.T;
   g.tiles_m = (int)(pb.mp / TT);

@@ -110,12 +110,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   wl.b_scales = off; off = align256(off + B * T * pb.np * pb.kblocks * pb.scale_bytes);
   wl.partial = off;
   if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
-  wl.a_scales_t = wl.b_scales_t = wl.products = off;
-  if (pb.split) {
-    wl.a_scales_t = off; off = align256(off + B * T * pb.mp * pb.kblocks);
-    wl.b_scales_t = off; off = align256(off + B * T * pb.np * pb.kblocks);
-    wl.products = off; off = align256(off + B * T * pb.mp * pb.np * sizeof(float));
-  }
+  wl.products = off;
+  if (pb.split) off = align256(off + B * T * pb.mp * pb.np * sizeof(float));
   wl.total = off;
 
   // host tables: fp32 flattened U, V (nonzeros in ascending block order), base w, outer w

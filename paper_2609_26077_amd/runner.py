@@ -64,8 +64,8 @@ class FMM:
 
     def operands(self):
         """(a_codes, a_scales, b_codes, b_scales) as [batch][terms][rows][kdim]
-        and [batch][terms][rows][kblocks] tensors: views of the workspace, except
-        codes held in the tiled layout, which are returned as a row-major copy."""
+        and [batch][terms][rows][kblocks] tensors: views of the workspace, or
+        row-major copies where the plan keeps them in the tiled layout."""
         a, b = fmm_operand_views(self.plan, self.ws)
         base = self.ws.data_ptr()
         out = []
@@ -75,13 +75,16 @@ class FMM:
             c0 = v.codes - base
             s0 = v.scales - base
             raw = self.ws[c0:c0 + nc]
-            if v.code_layout == FMM_LAYOUT_TILE256x64:
+            tiled = v.code_layout == FMM_LAYOUT_TILE256x64
+            if tiled:
                 codes = _untile256x64(raw, v.batch, v.terms, v.rows, v.kdim)
             else:
                 codes = raw.view(v.batch, v.terms, v.rows, v.kdim)
             sraw = self.ws[s0:s0 + ns * v.scale_bytes]
             if v.scale_bytes == 4:
                 scales = sraw.view(torch.float32).view(v.batch, v.terms, v.rows, v.kblocks)
+            elif tiled:
+                scales = _unpermute_scales256(sraw, v.batch, v.terms, v.rows, v.kblocks)
             else:
                 scales = sraw.view(v.batch, v.terms, v.rows, v.kblocks)
             out += [codes, scales]
@@ -95,6 +98,15 @@ def _untile256x64(raw, batch, terms, rows, kdim):
     chunk = torch.arange(4, device=raw.device)[None, :]
     t = t[:, :, :, :, row, chunk ^ ((row >> 2) & 3), :]      # logical chunk c of tile row
     return t.permute(0, 1, 2, 4, 3, 5, 6).reshape(batch, terms, rows, kdim)
+
+
+def _unpermute_scales256(raw, batch, terms, rows, kblocks):
+    """[batch][terms][rows][kblocks] copy of scales in FMM_LAYOUT_TILE256x64."""
+    t = raw.view(batch, terms, kblocks, rows // 256, 256)
+    r = torch.arange(256, device=raw.device)
+    stored = (((r >> 7) * 32 + (r & 31)) * 4 + ((r >> 5) & 3))     # where tile row r sits
+    t = t[..., stored]
+    return t.reshape(batch, terms, kblocks, rows).permute(0, 1, 3, 2).contiguous()
 
 
 def reference_f64(A, B, stream=None):

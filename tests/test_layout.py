@@ -11,7 +11,7 @@ import numpy as np
 import torch
 
 import paper_2609_26077_amd as fm
-from paper_2609_26077_amd.runner import _untile256x64
+from paper_2609_26077_amd.runner import _unpermute_scales256, _untile256x64
 
 HEADER = os.path.join(os.path.dirname(__file__), "..", "include", "fmm8.h")
 
@@ -50,3 +50,20 @@ def test_untile_inverts_the_documented_layout():
     raw = torch.from_numpy(_tile_by_definition(codes))
     back = _untile256x64(raw, 2, 3, 512, 192).numpy()
     assert np.array_equal(back, codes)
+
+
+def test_unpermute_scales_inverts_the_documented_layout():
+    rng = np.random.default_rng(1)
+    b, T, rows, kb = 2, 3, 512, 5
+    scales = rng.integers(0, 256, size=(b, T, rows, kb), dtype=np.uint8)
+    raw = np.empty(scales.size, dtype=np.uint8)
+    for bi in range(b):
+        for r in range(T):
+            for k in range(kb):
+                base = ((bi * T + r) * kb + k) * rows
+                for p in range(rows):
+                    tr = p % 256
+                    h, i, j = tr // 128, (tr // 32) % 4, tr % 32
+                    raw[base + (p - tr) + 4 * (32 * h + j) + i] = scales[bi, r, p, k]
+    back = _unpermute_scales256(torch.from_numpy(raw), b, T, rows, kb).numpy()
+    assert np.array_equal(back, scales)
