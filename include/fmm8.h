@@ -118,7 +118,16 @@ enum {
    * tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at byte 4 (32 h + j) + i.
    * Used by plans whose sub-products run on 256 x 256 tiles (depth 1, E8M0
    * scales, M / 2 and N / 2 multiples of 256). */
-  FMM_LAYOUT_TILE256x64 = 1
+  FMM_LAYOUT_TILE256x64 = 1,
+  /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
+   * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
+   * at chunk c ^ (t & 7) ^ ((t >> 3) & 1) of that row.
+   * scales [batch][terms][rows / 128][kdim / 128][128][4]: for each tile row
+   * and 128-byte step, 4 E8M0 bytes: at block 32 the step's blocks 0, 2, 1, 3
+   * in that order, at block 128 the step's one block repeated 4 times.
+   * Used by the other plans with E8M0 scales at block 32 or 128 whose
+   * M / 2^l and N / 2^l are multiples of 128 and K / 2^l a multiple of 128. */
+  FMM_LAYOUT_TILE128x128 = 2
 };
 
 /* Where the quantized operands of one side sit inside a workspace, in layout

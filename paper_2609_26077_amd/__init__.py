@@ -45,6 +45,7 @@ BUILTINS = {"cubic8": FMM_CUBIC8, "strassen": FMM_STRASSEN, "winograd": FMM_WINO
 FMM_FLAG_EXACT_DOT = 1
 FMM_LAYOUT_ROWS = 0
 FMM_LAYOUT_TILE256x64 = 1
+FMM_LAYOUT_TILE128x128 = 2
 
 FMM_RULE_FP32_AMAX = 0
 FMM_RULE_POW2_CEIL = 1

@@ -49,7 +49,14 @@ struct Problem {
   int scale_bytes;         // 1 (E8M0) or 4 (fp32)
   int exact_dot;           // FMM_FLAG_EXACT_DOT requested
   int split;               // large-tile sub-products + separate W-combine (depth 1, tile-aligned MX)
+  int layout;              // FMM_LAYOUT_* of the workspace's codes and scales
 };
+
+// Bytes of one (batch, term) plane of scales for `rows` rows.
+inline int64_t scale_plane_bytes(const Problem &pb, int64_t rows) {
+  if (pb.layout == FMM_LAYOUT_TILE128x128) return rows * (pb.kp / 128) * 4;
+  return rows * pb.kblocks * pb.scale_bytes;
+}
 
 // Layout of a workspace: byte offsets from its base.
 struct Workspace {

@@ -181,6 +181,10 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
   //   scales: row-major p kblocks + kb, or (large-tile plans) K-block-major with
   //           rows permuted inside each 256-row tile: row 128 wm + 32 i + r at
   //           byte 4 (32 wm + r) + i of the tile
+  //   128 x 128 tiles: codes as the 128-row x 128-byte tile image (chunk c of
+  //           tile row t at c ^ (t & 7) ^ ((t >> 3) & 1)); scales 4 bytes per
+  //           tile row and 128-byte step (blocks 0, 2, 1, 3 at block 32; the
+  //           one block repeated at block 128)
   struct Out {
     int64_t code, scale;
     bool valid, leader;
@@ -192,17 +196,24 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
     o.valid = p < rows && l < kp;
     o.leader = o.valid && (c4 % gl) == 0;
     const int64_t kb = l / pb.block;
-    if (pb.split) {
+    if (pb.layout == FMM_LAYOUT_TILE256x64) {
       const int64_t t = p & 255, c = (l >> 4) & 3;
       o.code = ((((p >> 8) * (kp >> 6) + (l >> 6)) << 14) + t * 64 + 16 * (c ^ ((t >> 2) & 3)) + (l & 15));
       o.scale = kb * rows + ((p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3)));
+    } else if (pb.layout == FMM_LAYOUT_TILE128x128) {
+      const int64_t t = p & 127, c = (l >> 4) & 7, tile = (p >> 7) * (kp >> 7) + (l >> 7);
+      o.code = (tile << 14) + t * 128 + 16 * (c ^ (t & 7) ^ ((t >> 3) & 1)) + (l & 15);
+      const int64_t kq = (l >> 5) & 3;                       // block of the step (block 32)
+      o.scale = tile * 512 + t * 4 + (pb.block == 32 ? ((kq & 1) << 1) | (kq >> 1) : 0);
     } else {
       o.code = p * kp + l;
       o.scale = p * kb_count + kb;
     }
     return o;
   };
-  const int64_t code_plane = rows * kp, scale_plane = rows * kb_count;
+  // elements of scales per (batch, term) plane (the 128 x 128 layout keeps 4 bytes per row and step)
+  const int64_t code_plane = rows * kp;
+  const int64_t scale_plane = pb.layout == FMM_LAYOUT_TILE128x128 ? rows * (kp / 128) * 4 : rows * kb_count;
 
   // one (term, position) item: combine, block maximum, scale, cast, store.
   // REG: the term's coefficients sit in a register array indexed by compile-time e.
@@ -219,10 +230,12 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(
     const int64_t plane = bt * T + r;
     if (o.valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + o.code) = w;
     if (o.leader) {
-      if (pb.scale_bytes == 1)
-        scales[plane * scale_plane + o.scale] = (uint8_t)sc.stored;
-      else
+      if (pb.scale_bytes == 4)
         reinterpret_cast<uint32_t *>(scales)[plane * scale_plane + o.scale] = sc.stored;
+      else if (pb.layout == FMM_LAYOUT_TILE128x128 && pb.block == 128)
+        *reinterpret_cast<uint32_t *>(scales + plane * scale_plane + o.scale) = sc.stored * 0x01010101u;
+      else
+        scales[plane * scale_plane + o.scale] = (uint8_t)sc.stored;
     }
   };
 

@@ -265,15 +265,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_kernel(GemmArgs g) {
 
 
 // ---------------------------------------------------------------------------
-// Fast MX path for tile-aligned shapes (m', n' multiples of 128; k' a multiple
-// of 128 for block 32, of 512 for block 128).
+// Fast MX path for tile-aligned shapes (m', n' and k' multiples of 128), whose
+// codes and scales the encoder writes in the 128 x 128 tile layout.
 //
 // One workgroup of four waves owns a 128 x 128 tile of the m' x n' grid; each
 // wave a 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  The codes and E8M0
 // scales of each 128-byte K step go from HBM straight into LDS
 // (global_load_lds: no staging registers) through a four-slot ring; each wave
 // issues exactly nine such transfers per step (four 1 KB of A codes, four of
-// B codes, one 256 B of scales) and waits for them with an explicit vmcnt.
+// B codes, one 256 B of scales), all straight copies of the tile images, and
+// waits for them with an explicit vmcnt.
 // While the MFMAs of step s run on fragments already in registers, the
 // fragments of step s + 1 are read from LDS into a second register set and the
 // transfers of steps s + 2 and s + 3 are in flight.  LDS code rows are 128
@@ -283,9 +284,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_kernel(GemmArgs g) {
 // The quadrant accumulators of the fused W-combine live in AGPRs for the
 // whole kernel (the four 64 x 64 sets fill the 256 accumulation registers),
 // leaving the architectural VGPRs to the MFMA accumulator, the two fragment
-// sets and addressing; they are touched only through the helpers below.  The
-// decoder weights are copied to LDS once, so the term-end combine never waits
-// on vector memory (which would drain the transfer ring).
+// sets and addressing; they are touched only through the helpers below, eight
+// at a time at a term end.  The decoder weights are copied to LDS once, so the
+// term-end combine never waits on vector memory (which would drain the
+// transfer ring).
 // ---------------------------------------------------------------------------
 constexpr int FBK = 128;
 constexpr int kSlot = 2 * BM * FBK + 2 * BM * 4;   // codes A, B + scale words A, B
@@ -306,6 +308,27 @@ __device__ __forceinline__ void agpr_fma(float &q, float w, float p) {
       "v_accvgpr_write_b32 %1, %0"
       : "=&v"(t), "+a"(q)
       : "s"(w), "v"(p));
+}
+// eight of the above at once, on eight temporaries, so the reads, the
+// multiply-adds and the writes each issue back to back
+__device__ __forceinline__ void agpr_fma8(float *q, float w, const float *p) {
+  float t0, t1, t2, t3, t4, t5, t6, t7;
+  asm volatile(
+      "v_accvgpr_read_b32 %0, %8\n\tv_accvgpr_read_b32 %1, %9\n\t"
+      "v_accvgpr_read_b32 %2, %10\n\tv_accvgpr_read_b32 %3, %11\n\t"
+      "v_accvgpr_read_b32 %4, %12\n\tv_accvgpr_read_b32 %5, %13\n\t"
+      "v_accvgpr_read_b32 %6, %14\n\tv_accvgpr_read_b32 %7, %15\n\t"
+      "v_fmac_f32_e32 %0, %16, %17\n\tv_fmac_f32_e32 %1, %16, %18\n\t"
+      "v_fmac_f32_e32 %2, %16, %19\n\tv_fmac_f32_e32 %3, %16, %20\n\t"
+      "v_fmac_f32_e32 %4, %16, %21\n\tv_fmac_f32_e32 %5, %16, %22\n\t"
+      "v_fmac_f32_e32 %6, %16, %23\n\tv_fmac_f32_e32 %7, %16, %24\n\t"
+      "v_accvgpr_write_b32 %8, %0\n\tv_accvgpr_write_b32 %9, %1\n\t"
+      "v_accvgpr_write_b32 %10, %2\n\tv_accvgpr_write_b32 %11, %3\n\t"
+      "v_accvgpr_write_b32 %12, %4\n\tv_accvgpr_write_b32 %13, %5\n\t"
+      "v_accvgpr_write_b32 %14, %6\n\tv_accvgpr_write_b32 %15, %7"
+      : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7),
+        "+a"(q[0]), "+a"(q[1]), "+a"(q[2]), "+a"(q[3]), "+a"(q[4]), "+a"(q[5]), "+a"(q[6]), "+a"(q[7])
+      : "s"(w), "v"(p[0]), "v"(p[1]), "v"(p[2]), "v"(p[3]), "v"(p[4]), "v"(p[5]), "v"(p[6]), "v"(p[7]));
 }
 __device__ __forceinline__ float agpr_read(const float &q) {
   float v;
@@ -331,11 +354,12 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int &
   tn = in / gm;
 }
 
-// Operands of one K step for one wave: fragments [substep s][tile i] and the
-// raw E8M0 scale word (four K blocks) of each of its A and B row tiles.
+// Operands of one K step for one wave: fragments [substep s][tile i] and,
+// for each of its A and B row tiles, the two E8M0 scale bytes of the lane's
+// blocks (byte s: substep s).
 struct MxFrags {
   v8i a[2][2], b[2][2];
-  uint32_t wa[2], wb[2];
+  int sa[2], sb[2];
 };
 
 template <int BS>
@@ -362,45 +386,44 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     for (int i = 0; i < 4 * kMaxRank; ++i) lds_w[i] = g.w[i];
   }
 
-  // per-lane DMA offsets into a region of 8 rows x 128 B: lane l fills LDS row
-  // l / 8, chunk l % 8, which holds global chunk (l % 8) ^ (l / 8) ^ (region & 1)
-  const uint32_t code_off0 = (uint32_t)(lane >> 3) * kp + 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
-  const uint32_t code_off1 = code_off0 ^ 16u;
-  // scale words: wave 0/1 -> A rows 64w.., wave 2/3 -> B rows 64(w-2)..
-  const int srow = (wave & 1) * 64 + lane;
-  const uint32_t scale_off = (uint32_t)srow * kblocks;
+  // Codes and scales arrive tiled (the 128-row x 128-byte tile image and 4
+  // scale bytes per tile row and step), so every transfer is a straight copy:
+  // lane l moves bytes 16 l .. 16 l + 15 (codes) or 4 l .. 4 l + 3 (scales).
+  // Scales: waves 0/1 move A tile rows 64 w .., waves 2/3 B tile rows 64 (w - 2) ..
   const bool scale_is_b = wave >= 2;
+  const int64_t kt = g.kp / FBK;                           // 128-byte steps per row tile
 
   auto issue = [&](int step) {
     const int ri = step / nk, ks = step - ri * nk;
     const int64_t r = ro * g.R + ri;
-    const uint32_t k0 = (uint32_t)ks * FBK;
-    const uint8_t *xa = g.xa + ((bt * g.T + r) * g.mp + pm0) * g.kp + k0;
-    const uint8_t *xb = g.xb + ((bt * g.T + r) * g.np + pn0) * g.kp + k0;
+    const int64_t ta = ((bt * g.T + r) * (g.mp / BM) + tm) * kt + ks;   // tile index, A
+    const int64_t tb = ((bt * g.T + r) * (g.np / BN) + tn) * kt + ks;
+    const uint8_t *xa = g.xa + ta * (BM * FBK);
+    const uint8_t *xb = g.xb + tb * (BN * FBK);
     const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int region = wave * 4 + j;                     // rows 8 region .. +8
-      const uint32_t off = (j & 1) ? code_off1 : code_off0;
-      copy16(off, xa + (int64_t)region * 8 * g.kp, m0 + region * 1024);
-      copy16(off, xb + (int64_t)region * 8 * g.kp, m0 + BM * FBK + region * 1024);
+      const int region = wave * 4 + j;                     // tile rows 8 region .. + 7
+      copy16(16u * (uint32_t)lane, xa + region * 1024, m0 + region * 1024);
+      copy16(16u * (uint32_t)lane, xb + region * 1024, m0 + BM * FBK + region * 1024);
     }
-    const uint8_t *sbase = scale_is_b ? g.sb + ((bt * g.T + r) * g.np + pn0) * g.kblocks
-                                      : g.sa + ((bt * g.T + r) * g.mp + pm0) * g.kblocks;
-    const uint32_t kw = BS == 32 ? k0 / 32 : (k0 / 128) & ~3u;   // 4-byte aligned word
-    copy4(scale_off + kw, sbase, m0 + 2 * BM * FBK + (scale_is_b ? BM * 4 : 0) + (wave & 1) * 256);
+    const uint8_t *sbase = scale_is_b ? g.sb + tb * (BN * 4) : g.sa + ta * (BM * 4);
+    copy4(4u * (uint32_t)lane + (wave & 1) * 256u, sbase,
+          m0 + 2 * BM * FBK + (scale_is_b ? BM * 4 : 0) + (wave & 1) * 256);
   };
 
-  // LDS -> registers for one step (slot step % 4; any step index reads in bounds)
+  // LDS -> registers for one step (slot step % 4; any step index reads in bounds).
+  // Scale record of a row: blocks (0, 2, 1, 3) at block 32, so lane (r, h) reads
+  // the 16-bit pair at byte 2h: byte 0 = block h (substep 0), byte 1 = block 2 + h.
   auto load = [&](int step, MxFrags &f) {
     const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
     const uint8_t *lb = la + BM * FBK;
-    const uint32_t *lsa = reinterpret_cast<const uint32_t *>(la + 2 * BM * FBK);
-    const uint32_t *lsb = lsa + BM;
+    const uint8_t *lsa = la + 2 * BM * FBK;
+    const uint8_t *lsb = lsa + BM * 4;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      f.wa[i] = lsa[wrow_a + 32 * i + r32];
-      f.wb[i] = lsb[wrow_b + 32 * i + r32];
+      f.sa[i] = *reinterpret_cast<const uint16_t *>(lsa + 4 * (wrow_a + 32 * i + r32) + 2 * h);
+      f.sb[i] = *reinterpret_cast<const uint16_t *>(lsb + 4 * (wrow_b + 32 * i + r32) + 2 * h);
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -435,27 +458,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     }
     if (step + 3 < total) issue(step + 3);
     const int ks = step % nk;
-    const int sh = BS == 32 ? 8 * h : 8 * (ks & 3);   // block 2s + h at byte 2s / block ks % 4 at byte 0
-    int sa[2], sb[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      sa[i] = (int)(cur.wa[i] >> sh);
-      sb[i] = (int)(cur.wb[i] >> sh);
-    }
     load(step + 1, nxt);
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          if (BS == 32 && s == 1)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[s][i], cur.b[s][j], acc[i][j],
-                                                                          0, 0, 2, sa[i], 2, sb[j]);
-          else
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[s][i], cur.b[s][j], acc[i][j],
-                                                                          0, 0, 0, sa[i], 0, sb[j]);
-        }
+#define FMM_MFMA_SIJ(S, I, J)                                                                      \
+  acc[I][J] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[S][I], cur.b[S][J], acc[I][J], 0, 0, \
+                                                              S, cur.sa[I], S, cur.sb[J])
+    FMM_MFMA_SIJ(0, 0, 0); FMM_MFMA_SIJ(0, 0, 1); FMM_MFMA_SIJ(0, 1, 0); FMM_MFMA_SIJ(0, 1, 1);
+    FMM_MFMA_SIJ(1, 0, 0); FMM_MFMA_SIJ(1, 0, 1); FMM_MFMA_SIJ(1, 1, 0); FMM_MFMA_SIJ(1, 1, 1);
+#undef FMM_MFMA_SIJ
     // MFMA and LDS reads alternate: 1 MFMA, then 3 reads (20 reads over 7 gaps)
 #pragma unroll
     for (int k = 0; k < 6; ++k) {
@@ -478,7 +487,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
 #pragma unroll
             for (int j = 0; j < 2; ++j)
 #pragma unroll
-              for (int e = 0; e < 16; ++e) agpr_fma(quad[q][i][j][e], wq, acc[i][j][e]);
+              for (int e = 0; e < 16; e += 8) {
+                float pv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) pv[u] = acc[i][j][e + u];
+                agpr_fma8(&quad[q][i][j][e], wq, pv);
+              }
         }
       }
 #pragma unroll
@@ -706,9 +720,7 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
   g.w = tab.w_inner;
   const dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)pb.To, (unsigned)pb.batch);
   const bool mx = !pb.exact_dot && pb.rule != dev::RULE_FP32_AMAX && (pb.block == 32 || pb.block == 128);
-  const bool aligned = pb.mp % BM == 0 && pb.np % BN == 0 && pb.kp > 0 &&
-                       pb.kp % (pb.block == 32 ? FBK : 4 * FBK) == 0 &&
-                       pb.mp * pb.kp < (int64_t(1) << 31) && pb.np * pb.kp < (int64_t(1) << 31);
+  const bool aligned = pb.layout == FMM_LAYOUT_TILE128x128;
   if (mx && aligned && pb.block == 32)
     hipLaunchKernelGGL(gemm_mx_fast_kernel<32>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
   else if (mx && aligned && pb.block == 128)

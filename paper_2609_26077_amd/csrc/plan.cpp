@@ -93,12 +93,17 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.kblocks = pb.kp / q.block;
   pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
   pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
+  const bool mx = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
   // large-tile path: E8M0 scales applied by the MFMA, one level, 256-row tiles,
   // whole 64-byte (block 32) or 128-byte (block 128) K steps
   pb.split = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
              q.depth == 1 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
              pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
              q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTile) < (int64_t(1) << 31);
+  // fused 128 x 128 path: E8M0 scales, whole 128-row tiles and 128-byte K steps
+  const bool tile128 = mx && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 && pb.kp % 128 == 0 &&
+                       pb.kp < (int64_t(1) << 26);
+  pb.layout = pb.split ? FMM_LAYOUT_TILE256x64 : tile128 ? FMM_LAYOUT_TILE128x128 : FMM_LAYOUT_ROWS;
 
   // workspace layout
   fmm::Workspace &wl = p->wl;
@@ -106,8 +111,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   const size_t B = (size_t)q.batch;
   wl.a_codes = off; off = align256(off + B * T * pb.mp * pb.kp);
   wl.b_codes = off; off = align256(off + B * T * pb.np * pb.kp);
-  wl.a_scales = off; off = align256(off + B * T * pb.mp * pb.kblocks * pb.scale_bytes);
-  wl.b_scales = off; off = align256(off + B * T * pb.np * pb.kblocks * pb.scale_bytes);
+  wl.a_scales = off; off = align256(off + B * T * fmm::scale_plane_bytes(pb, pb.mp));
+  wl.b_scales = off; off = align256(off + B * T * fmm::scale_plane_bytes(pb, pb.np));
   wl.partial = off;
   if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
   wl.products = off;
@@ -204,14 +209,14 @@ int fmm_operand_views(const fmm_plan *p, void *dWs, fmm_view *a, fmm_view *b) {
     a->scales = ws ? ws + p->wl.a_scales : nullptr;
     a->batch = pb.batch; a->terms = pb.T; a->rows = pb.mp; a->kdim = pb.kp;
     a->kblocks = pb.kblocks; a->scale_bytes = pb.scale_bytes;
-    a->code_layout = pb.split ? FMM_LAYOUT_TILE256x64 : FMM_LAYOUT_ROWS;
+    a->code_layout = pb.layout;
   }
   if (b) {
     b->codes = ws ? ws + p->wl.b_codes : nullptr;
     b->scales = ws ? ws + p->wl.b_scales : nullptr;
     b->batch = pb.batch; b->terms = pb.T; b->rows = pb.np; b->kdim = pb.kp;
     b->kblocks = pb.kblocks; b->scale_bytes = pb.scale_bytes;
-    b->code_layout = pb.split ? FMM_LAYOUT_TILE256x64 : FMM_LAYOUT_ROWS;
+    b->code_layout = pb.layout;
   }
   return FMM_OK;
 }

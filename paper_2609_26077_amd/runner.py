@@ -8,7 +8,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (FMM_LAYOUT_TILE256x64, Realization, fmm_combine, fmm_encode, fmm_error_stats,
+from . import (FMM_LAYOUT_TILE128x128, FMM_LAYOUT_TILE256x64, Realization, fmm_combine, fmm_encode, fmm_error_stats,
                fmm_error_stats_scratch_size, fmm_matmul, fmm_multiply, fmm_operand_views,
                fmm_plan_create, fmm_products,
                fmm_plan_workspace_size, fmm_realization_builtin, fmm_reference_f64, make_desc)
@@ -75,18 +75,21 @@ class FMM:
             c0 = v.codes - base
             s0 = v.scales - base
             raw = self.ws[c0:c0 + nc]
-            tiled = v.code_layout == FMM_LAYOUT_TILE256x64
-            if tiled:
+            if v.code_layout == FMM_LAYOUT_TILE256x64:
                 codes = _untile256x64(raw, v.batch, v.terms, v.rows, v.kdim)
+                scales = _unpermute_scales256(self.ws[s0:s0 + ns], v.batch, v.terms, v.rows, v.kblocks)
+            elif v.code_layout == FMM_LAYOUT_TILE128x128:
+                codes = _untile128x128(raw, v.batch, v.terms, v.rows, v.kdim)
+                nrec = v.batch * v.terms * v.rows * (v.kdim // 128) * 4
+                scales = _unpack_scales128(self.ws[s0:s0 + nrec], v.batch, v.terms, v.rows, v.kdim,
+                                           v.kblocks)
             else:
                 codes = raw.view(v.batch, v.terms, v.rows, v.kdim)
-            sraw = self.ws[s0:s0 + ns * v.scale_bytes]
-            if v.scale_bytes == 4:
-                scales = sraw.view(torch.float32).view(v.batch, v.terms, v.rows, v.kblocks)
-            elif tiled:
-                scales = _unpermute_scales256(sraw, v.batch, v.terms, v.rows, v.kblocks)
-            else:
-                scales = sraw.view(v.batch, v.terms, v.rows, v.kblocks)
+                sraw = self.ws[s0:s0 + ns * v.scale_bytes]
+                if v.scale_bytes == 4:
+                    scales = sraw.view(torch.float32).view(v.batch, v.terms, v.rows, v.kblocks)
+                else:
+                    scales = sraw.view(v.batch, v.terms, v.rows, v.kblocks)
             out += [codes, scales]
         return tuple(out)
 
@@ -98,6 +101,25 @@ def _untile256x64(raw, batch, terms, rows, kdim):
     chunk = torch.arange(4, device=raw.device)[None, :]
     t = t[:, :, :, :, row, chunk ^ ((row >> 2) & 3), :]      # logical chunk c of tile row
     return t.permute(0, 1, 2, 4, 3, 5, 6).reshape(batch, terms, rows, kdim)
+
+
+def _untile128x128(raw, batch, terms, rows, kdim):
+    """Row-major copy of codes in FMM_LAYOUT_TILE128x128 (see include/fmm8.h)."""
+    t = raw.view(batch, terms, rows // 128, kdim // 128, 128, 8, 16)
+    row = torch.arange(128, device=raw.device)[:, None]
+    chunk = torch.arange(8, device=raw.device)[None, :]
+    t = t[:, :, :, :, row, chunk ^ (row & 7) ^ ((row >> 3) & 1), :]
+    return t.permute(0, 1, 2, 4, 3, 5, 6).reshape(batch, terms, rows, kdim)
+
+
+def _unpack_scales128(raw, batch, terms, rows, kdim, kblocks):
+    """[batch][terms][rows][kblocks] copy of E8M0 scales in FMM_LAYOUT_TILE128x128."""
+    t = raw.view(batch, terms, rows // 128, kdim // 128, 128, 4)
+    if kblocks == kdim // 32:                  # block 32: record order is blocks 0, 2, 1, 3
+        t = t[..., torch.tensor([0, 2, 1, 3], device=raw.device)]
+    else:                                      # block 128: the byte repeated
+        t = t[..., :1]
+    return t.permute(0, 1, 2, 4, 3, 5).reshape(batch, terms, rows, kblocks)
 
 
 def _unpermute_scales256(raw, batch, terms, rows, kblocks):

@@ -136,3 +136,21 @@ def check_case(spec, family, batch, M, K, N, depth, bs, rule, seed=0, cfg=0, tri
     assert abs(rel_gpu / rel_orc - 1) <= MSE_REL_TOL, (rel_gpu, rel_orc)
     return {"rel_mse_gpu": rel_gpu, "rel_mse_oracle": rel_orc, "max_rel_fro": worst_rel_fro,
             "path": "fp8" if mx else "exact"}
+
+
+def oracle_rows(M, table, depth, bs, rule, side, rows):
+    """Codes (T, s, k'), stored scales (T, s, k'/bs) and dequantized values of
+    the given rows of x_r (side 'A') or of y_r^T (side 'B') for every term:
+    the oracle's split / combine / quantize applied to those rows only (the
+    combination is elementwise and quantization runs along each row, so this
+    equals the full encoder's rows)."""
+    blocks = fmm.split(np.asarray(M, dtype=np.float32), depth)
+    if side == "B":                      # rows of y^T are columns of y: combine the transposes
+        blocks = [b.T for b in blocks]
+    sub = [np.ascontiguousarray(b[rows, :]) for b in blocks]
+    codes, scales, deqs = [], [], []
+    for r in range(table.shape[0]):
+        x = fmm.combine(sub, table[r])
+        c, st, _, dq = e4m3.quantize_rows(x, bs, rule)
+        codes.append(c); scales.append(st); deqs.append(dq)
+    return np.stack(codes), np.stack(scales), np.stack(deqs)

@@ -11,7 +11,8 @@ import numpy as np
 import torch
 
 import paper_2609_26077_amd as fm
-from paper_2609_26077_amd.runner import _unpermute_scales256, _untile256x64
+from paper_2609_26077_amd.runner import (_unpack_scales128, _unpermute_scales256, _untile128x128,
+                                          _untile256x64)
 
 HEADER = os.path.join(os.path.dirname(__file__), "..", "include", "fmm8.h")
 
@@ -67,3 +68,49 @@ def test_unpermute_scales_inverts_the_documented_layout():
                     raw[base + (p - tr) + 4 * (32 * h + j) + i] = scales[bi, r, p, k]
     back = _unpermute_scales256(torch.from_numpy(raw), b, T, rows, kb).numpy()
     assert np.array_equal(back, scales)
+
+
+def test_untile128_inverts_the_documented_layout():
+    rng = np.random.default_rng(2)
+    b, T, rows, kdim = 2, 2, 256, 384
+    codes = rng.integers(0, 256, size=(b, T, rows, kdim), dtype=np.uint8)
+    raw = np.empty(codes.size, dtype=np.uint8)
+    pos = 0
+    for bi in range(b):
+        for r in range(T):
+            for tile in range(rows // 128):
+                for ks in range(kdim // 128):
+                    img = np.empty((128, 128), dtype=np.uint8)
+                    for t in range(128):
+                        src = codes[bi, r, 128 * tile + t, 128 * ks:128 * ks + 128]
+                        for c in range(8):
+                            s = c ^ (t & 7) ^ ((t >> 3) & 1)
+                            img[t, 16 * s:16 * s + 16] = src[16 * c:16 * c + 16]
+                    raw[pos:pos + img.size] = img.ravel()
+                    pos += img.size
+    back = _untile128x128(torch.from_numpy(raw), b, T, rows, kdim).numpy()
+    assert np.array_equal(back, codes)
+
+
+def test_unpack_scales128_inverts_the_documented_layout():
+    rng = np.random.default_rng(3)
+    b, T, rows, kdim = 2, 2, 256, 384
+    for block in (32, 128):
+        kb = kdim // block
+        scales = rng.integers(0, 256, size=(b, T, rows, kb), dtype=np.uint8)
+        raw = np.empty(b * T * rows * (kdim // 128) * 4, dtype=np.uint8)
+        pos = 0
+        for bi in range(b):
+            for r in range(T):
+                for tile in range(rows // 128):
+                    for ks in range(kdim // 128):
+                        for t in range(128):
+                            p = 128 * tile + t
+                            if block == 32:
+                                rec = [scales[bi, r, p, 4 * ks + q] for q in (0, 2, 1, 3)]
+                            else:
+                                rec = [scales[bi, r, p, ks]] * 4
+                            raw[pos:pos + 4] = rec
+                            pos += 4
+        back = _unpack_scales128(torch.from_numpy(raw), b, T, rows, kdim, kb).numpy()
+        assert np.array_equal(back, scales), block

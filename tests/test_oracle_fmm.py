@@ -188,3 +188,26 @@ def test_general_gauge_and_the_clamp():
     for alpha in (3.7, 1e-6, 1e-11):
         assert abs(err(_rescaled(D, alpha)) / e0 - 1) < 1e-4
     assert abs(err(_rescaled(D, 1e-13)) / e0 - 1) > 1e-3
+
+
+def test_row_sampled_encoding_matches_the_full_encoder():
+    """The full-size GPU tests encode only sampled rows with the oracle's own
+    split / combine / quantize; at a small size that equals the full encoder's
+    rows, for both sides and every depth."""
+    from tests.gpu_helpers import oracle_rows
+    rng = np.random.default_rng(5)
+    for depth in (1, 2, 3):
+        n = 2 ** depth
+        M, K, N = 16 * n, 64 * n, 8 * n
+        A = (rng.standard_normal((M, K)) * 10.0 ** rng.uniform(-2, 2, (M, 1))).astype(np.float32)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        U, V, W = R.tables_f32(R.builtin_f64("tstar"), depth)
+        ea = fmm.encode_side(A, U, depth, 32, e4m3.RULE_POW2_CEIL, "A")
+        eb = fmm.encode_side(B, V, depth, 32, e4m3.RULE_POW2_CEIL, "B")
+        prow, qrow = np.array([0, 3, 7, 15]), np.array([1, 6])
+        xc, xs, xd = oracle_rows(A, U, depth, 32, e4m3.RULE_POW2_CEIL, "A", prow)
+        yc, ys, yd = oracle_rows(B, V, depth, 32, e4m3.RULE_POW2_CEIL, "B", qrow)
+        assert np.array_equal(xc, ea["codes"][:, prow, :]) and np.array_equal(xs, ea["scales"][:, prow, :])
+        assert np.array_equal(yc, eb["codes"][:, qrow, :]) and np.array_equal(ys, eb["scales"][:, qrow, :])
+        assert np.array_equal(xd, np.stack(ea["deq"])[:, prow, :])
+        assert np.array_equal(yd, np.stack(eb["deq"])[:, qrow, :])
