@@ -63,5 +63,25 @@ __device__ __forceinline__ uint32_t e4m3_pack4(float v0, float v1, float v2, flo
   return (uint32_t)w;
 }
 
+// Codes of four values under a power-of-two scale s = 2^e, e in [-48, 120]:
+// the e4m3 code of x / s with round to nearest even, saturated to 448.
+// v_cvt_scalef32_pk_fp8_f32 divides by the power of two that its scale
+// operand holds (exactly, subnormal binary32 inputs included) and rounds to
+// nearest even, but, like the plain cast, does not saturate; clamping x to
+// +-448 s first is exact because 448 s is.  Where 448 s overflows binary32
+// (e = 120, reached only by the ceiling rule) |x| <= 448 s holds already and
+// the clamp to +-inf is the identity.
+__device__ __forceinline__ uint32_t e4m3_pack4_pow2(float v0, float v1, float v2, float v3, float s) {
+  typedef short v2i16 __attribute__((ext_vector_type(2)));
+  const float lim = 448.0f * s;
+  v0 = __builtin_amdgcn_fmed3f(v0, -lim, lim);
+  v1 = __builtin_amdgcn_fmed3f(v1, -lim, lim);
+  v2 = __builtin_amdgcn_fmed3f(v2, -lim, lim);
+  v3 = __builtin_amdgcn_fmed3f(v3, -lim, lim);
+  v2i16 w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32((v2i16){0, 0}, v0, v1, s, false);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, v2, v3, s, true);
+  return __builtin_bit_cast(uint32_t, w);
+}
+
 }  // namespace dev
 }  // namespace fmm
