@@ -32,13 +32,15 @@ constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slot
                                     // 4 slots, or in 16 consecutive rows, hit 16 distinct
                                     // bank groups
 
-// Tile geometry.  VEC = contracted positions per lane (16 at depths 1-2, 4 at depth 3).
-template <int DEPTH, int VEC>
+// Tile geometry.  VEC = contracted positions per lane (16 at depths 1-2, 4 at
+// depth 3).  At depth 1 the B side takes 32 columns (its rows of B are read as
+// 128-byte segments) with four waves, the A side 16 rows with two.
+template <int DEPTH, int VEC, int SIDE>
 struct Tile {
   static constexpr int nblk = 1 << (2 * DEPTH);
-  static constexpr int TR = VEC == 16 ? (DEPTH == 1 ? 16 : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
-  static constexpr int threads = VEC == 16 && DEPTH == 1 ? 128 : 256;
-  static constexpr int lds_floats = nblk * TR * kStride;   // 33.8, 67.6 KB (VEC 16); 67.6 KB (depth 3)
+  static constexpr int TR = VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
+  static constexpr int threads = VEC == 16 && DEPTH == 1 && SIDE == 0 ? 128 : 256;
+  static constexpr int lds_floats = nblk * TR * kStride;   // 33.8 (A) / 67.6 (B), 67.6, 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
 };
 
@@ -49,7 +51,12 @@ __device__ __forceinline__ float dpp(float v) {
 
 // Read the tile into LDS ([block][row][l], row stride kStride floats).  Every
 // load is issued before the first LDS write, so the workgroup waits for HBM
-// once, not once per element.  Positions outside the operand read as zero.
+// once, not once per element.  The fp32 operands are read exactly once, so
+// the loads are nontemporal (they do not displace the codes, which the
+// sub-product kernel reads next, from the caches).  Positions outside the
+// operand read as zero.
+typedef float f4v __attribute__((ext_vector_type(4)));
+
 template <int SIDE, int NB, int TR, int NT>
 __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__ src, const Problem &pb,
                                            int64_t bt, int64_t row0, int64_t l0, int t) {
@@ -71,7 +78,8 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
       stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (p < rows && l < kp) {
         const int I = b / n, J = b % n;
-        stage[k] = *reinterpret_cast<const float4 *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l);
+        const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l));
+        stage[k] = make_float4(x.x, x.y, x.z, x.w);
       }
     }
 #pragma unroll
@@ -95,10 +103,10 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
       if (qq < rows && l < kp) {
         const int J = b / n, Kb = b % n;
         const float *p = Bb + (J * kp + l) * pb.N + Kb * pb.np + qq;
-        stage[k].x = p[0];
-        stage[k].y = p[pb.N];
-        stage[k].z = p[2 * pb.N];
-        stage[k].w = p[3 * pb.N];
+        stage[k].x = __builtin_nontemporal_load(p);
+        stage[k].y = __builtin_nontemporal_load(p + pb.N);
+        stage[k].z = __builtin_nontemporal_load(p + 2 * pb.N);
+        stage[k].w = __builtin_nontemporal_load(p + 3 * pb.N);
       }
     }
 #pragma unroll
@@ -170,17 +178,17 @@ __device__ __forceinline__ void store_scale(const Problem &pb, uint8_t *scales, 
 // holds row r, positions 16 (4 h + c') .. +15, so a 16-lane group reads 4
 // rows x 4 slots (conflict-free at the odd stride) and a block of 32 is a lane
 // pair (lane, lane ^ 1), a block of 128 the quad plus its partner 32 lanes on.
-// Depth 1: 16 rows, two waves (one per row half), every term; depth 2: 8 rows,
-// four waves, wave w takes terms w, w + 4, ...
+// Depth 1: 16 (A) or 32 (B) rows, one wave per 8 of them, every term; depth 2:
+// 8 rows, four waves, wave w takes terms w, w + 4, ...
 // ---------------------------------------------------------------------------
 template <int SIDE, int DEPTH, int BS, bool F32>
-__global__ __launch_bounds__((Tile<DEPTH, 16>::threads)) void encode16_kernel(
+__global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
-  using TT = Tile<DEPTH, 16>;
+  using TT = Tile<DEPTH, 16, SIDE>;
   constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads;
-  constexpr int WPT = TR * 8 / 64;          // waves per term (2 at depth 1, 1 at depth 2)
+  constexpr int WPT = TR * 8 / 64;          // waves per term (2 or 4 at depth 1, 1 at depth 2)
   constexpr int TSTEP = NT / 64 / WPT;      // terms a workgroup works on at once
   __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
@@ -284,7 +292,7 @@ __global__ __launch_bounds__(256) void encode4_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
-  using TT = Tile<3, 4>;
+  using TT = Tile<3, 4, SIDE>;
   constexpr int TR = TT::TR;
   constexpr int P = TR * (kTL / 4);          // positions (row, 4 consecutive l) per term
   static_assert(256 % P == 0 && P % 64 == 0, "a wave's 64 items belong to one term; a thread keeps one position");
@@ -345,7 +353,7 @@ __global__ __launch_bounds__(256) void encode4_kernel(
 template <int SIDE, int DEPTH, int BS, bool F32>
 hipError_t launch16(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
                     uint8_t *codes, uint8_t *scales, hipStream_t st) {
-  using TT = Tile<DEPTH, 16>;
+  using TT = Tile<DEPTH, 16, SIDE>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
@@ -379,7 +387,7 @@ hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
     case 3: {
       const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
       const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
-      const int64_t tiles_r = (rows + Tile<3, 4>::TR - 1) / Tile<3, 4>::TR;
+      const int64_t tiles_r = (rows + Tile<3, 4, SIDE>::TR - 1) / Tile<3, 4, SIDE>::TR;
       const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
       hipLaunchKernelGGL((encode4_kernel<SIDE>), grid, dim3(256), 0, st, src, pb, off, ent, codes, scales, tiles_l);
       return hipGetLastError();

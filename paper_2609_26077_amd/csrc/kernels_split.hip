@@ -11,7 +11,7 @@
 //      registers each), two per SIMD, run in alternating phases so that one
 //      wave's MFMAs cover the other's LDS reads; 64-byte K steps through a
 //      four-slot LDS ring filled by global_load_lds three steps ahead; P_r is
-//      stored in fp32.
+//      stored in fp32 with nontemporal stores.
 //   2. combine1_kernel: C block (i, k) = sum_r w[r][2k + i] P_r, ascending r,
 //      one fused multiply-add per nonzero weight (the order of the fused
 //      W-combine of the 128 x 128 path).
@@ -210,7 +210,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(SplitArgs g) 
   }
   if (grp == 0) phase(ph++);
 
-  // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32
+  // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32.
+  // The stores are nontemporal: P_r is read once, by the W-combine, and
+  // caching it only displaces the codes the other workgroups still read.
   float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 128) * g.np + pn0 + wn * 64 + r32;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -219,7 +221,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(SplitArgs g) 
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-        out[(int64_t)row * g.np + 32 * j] = acc[i][j][e];
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
       }
 }
 
