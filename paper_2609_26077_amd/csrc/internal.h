@@ -10,7 +10,8 @@ namespace fmm {
 
 constexpr int kMaxRank = 8;    // <2,2,2;R>, R <= 8 (cubic has 8 terms)
 constexpr int kMaxDepth = 3;
-constexpr int kSplitTile = 256; // tile edge of the large-tile sub-product path
+constexpr int kSplitTile = 256;  // A rows per tile of the large-tile sub-product path (and code image rows)
+constexpr int kSplitTileN = 128; // B rows per tile of that path (half a code image)
 
 struct Realization {
   int R;

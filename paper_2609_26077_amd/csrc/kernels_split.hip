@@ -1,16 +1,17 @@
 // Large-tile sub-products for tile-aligned block-scaled problems at depth 1.
 //
 // The sub-products are the dominant cost; each is a plain block-scaled fp8
-// GEMM P_r = A_r B_r^T with fp32 accumulation.  A 256 x 256 tile of P_r
-// halves the operand bytes per MFMA flop of a 128 x 128 tile, which is what
-// bounds the feed from L2 into LDS; the price is that P_r leaves the
-// workgroup, so the W-combine becomes its own bandwidth-bound pass:
+// GEMM P_r = A_r B_r^T with fp32 accumulation.  Large tiles halve the operand
+// bytes per MFMA flop of a 128 x 128 tile, which is what bounds the feed from
+// L2 into LDS; the price is that P_r leaves the workgroup, so the W-combine
+// becomes its own bandwidth-bound pass:
 //
-//   1. gemm_tile256_kernel: one workgroup per (batch, term r, 256 x 256 tile),
-//      eight waves of 128 x 64 (4 x 2 MFMA tiles of 32 x 32, 128 accumulation
-//      registers each), two per SIMD, run in alternating phases so that one
-//      wave's MFMAs cover the other's LDS reads; 64-byte K steps through a
-//      four-slot LDS ring filled by global_load_lds three steps ahead; P_r is
+//   1. gemm_tile256x128_kernel: one workgroup per (batch, term r, 256 x 128
+//      tile), four waves of 128 x 64 (4 x 2 MFMA tiles of 32 x 32, 128
+//      accumulation registers each), one per SIMD, and two workgroups per CU:
+//      while one waits (LDS reads, a barrier, its epilogue) the other's MFMAs
+//      keep the SIMDs busy.  64-byte K steps run through a three-slot LDS ring
+//      filled by global_load_lds two steps ahead, one barrier per step; P_r is
 //      stored in fp32 with nontemporal stores.
 //   2. combine1_kernel: C block (i, k) = sum_r w[r][2k + i] P_r, ascending r,
 //      one fused multiply-add per nonzero weight (the order of the fused
@@ -21,7 +22,9 @@
 // tile so that row 128 wm + 32 i + r sits at byte 4 (32 wm + r) + i.  One
 // 32-bit LDS read then gives a lane the scales of its four A row tiles (or,
 // shifted by 16 (wn & 1) bits, of its two B row tiles), and the MFMA's op_sel
-// picks the byte of each tile.
+// picks the byte of each tile.  A 128-row B tile is one half of a 256-row
+// tile: the contiguous 8 KB half of each code image and the contiguous 128
+// bytes 128 h .. 128 h + 127 of each K block's scales.
 #include <hip/hip_runtime.h>
 
 #include "device.h"
@@ -35,23 +38,28 @@ namespace {
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr int TT = kSplitTile;        // tile edge in rows of A_r and of B_r
+constexpr int TM = kSplitTile;        // tile rows of A_r (and rows of one code image)
+constexpr int TN = kSplitTileN;       // tile rows of B_r: half an image
 constexpr int SK = 64;                // contracted bytes per step
-constexpr int kThreads = 512;
-constexpr int kSlots = 4;
-constexpr int kCode = TT * SK;        // 16 KB of codes per operand per step
-constexpr int kScale = 2 * TT;        // two K blocks x 256 rows of scale bytes per operand
-constexpr int kSlot = 2 * kCode + 2 * kScale;
+constexpr int kThreads = 256;
+constexpr int kSlots = 3;
+constexpr int kCodeA = TM * SK;       // 16 KB of A codes per step
+constexpr int kCodeB = TN * SK;       // 8 KB of B codes per step
+constexpr int kImage = TM * SK;       // one (256-row tile, k-step) code image
+constexpr int kScaleA = 2 * TM;       // two K blocks x 256 rows of scale bytes
+constexpr int kScaleB = 2 * TN;       // two K blocks x 128 rows
+constexpr int kSlot = kCodeA + kCodeB + kScaleA + kScaleB;   // 25344 B; two workgroups fit in LDS
+static_assert(2 * kSlots * kSlot <= 160 * 1024, "two workgroups per CU");
 
 struct SplitArgs {
   const uint8_t *xa, *xb;      // codes [batch][T][rows / 256][kp / 64][256 x 64 tile image]
-  const uint8_t *sat, *sbt;    // scales [batch][T][kblocks][rows] (rows permuted per tile)
+  const uint8_t *sat, *sbt;    // scales [batch][T][kblocks][rows] (rows permuted per 256-row tile)
   float *P;                    // products [batch][T][mp][np]
   int64_t mp, np, kp, kblocks, T;
-  int tiles_m, tiles_n;
+  int tiles_m, tiles_n;        // mp / 256, np / 128
 };
 
-// LDS tile of one operand: 256 rows x 64 bytes; 16-byte chunk c of row r sits
+// LDS image of one operand: rows x 64 bytes; 16-byte chunk c of row r sits
 // at chunk c ^ ((r >> 2) & 3), so the 16 rows of a 16-lane fragment read fall
 // on 16 distinct bank groups of the 64 banks.  The encoder writes the codes of
 // these plans in exactly this image, one contiguous 16 KB block per
@@ -100,57 +108,67 @@ __device__ __forceinline__ void work_of(int bid, int64_t nitems, int64_t T, int 
 }
 
 template <int BS>
-__global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(SplitArgs g) {
+__global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs g) {
   __shared__ uint4 lds_raw[kSlots * kSlot / 16];
   const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
   const uint32_t lds_base = dma::lds_addr(lds_raw);
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wm = wave >> 2, wn = wave & 3;       // A rows 128 wm.., B rows 64 wn..
+  const int wm = wave >> 1, wn = wave & 1;       // A rows 128 wm.., B rows 64 wn.. of the tile
   const int r32 = lane & 31, h = lane >> 5;
   const int64_t nitems = (int64_t)gridDim.x;
   int64_t bt, r;
   int tm, tn;
   work_of(blockIdx.x, nitems, g.T, g.tiles_m, g.tiles_n, bt, r, tm, tn);
-  const int64_t pm0 = (int64_t)tm * TT, pn0 = (int64_t)tn * TT;
+  const int64_t pm0 = (int64_t)tm * TM, pn0 = (int64_t)tn * TN;
+  const int hb = tn & 1;                          // half of the 256-row B tile
   const int nk = (int)(g.kp / SK);
-  // codes arrive tiled: the 16 KB image of (tile, k-step) is contiguous, so a
+  // codes arrive tiled: the image of (256-row tile, k-step) is contiguous, so a
   // transfer is a straight 1 KB copy (lane l moves bytes 16 l .. 16 l + 15)
-  const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kCode;
-  const uint8_t *xb = g.xb + ((bt * g.T + r) * g.tiles_n + tn) * (int64_t)nk * kCode;
+  const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kImage;
+  const uint8_t *xb = g.xb + ((bt * g.T + r) * (g.tiles_n / 2) + (tn >> 1)) * (int64_t)nk * kImage + hb * kCodeB;
   const uint32_t code_off = 16u * (uint32_t)lane;
-  // scale transfer of this wave: operand (wave & 3) / 2 (A, B), K block
-  // 2 step + (wave & 1) (block 32) or step / 2 (block 128); waves w and w + 4,
-  // and at block 128 also w and w + 1, move the same bytes
-  const bool s_is_b = (wave & 3) >= 2;
-  const int seg = BS == 32 ? (wave & 1) : 0;
+  // the six 1 KB regions wave w moves each step: regions 6 w .. 6 w + 5 of
+  // the slot's codes, 0..15 from A's image, 16..23 from B's half image
+  const uint8_t *csrc[6];
+  uint32_t cdst[6];
+#pragma unroll
+  for (int j = 0; j < 6; ++j) {
+    const int region = wave * 6 + j;
+    csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
+    cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
+  }
+  // scale transfer of this wave (256 bytes, lane l moves 4):
+  //   wave 0 / 1: A scale bytes of K block 2 step + wave (block 32) or step / 2
+  //   wave 2 / 3: B scale bytes of the tile's half, lanes 32 k' .. of K block
+  //               2 step + k' (block 32), or of block step / 2 in both halves
+  //               of the lanes (block 128); waves 2 and 3 move the same bytes
+  const bool s_is_b = wave >= 2;
   const int64_t srows = s_is_b ? g.np : g.mp;
-  const uint8_t *sbase = s_is_b ? g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0
-                                : g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0;
+  const uint8_t *ssrc = s_is_b ? g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0   // bytes 128 hb .. of the 256-row tile
+                               : g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0 + (BS == 32 ? wave * g.mp : 0);
+  const uint32_t s_off = s_is_b ? 4u * (uint32_t)r32 + (BS == 32 ? (uint32_t)(h * g.np) : 0u) : 4u * (uint32_t)lane;
+  const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_b ? kScaleA : (BS == 32 ? wave * TM : 0)));
 
   auto issue = [&](int step) {
-    const int64_t src = (int64_t)step * kCode;
-    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
+    const uint32_t m0 = lds_base + (uint32_t)(step % kSlots) * kSlot;
+    const int64_t src = (int64_t)step * kImage;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int region = wave * 2 + j;             // 1 KB = tile rows 16 region .. + 15
-      dma::copy16(code_off, xa + src + region * 1024, m0 + region * 1024);
-      dma::copy16(code_off, xb + src + region * 1024, m0 + kCode + region * 1024);
-    }
-    const int64_t kb = BS == 32 ? 2 * (int64_t)step + seg : step / 2;
-    dma::copy4(4u * (uint32_t)lane, sbase + kb * srows,
-               m0 + 2 * kCode + (s_is_b ? kScale : 0) + seg * TT);
+    for (int j = 0; j < 6; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
+    const int64_t kb = BS == 32 ? 2 * (int64_t)step : step / 2;
+    dma::copy4(s_off, ssrc + kb * srows, m0 + sdst);
   };
 
-  // LDS -> registers for one step (slot step % 4; any step index reads in bounds)
+  // LDS -> registers for one step (any step index reads in bounds)
   auto load = [&](int step, Frags &f) {
-    const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
-    const uint8_t *lb = la + kCode;
-    const int sseg = BS == 32 ? h * TT : 0;     // block 2 step + h, or step / 2
-    f.sa = *reinterpret_cast<const uint32_t *>(la + 2 * kCode + sseg + 4 * (wm * 32 + r32));
-    // B row 64 wn + 32 j + r is row 128 (wn / 2) + 32 (2 (wn & 1) + j) + r of the tile
-    f.sb = *reinterpret_cast<const uint32_t *>(la + 2 * kCode + kScale + sseg + 4 * ((wn >> 1) * 32 + r32)) >>
-           (16 * (wn & 1));
+    const uint8_t *la = lds + (step % kSlots) * kSlot;
+    const uint8_t *lb = la + kCodeA;
+    const uint8_t *ls = lb + kCodeB;
+    // A: block 2 step + h (block 32) or step / 2 at bytes h TM .. (block 32) / 0 ..;
+    // B: the 128 bytes of K block 2 step + h at 128 h (block 32) / 0 (block 128)
+    f.sa = *reinterpret_cast<const uint32_t *>(ls + (BS == 32 ? h * TM : 0) + 4 * (wm * 32 + r32));
+    // B row 64 wn + 32 j + r of the half is row 128 hb + 32 (2 wn + j) + r of the 256-row tile
+    f.sb = *reinterpret_cast<const uint32_t *>(ls + kScaleA + (BS == 32 ? h * TN : 0) + 4 * r32) >> (16 * wn);
 #pragma unroll
     for (int i = 0; i < 4; ++i) f.a[i] = frag64(la, wm * 128 + 32 * i + r32, h);
 #pragma unroll
@@ -172,43 +190,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_tile256_kernel(SplitArgs g) 
 #undef FMM_MFMA_IJ
   };
 
-  // Two phases per step, separated by barriers.  Waves w and w + 4 share a
-  // SIMD and sit in different groups: in every phase one group reads a
-  // step's fragments from LDS while the other runs its MFMAs on the fragments
-  // it read in the phase before, so each SIMD always has a wave issuing MFMAs.
-  //   phase 2s:     group 0 reads step s;   group 1 multiplies step s - 1
-  //   phase 2s + 1: group 0 multiplies s;   group 1 reads step s
-  // Steps 0, 1, 2 are in flight at the start; at phase 2s every wave waits for
-  // its own transfers of step s (five a step) and, after the barrier, starts
-  // step s + 3 into the slot of step s - 1, which group 1 finished reading in
-  // phase 2s - 1.
-  // Every wave runs the same sequence (phase, read s, phase, multiply s);
-  // group 1 starts one phase late and group 0 ends one phase late, so both
-  // pass 2 nk + 1 barriers.  An even phase 2s begins with the wait for the
-  // wave's own transfers of step s (five a step) and, after its barrier,
-  // starts step s + 3.
-  auto phase = [&](int ph) {
-    if ((ph & 1) == 0) {
-      const int s = ph >> 1;
-      if (s + 2 < nk) dma::wait_vmcnt<10>(); else if (s + 1 < nk) dma::wait_vmcnt<5>(); else dma::wait_vmcnt<0>();
-    }
-    __syncthreads();
-    if ((ph & 1) == 0 && (ph >> 1) + 3 < nk) issue((ph >> 1) + 3);
-  };
-  const int grp = wave >> 2;
+  // Step s: wait for this wave's own transfers of step s (seven a step; those
+  // of step s + 1 may stay in flight), barrier (every wave's transfers of s
+  // have landed, and every wave has read step s - 1), start step s + 2 into
+  // the slot of step s - 1, read step s, multiply.
   issue(0);
   if (nk > 1) issue(1);
-  if (nk > 2) issue(2);
-  int ph = 0;
-  if (grp == 1) phase(ph++);
   for (int step = 0; step < nk; ++step) {
+    if (step + 1 < nk) dma::wait_vmcnt<7>(); else dma::wait_vmcnt<0>();
+    __syncthreads();
+    if (step + 2 < nk) issue(step + 2);
     Frags f;
-    phase(ph++);
     load(step, f);
-    phase(ph++);
     mfma(f);
   }
-  if (grp == 0) phase(ph++);
 
   // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32.
   // The stores are nontemporal: P_r is read once, by the W-combine, and
@@ -282,13 +277,13 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
   g.sbt = ws + wl.b_scales;
   g.P = reinterpret_cast<float *>(const_cast<uint8_t *>(ws) + wl.products);
   g.mp = pb.mp; g.np = pb.np; g.kp = pb.kp; g.kblocks = pb.kblocks; g.T = pb.T;
-  g.tiles_m = (int)(pb.mp / TT);
-  g.tiles_n = (int)(pb.np / TT);
+  g.tiles_m = (int)(pb.mp / TM);
+  g.tiles_n = (int)(pb.np / TN);
   const int64_t items = pb.batch * pb.T * g.tiles_m * g.tiles_n;
   if (pb.block == 32)
-    hipLaunchKernelGGL(gemm_tile256_kernel<32>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+    hipLaunchKernelGGL(gemm_tile256x128_kernel<32>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
   else
-    hipLaunchKernelGGL(gemm_tile256_kernel<128>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+    hipLaunchKernelGGL(gemm_tile256x128_kernel<128>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
   return hipGetLastError();
 }
 

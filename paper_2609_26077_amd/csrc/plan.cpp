@@ -99,7 +99,7 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.split = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
              q.depth == 1 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
              pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
-             q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTile) < (int64_t(1) << 31);
+             q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);
   // fused 128 x 128 path: E8M0 scales, whole 128-row tiles and 128-byte K steps
   const bool tile128 = mx && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 && pb.kp % 128 == 0 &&
                        pb.kp < (int64_t(1) << 26);
