@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--family", default="gaussian")
     p.add_argument("--exact-dot", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-arms", action="store_true",
+                   help="skip the comparison arms (cubic and Strassen realizations, heavy-tailed operands)")
+    p.add_argument("--arm-steps", type=int, default=20)
     p.add_argument("--cpu-sample", type=int, default=4096,
                    help="edge of the cubic products the oracle is timed on")
     p.add_argument("--cpu-trials", type=int, default=6)
@@ -97,6 +100,58 @@ def kernel_source_hash():
         with open(os.path.join(csrc, name), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def time_arm(f, dA, dB, C, stream, steps, warmup):
+    """Mean and median wall of `steps` whole steps (encode, sub-products,
+    W-combine) from HIP events on the launch stream, after `warmup` steps."""
+    import torch
+    for _ in range(warmup):
+        f.matmul(dA, dB, C, stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record(stream)
+        f.matmul(dA, dB, C, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev])
+    return float(t.mean()), float(np.median(t))
+
+
+def other_arms(args, dA, dB, C, stream):
+    """The comparison arms on the same code path and workload size: the cubic
+    (8-product) and Strassen 1969 realizations on the same Gaussian operands,
+    and the default realization on heavy-tailed operands (Student-t, 3 degrees
+    of freedom, unit variance).  Each: effective TFLOP/s from the mean event
+    time of whole steps, and the relative RMS error against fp64."""
+    import torch
+    import fmm_inputs as gen
+    from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
+    n = args.size
+    mkn = 2.0 * n ** 3
+    out = {}
+    arms = [("cubic8", "gaussian"), ("strassen", "gaussian"), (args.realization, "student_t3")]
+    for real, family in arms:
+        if real == args.realization and family == args.family:
+            continue
+        if family != args.family:
+            A, B = gen.operands(family, 1, n, n, n, seed=0, cfg=0, trial=0)
+            xa, xb = torch.from_numpy(A).to(dA.device), torch.from_numpy(B).to(dA.device)
+            del A, B
+        else:
+            xa, xb = dA, dB
+        f = FMM(real, 1, n, n, n, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
+        mean_ms, med_ms = time_arm(f, xa, xb, C, stream, args.arm_steps, 5)
+        Cref = reference_f64(xa, xb)
+        err2, ref2 = error_stats(C, Cref)
+        del Cref, f
+        out[f"{real}/{family}"] = {"value": mkn / (mean_ms * 1e-3) / 1e12, "unit": "TFLOP/s",
+                                   "ms_per_step": mean_ms, "median_ms": med_ms,
+                                   "rel_rms_error_vs_fp64": float(np.sqrt(err2.sum() / ref2.sum())),
+                                   "steps": args.arm_steps}
+        torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(args):
@@ -178,6 +233,7 @@ def main():
         ev[s][3].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
+    step_ms = np.array([e[0].elapsed_time(e[3]) for e in ev])
     enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     prod_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
     comb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
@@ -207,7 +263,7 @@ def main():
     peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \
         else FP8_DENSE_PEAK_TFLOPS
     achieved = mfma_flop / (prod_ms * 1e-3) / 1e12
-    traffic = recorded_traffic("gemm_tile256" if split else "gemm_mx_fast", M, args)
+    traffic = recorded_traffic("gemm_tile256x128" if split else "gemm_mx_fast", M, args)
 
     def hbm(nbytes, ms):
         gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
@@ -239,6 +295,8 @@ def main():
         "rel_rms_error_vs_fp64": float(np.sqrt(rel_mse)),
         "rel_mse_vs_fp64": rel_mse,
         "kernels_ms": {"encode": enc_ms, "products": prod_ms, "combine": comb_ms},
+        "step_event_ms": {"median": float(np.median(step_ms)), "min": float(step_ms.min()),
+                          "mean": float(step_ms.mean())},
         "roofline": {"bound": "mfma", "kernel": "fp8 sub-product GEMM (fmm_products)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
@@ -249,6 +307,8 @@ def main():
     }
     if split:
         line["combine_roofline"] = hbm(comb_bytes, comb_ms)
+    if not args.no_arms:
+        line["arms"] = other_arms(args, dA, dB, C, stream)
     if not args.no_cpu_baseline:
         del dA, dB, C
         torch.cuda.empty_cache()

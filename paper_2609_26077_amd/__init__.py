@@ -12,6 +12,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfmm8.so")
@@ -153,13 +154,18 @@ def _stream(stream):
 class Realization:
     """Owns an fmm_real handle."""
 
+    # bound here, not looked up at collection time: module globals may already
+    # be gone while the interpreter shuts down, when handles are left to the OS
+    _destroy = _lib.fmm_realization_destroy
+    _finalizing = sys.is_finalizing
+
     def __init__(self, handle: int):
         self.handle = handle
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
-        if h:
-            _lib.fmm_realization_destroy(h)
+        if h and not self._finalizing():
+            self._destroy(h)
 
 
 def fmm_realization_builtin(which) -> Realization:
@@ -248,14 +254,17 @@ def fmm_realization_tables(d: Realization, depth: int = 1):
 class Plan:
     """Owns an fmm_plan handle and remembers its descriptor."""
 
+    _destroy = _lib.fmm_plan_destroy
+    _finalizing = sys.is_finalizing
+
     def __init__(self, handle: int, desc: fmm_plan_desc):
         self.handle = handle
         self.desc = desc
 
     def __del__(self):
         h, self.handle = getattr(self, "handle", None), None
-        if h:
-            _lib.fmm_plan_destroy(h)
+        if h and not self._finalizing():
+            self._destroy(h)
 
 
 def make_desc(batch, M, K, N, depth=1, block=32, rule="pow2_ceil", exact_dot=False,
