@@ -89,3 +89,13 @@ def basis_change(rng: np.random.Generator, scale: float = 0.45,
 def basis_changes(count: int, seed: int = 0, cfg: int = 4):
     """``count`` basis changes; change i is drawn from key [seed, cfg, i, 4]."""
     return [basis_change(generator(seed, cfg, i, OPERAND_G)) for i in range(count)]
+
+
+def rebasing_starts(count: int, seed: int = 0, cfg: int = 6) -> np.ndarray:
+    """``count`` re-basing starts as a (count, 12) float64 array: row i is
+    (X, Y, Z) of basis change i (drawn as in ``basis_changes`` from key
+    [seed, cfg, i, 4]), each 2x2 flattened row-major."""
+    out = np.empty((count, 12), dtype=np.float64)
+    for i, g in enumerate(basis_changes(count, seed=seed, cfg=cfg)):
+        out[i] = np.concatenate([m.reshape(-1) for m in g])
+    return out
