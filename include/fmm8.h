@@ -170,6 +170,33 @@ int fmm_realization_transform(const fmm_real *d, const double X[4], const double
  * (U_r, V_r, W_r) -> (U_r / s_r, s_r V_r, W_r), s_r = sqrt(|U_r| / |V_r|). */
 int fmm_realization_rebalance(const fmm_real *d, fmm_real **out);
 
+/* Re-basing (Section 3.1; the protocol of Appendix E.2): minimize Phi over
+ * the change-of-basis orbit D . g, g = (X, Y, Z) in GL(2)^3 (eq. A.1).
+ * Starts: g = (I, I, I) (the realization itself) and, for s < nstarts, the
+ * caller's triple starts[12 s .. 12 s + 11] = (X, Y, Z), each 2x2 row-major
+ * (the paper draws X, Y, Z as I + 0.45 N(0,1) and rejects |det| < 1e-3; the
+ * caller does the drawing).  Each start runs limited-memory BFGS (memory 10)
+ * with a strong-Wolfe line search (c1 = 1e-4, c2 = 0.9) in binary64 over the
+ * 12 entries of g, with the exact gradient, until the largest gradient entry
+ * is at most gtol * max(1, Phi), progress falls below rounding, or max_iter
+ * iterations.  The terminal g gives D . g by fmm_realization_transform's
+ * arithmetic; among the terminal realizations with a finite Phi and a Brent
+ * residual <= tol, the one with the least Phi (the earliest start on ties)
+ * is returned in *out (a new handle), its Phi in *phi (may be NULL).
+ * start_phi (may be NULL; 1 + nstarts entries) receives each start's terminal
+ * Phi, NaN where it was singular or failed the exactness check.
+ * Errors: FMM_ERR_ARG (null d or out; nstarts < 0; starts NULL while
+ * nstarts > 0; max_iter < 1; gtol <= 0; tol < 0 or NaN); FMM_ERR_NOT_EXACT
+ * if no start ends exact within tol.  Host only. */
+int fmm_realization_optimize(const fmm_real *d, int nstarts, const double *starts, int max_iter,
+                             double gtol, double tol, fmm_real **out, double *phi, double *start_phi);
+
+/* Phi(D . g) for g = (X, Y, Z) = g[0..3], g[4..7], g[8..11] (row-major 2x2
+ * each; eq. A.1) and its gradient with respect to those 12 entries, the
+ * objective fmm_realization_optimize minimizes.  phi may be NULL.  Errors:
+ * FMM_ERR_ARG (null d, g or grad).  A singular g gives non-finite values. */
+int fmm_realization_phi_gradient(const fmm_real *d, const double g[12], double *phi, double grad[12]);
+
 /* Phi = sum_r |U_r|^2 |V_r|^2 |W_r|^2 and Gamma = sum_r |U_r||V_r||W_r|
  * (Section 2.1) of the depth-l flattening (Phi^l, Gamma^l), and the Brent
  * residual of the base realization.  Any output pointer may be NULL. */

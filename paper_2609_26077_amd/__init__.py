@@ -79,6 +79,9 @@ _SIGS = {
                                               ctypes.POINTER(_vp)]),
     "fmm_realization_transform": (ctypes.c_int, [_vp, _dp, _dp, _dp, ctypes.POINTER(_vp)]),
     "fmm_realization_rebalance": (ctypes.c_int, [_vp, ctypes.POINTER(_vp)]),
+    "fmm_realization_optimize": (ctypes.c_int, [_vp, ctypes.c_int, _dp, ctypes.c_int, ctypes.c_double,
+                                                ctypes.c_double, ctypes.POINTER(_vp), _dp, _dp]),
+    "fmm_realization_phi_gradient": (ctypes.c_int, [_vp, _dp, _dp, _dp]),
     "fmm_realization_metrics": (ctypes.c_int, [_vp, ctypes.c_int, _dp, _dp, _dp]),
     "fmm_realization_terms": (ctypes.c_int, [_vp, ctypes.c_int, ctypes.POINTER(_i64),
                                              ctypes.POINTER(_i64)]),
@@ -204,6 +207,37 @@ def fmm_realization_transform(d: Realization, X, Y, Z) -> Realization:
     _check(_lib.fmm_realization_transform(d.handle, Xp, Yp, Zp, ctypes.byref(h)),
            "fmm_realization_transform")
     return Realization(h.value)
+
+
+def fmm_realization_optimize(d: Realization, starts=None, max_iter: int = 1000, gtol: float = 1e-10,
+                             tol: float = 1e-9):
+    """Re-basing: (realization of least Phi, its Phi, per-start terminal Phi).
+    starts: None or an (n, 12) array of (X, Y, Z) triples, row-major 2x2 each;
+    the identity start is always run first."""
+    import numpy as np
+    if starts is None:
+        n, sp = 0, None
+    else:
+        sa = np.ascontiguousarray(starts, dtype=np.float64).reshape(-1, 12)
+        n, sp = sa.shape[0], sa.ctypes.data_as(_dp)
+    start_phi = np.empty(n + 1, dtype=np.float64)
+    phi = ctypes.c_double()
+    h = _vp()
+    _check(_lib.fmm_realization_optimize(d.handle, n, sp, int(max_iter), float(gtol), float(tol),
+                                         ctypes.byref(h), ctypes.byref(phi),
+                                         start_phi.ctypes.data_as(_dp)), "fmm_realization_optimize")
+    return Realization(h.value), phi.value, start_phi
+
+
+def fmm_realization_phi_gradient(d: Realization, g):
+    """(Phi(D . g), gradient over the 12 entries of g = (X, Y, Z))."""
+    import numpy as np
+    ga, gp = _darr(g, 12)
+    grad = np.empty(12, dtype=np.float64)
+    phi = ctypes.c_double()
+    _check(_lib.fmm_realization_phi_gradient(d.handle, gp, ctypes.byref(phi), grad.ctypes.data_as(_dp)),
+           "fmm_realization_phi_gradient")
+    return phi.value, grad
 
 
 def fmm_realization_rebalance(d: Realization) -> Realization:

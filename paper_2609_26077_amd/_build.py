@@ -13,7 +13,7 @@ LIB = os.path.join(HERE, "libfmm8.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
-SOURCES = ["realization.cpp", "plan.cpp", "kernels_encode.hip", "kernels_gemm.hip",
+SOURCES = ["realization.cpp", "optimize.cpp", "plan.cpp", "kernels_encode.hip", "kernels_gemm.hip",
            "kernels_split.hip", "kernels_measure.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",

@@ -27,6 +27,11 @@ int realization_transform(const Realization &d, const double X[4], const double 
 void realization_rebalance(const Realization &d, Realization &out);
 void realization_phi_gamma(const Realization &d, double &phi, double &gamma);
 int64_t ipow(int64_t b, int e);
+// Phi(D . g) and its gradient over the 12 entries of g = (X, Y, Z)
+double rebase_phi_grad(const Realization &D, const double g[12], double grad[12]);
+// re-basing from the identity and nstarts caller starts (fmm_realization_optimize)
+int realization_optimize(const Realization &D, int nstarts, const double *starts, int max_iter,
+                         double gtol, double tol, Realization &best, double &best_phi, double *start_phi);
 void flatten(const double (*base)[4], int R, int depth, float *out);
 
 // ---- device-side coefficient tables -------------------------------------

@@ -143,3 +143,69 @@ def test_status_strings(fm):
     for s in range(0, -10, -1):
         assert fm.fmm_status_string(s) != "unknown status"
     assert fm.fmm_status_string(-99) == "unknown status"
+
+
+# ---- re-basing (fmm_realization_optimize, fmm_realization_phi_gradient) -----
+
+PHI_MIN = 200.0 / 9.0
+GAMMA_MIN = 2.0 * np.sqrt(2.0) + 16.0 / np.sqrt(3.0)
+
+
+@pytest.mark.parametrize("name", ["strassen", "winograd", "tstar", "cubic8"])
+def test_phi_gradient_matches_oracle(fm, name):
+    from oracle import rebase as RB
+    d = fm.fmm_realization_builtin(name)
+    D = R.builtin_f64(name)
+    for x in [RB.IDENTITY] + list(gen.rebasing_starts(6, seed=11)):
+        phi, grad = fm.fmm_realization_phi_gradient(d, x)
+        ophi, ograd = RB.phi_and_grad(D, x)
+        assert phi == pytest.approx(ophi, rel=1e-13)
+        assert np.max(np.abs(grad - ograd)) <= 1e-11 * max(1.0, np.max(np.abs(ograd)))
+
+
+@pytest.mark.parametrize("name", ["strassen", "winograd"])
+def test_optimize_matches_oracle(fm, name):
+    from oracle import rebase as RB
+    starts = gen.rebasing_starts(23, seed=0)
+    best, phi, start_phi = fm.fmm_realization_optimize(fm.fmm_realization_builtin(name), starts)
+    obest, ophi, oterm = RB.rebase(R.builtin_f64(name), starts)
+    # the minimum value is unique (Theorem 1); the minimizer is not (gauge orbit)
+    assert phi == pytest.approx(ophi, rel=1e-12)
+    assert phi == pytest.approx(PHI_MIN, rel=1e-12)
+    assert np.allclose(start_phi, oterm, rtol=1e-10, atol=0)
+    m = fm.fmm_realization_metrics(best, 1)
+    assert m["phi"] == pytest.approx(phi, rel=1e-15)
+    assert m["gamma"] == pytest.approx(GAMMA_MIN, rel=1e-10)
+    assert m["brent_residual"] <= 1e-12
+
+
+def test_optimize_random_orbit_points(fm):
+    t = fm.fmm_realization_builtin("tstar")
+    for x in gen.rebasing_starts(4, seed=13):
+        X, Y, Z = x.reshape(3, 2, 2)
+        d = fm.fmm_realization_transform(t, X, Y, Z)
+        assert fm.fmm_realization_metrics(d, 1)["phi"] > PHI_MIN * (1 + 1e-3)
+        best, phi, _ = fm.fmm_realization_optimize(d)
+        assert phi == pytest.approx(PHI_MIN, rel=1e-12)
+        assert fm.fmm_realization_metrics(best, 1)["brent_residual"] <= 1e-12
+
+
+def test_optimize_argument_and_exactness_errors(fm):
+    import ctypes
+    d = fm.fmm_realization_builtin("strassen")
+    out, phi = ctypes.c_void_p(), ctypes.c_double()
+    starts = gen.rebasing_starts(1, seed=0)
+    sp = starts.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    lib = fm._lib
+    assert lib.fmm_realization_optimize(d.handle, -1, None, 10, 1e-10, 1e-9, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_realization_optimize(d.handle, 1, None, 10, 1e-10, 1e-9, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_realization_optimize(d.handle, 1, sp, 0, 1e-10, 1e-9, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_realization_optimize(d.handle, 1, sp, 10, 0.0, 1e-9, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_realization_optimize(d.handle, 1, sp, 10, 1e-10, -1.0, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_realization_optimize(None, 1, sp, 10, 1e-10, 1e-9, ctypes.byref(out), None, None) == fm.FMM_ERR_ARG
+    # a realization that is not a <2,2,2> algorithm: no start ends exact
+    U, V, W = (np.array(M) for M in R.builtin_f64("strassen"))
+    U[2, 0] = -U[2, 0]
+    bad = fm.fmm_realization_create(U, V, W, tol=10.0)
+    st = lib.fmm_realization_optimize(bad.handle, 1, sp, 100, 1e-10, 1e-9, ctypes.byref(out), ctypes.byref(phi), None)
+    assert st == fm.FMM_ERR_NOT_EXACT and not out.value
