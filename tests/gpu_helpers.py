@@ -37,10 +37,13 @@ MSE_REL_TOL = 0.01
 
 
 def oracle_realization(spec):
-    """spec: a builtin name, or (name, (X, Y, Z)) for a transformed one."""
+    """spec: a builtin name, (name, (X, Y, Z)) for a transformed one, or
+    ("coeffs", (U, V, w)) for explicit binary64 coefficient arrays."""
     if isinstance(spec, str):
         return R.builtin_f64(spec)
     name, g = spec
+    if name == "coeffs":
+        return tuple(np.asarray(M, dtype=np.float64) for M in g)
     return R.act_f64(R.builtin_f64(name), g)
 
 
@@ -48,7 +51,11 @@ def gpu_realization(spec):
     import paper_2609_26077_amd as fm
     if isinstance(spec, str):
         return fm.fmm_realization_builtin(spec)
-    name, (X, Y, Z) = spec
+    name, g = spec
+    if name == "coeffs":
+        U, V, W = g
+        return fm.fmm_realization_create(U, V, W, tol=1e-9)
+    X, Y, Z = g
     return fm.fmm_realization_transform(fm.fmm_realization_builtin(name), X, Y, Z)
 
 

@@ -68,6 +68,23 @@ def test_transformed_realizations():
             print(i, r, flush=True)
 
 
+def test_rebased_realization():
+    """The oracle's re-basing of Strassen (Appendix E.2 protocol: identity and
+    23 perturbed starts, least exact terminal Phi), in the canonical gauge,
+    through the whole path; and the intervention it exists for: re-basing
+    lowers the measured error (Phi 32 -> 200/9; the oracle gives an RMS ratio
+    of 1.148 on these operands)."""
+    from oracle import realizations as R
+    from oracle import rebase as RB
+    best, phi, _ = RB.rebase(R.builtin_f64("strassen"), gen.rebasing_starts(23, seed=0))
+    assert abs(phi - 200 / 9) < 1e-12
+    r = check_case(("coeffs", R.rebalance_f64(best)), "uniform", 2, 512, 512, 512, 1, 32, 1, seed=2, cfg=7)
+    r0 = check_case("strassen", "uniform", 2, 512, 512, 512, 1, 32, 1, seed=2, cfg=7)
+    ratio = np.sqrt(r0["rel_mse_gpu"] / r["rel_mse_gpu"])
+    print("re-based", r, "strassen", r0, "RMS ratio", ratio, flush=True)
+    assert ratio > 1.1
+
+
 def test_rowscaled_family():
     """Per-row log-uniform scales over four decades stress the blocks along K."""
     for depth in (1, 2, 3):
