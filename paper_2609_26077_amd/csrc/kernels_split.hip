@@ -37,6 +37,7 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 constexpr int TM = kSplitTile;        // tile rows of A_r (and rows of one code image)
 constexpr int TN = kSplitTileN;       // tile rows of B_r: half an image
@@ -241,7 +242,9 @@ __global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__
 #pragma unroll
   for (int r = 0; r < kMaxRank; ++r) {
     if (r < pb.T) {
-      const float4 v = *reinterpret_cast<const float4 *>(P + ((bt * pb.T + r) * pb.mp + p) * pb.np + 4 * q4);
+      // P_r is dead after this read: nontemporal, so it does not displace C in the caches
+      const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(P + ((bt * pb.T + r) * pb.mp + p) * pb.np + 4 * q4));
+      const float4 v = make_float4(x.x, x.y, x.z, x.w);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float wq = wr[r][q];
