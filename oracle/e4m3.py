@@ -193,3 +193,52 @@ def quantize_rows(x, bs: int, rule: int):
     deq = (decode(codes).reshape(rows, kdim // bs, bs)
            * s[:, :, None].astype(np.float64)).reshape(rows, kdim)
     return codes, stored, s, deq
+
+
+# ---------------------------------------------------------------------------
+# Deployment-granularity pieces (Appendix E, weight-scale granularity):
+# bfloat16 pre-rounding of an encoded weight combination, and block scales
+# shared by a run of rows as well as a run of the contracted axis.
+# ---------------------------------------------------------------------------
+
+def bf16_round(x) -> np.ndarray:
+    """float32 values rounded to the nearest bfloat16 value (8 significant
+    bits, the float32 exponent range), ties to the even mantissa; returned
+    as float32.  For x != 0 let e = max(floor(log2 |x|), -126); the
+    bfloat16 values in [2^e, 2^(e+1)) (or below 2^-126, the subnormals) are
+    the multiples of q = 2^(e-7).  |x|/q is exact in binary64 and numpy's
+    rint rounds half to even; a result of 2^128 overflows to infinity."""
+    x = np.asarray(x, dtype=np.float32)
+    a = np.abs(x.astype(np.float64))
+    _, ex = np.frexp(a)
+    e = np.maximum(ex - 1, -126)
+    q = np.ldexp(1.0, e - 7)
+    with np.errstate(over="ignore"):
+        r = (np.rint(a / q) * q).astype(np.float32)
+    return np.where(np.signbit(x), -r, r).astype(np.float32)
+
+
+def quantize_blocks2d(x, row_block: int, bs: int, rule: int):
+    """Quantize a float32 matrix with one scale per block of row_block rows x
+    bs consecutive positions of the last axis (the last row block may be
+    short): the block maximum is taken over the whole 2-D block.  Returns the
+    same tuple as quantize_rows, the stored scales replicated over the rows of
+    each block: (codes (rows, kdim), stored (rows, kdim/bs), s (rows, kdim/bs),
+    dequantized float64)."""
+    x = np.asarray(x, dtype=np.float32)
+    rows, kdim = x.shape
+    if kdim % bs:
+        raise ValueError("block size does not divide the contracted length")
+    nrb = -(-rows // row_block)
+    amax_rows = np.max(np.abs(x.reshape(rows, kdim // bs, bs)), axis=2)   # (rows, kdim/bs)
+    amax = np.empty_like(amax_rows)
+    for i in range(nrb):
+        sl = slice(i * row_block, min(rows, (i + 1) * row_block))
+        amax[sl] = np.max(amax_rows[sl], axis=0, keepdims=True)
+    s, stored = block_scales(amax, rule)
+    xb = x.reshape(rows, kdim // bs, bs)
+    v = (xb / s[:, :, None]).astype(np.float32)
+    codes = encode(v).reshape(rows, kdim)
+    deq = (decode(codes).reshape(rows, kdim // bs, bs)
+           * s[:, :, None].astype(np.float64)).reshape(rows, kdim)
+    return codes, stored, s, deq

@@ -58,12 +58,17 @@ def combine(blocks, coeffs) -> np.ndarray:
 
 
 def encode_side(M: np.ndarray, table: np.ndarray, depth: int, bs: int,
-                rule: int, side: str, want_deq: bool = True):
+                rule: int, side: str, want_deq: bool = True, row_block: int = 1,
+                bf16: bool = False):
     """Encode and quantize one operand for every flattened term.
 
     side 'A': M is A (M x K), blocks (I, J), output rows p, contracted l.
     side 'B': M is B (K x N), blocks (J, K); the combination y (k' x n') is
     transposed (exactly) so its contracted axis is last.
+    Deployment granularity (Appendix E, weight-scale granularity): with
+    bf16 each combination is first rounded to bfloat16; with row_block > 1
+    one scale covers row_block rows x bs positions, its maximum taken over the
+    combination (scales stored per row, replicated over each block's rows).
     Returns dict(codes (T, r, k'), scales (T, r, k'/bs) stored form,
     s (float32 scales), deq (float64, if want_deq), x (fp32 combos list if
     want_deq)).
@@ -75,7 +80,12 @@ def encode_side(M: np.ndarray, table: np.ndarray, depth: int, bs: int,
         x = combine(blocks, table[r])
         if side == "B":
             x = np.ascontiguousarray(x.T)
-        c, st, s, dq = e4m3.quantize_rows(x, bs, rule)
+        if bf16:
+            x = e4m3.bf16_round(x)
+        if row_block > 1:
+            c, st, s, dq = e4m3.quantize_blocks2d(x, row_block, bs, rule)
+        else:
+            c, st, s, dq = e4m3.quantize_rows(x, bs, rule)
         codes.append(c); scales.append(st); s_all.append(s)
         if want_deq:
             deqs.append(dq); xs.append(x)
@@ -108,12 +118,15 @@ def wcombine(P, wtab: np.ndarray, depth: int, M: int, N: int) -> np.ndarray:
 
 
 def fmm(A: np.ndarray, B: np.ndarray, tables, depth: int, bs: int, rule: int,
-        keep: bool = True):
+        keep: bool = True, b_rows: int = 1, b_bf16: bool = False):
     """One product: the full quantized evaluation for a single (A, B) pair.
 
     tables = (U, V, w) fp32 flattened tables (T x 4^l).  Returns a dict with
     C (binary64), and the codes/scales of both sides; with keep=True also
     the fp32 combinations and dequantized operands (for the noise model).
+    b_rows, b_bf16: the weight (B) side's deployment granularity -- scale
+    blocks of b_rows columns of B x bs, and a bfloat16 pre-round of each
+    encoded B combination (Appendix E, weight-scale granularity).
     """
     U, V, W = tables
     Mdim, Kdim = A.shape
@@ -121,7 +134,7 @@ def fmm(A: np.ndarray, B: np.ndarray, tables, depth: int, bs: int, rule: int,
     if Kb != Kdim:
         raise ValueError("inner dimensions differ")
     ea = encode_side(A, U, depth, bs, rule, "A")
-    eb = encode_side(B, V, depth, bs, rule, "B")
+    eb = encode_side(B, V, depth, bs, rule, "B", row_block=b_rows, bf16=b_bf16)
     P = products(ea["deq"], eb["deq"])
     C = wcombine(P, W, depth, Mdim, Ndim)
     out = {"C": C, "a": ea, "b": eb}

@@ -188,3 +188,63 @@ def test_power_of_two_homogeneity(rule):
         assert np.array_equal(c0, c1)
         assert np.array_equal(s1, (s0 * f).astype(np.float32))
         assert np.array_equal(d1, d0 * float(f))
+
+
+# ---- deployment granularity: bfloat16 pre-round, 2-D weight blocks ----------
+
+def test_bf16_round_matches_torch_conversion():
+    """torch's float32 -> bfloat16 cast rounds to nearest even: a library
+    routine the definition reduces to."""
+    import torch
+    rng = np.random.default_rng(7)
+    x = (rng.standard_normal(400_000) * np.exp(rng.uniform(-85, 85, 400_000))).astype(np.float32)
+    bits = rng.integers(0, 2 ** 32, 400_000, dtype=np.uint64).astype(np.uint32).view(np.float32)
+    x = np.concatenate([x, bits[np.isfinite(bits)], np.float32([0.0, -0.0, 1e-45, -1e-45, 1.17549435e-38])])
+    got = e4m3.bf16_round(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_bf16_round_special_values():
+    f = lambda v: float(e4m3.bf16_round(np.float32(v)))
+    assert f(1 + 2 ** -8) == 1.0                      # tie -> even (mantissa 0)
+    assert f(1 + 3 * 2 ** -8) == 1 + 2 ** -6          # tie -> even (mantissa 2)
+    assert f(1 + 2 ** -8 + 2 ** -20) == 1 + 2 ** -7   # above the tie
+    assert f(-(1 + 2 ** -8)) == -1.0
+    assert f(3.0) == 3.0 and f(0.0) == 0.0
+    assert np.signbit(e4m3.bf16_round(np.float32(-0.0)))
+    # power-of-two scaling commutes with the rounding (normal range)
+    v = np.random.default_rng(1).standard_normal(1000).astype(np.float32)
+    for k in (-20, -3, 5, 40):
+        sc = np.float32(2.0 ** k)
+        assert np.array_equal(e4m3.bf16_round(v * sc), e4m3.bf16_round(v) * sc)
+
+
+@pytest.mark.parametrize("rule", [e4m3.RULE_FP32_AMAX, e4m3.RULE_POW2_CEIL, e4m3.RULE_POW2_OCP])
+def test_blocks2d_one_row_is_the_row_quantizer(rule):
+    x = np.random.default_rng(2).standard_normal((37, 256)).astype(np.float32)
+    a = e4m3.quantize_blocks2d(x, 1, 32, rule)
+    b = e4m3.quantize_rows(x, 32, rule)
+    for u, v in zip(a, b):
+        assert np.array_equal(np.asarray(u), np.asarray(v))
+
+
+@pytest.mark.parametrize("rule", [e4m3.RULE_FP32_AMAX, e4m3.RULE_POW2_CEIL, e4m3.RULE_POW2_OCP])
+def test_blocks2d_scale_is_the_block_max_and_codes_follow(rule):
+    """One scale per (4 rows x 16) block from the maximum over the whole
+    block; every code is the brute-force nearest code of fl32(x / s); a short
+    last row block."""
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal((10, 48)) * np.exp(rng.uniform(-3, 3, (10, 1)))).astype(np.float32)
+    codes, stored, s, deq = e4m3.quantize_blocks2d(x, 4, 16, rule)
+    for rb in range(3):
+        rows = slice(4 * rb, min(10, 4 * rb + 4))
+        for kb in range(3):
+            blk = x[rows, 16 * kb:16 * kb + 16]
+            amax = np.float32(np.max(np.abs(blk)))
+            sb, stb = e4m3.block_scales(np.array([amax]), rule)
+            assert np.all(s[rows, kb] == sb[0])
+            assert np.all(stored[rows, kb] == stb[0])
+            for (i, j), v in np.ndenumerate(blk):
+                q = np.float32(v / sb[0])
+                assert codes[rows][i, 16 * kb + j] == e4m3.encode_bruteforce(float(q))

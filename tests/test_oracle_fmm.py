@@ -211,3 +211,32 @@ def test_row_sampled_encoding_matches_the_full_encoder():
         assert np.array_equal(yc, eb["codes"][:, qrow, :]) and np.array_equal(ys, eb["scales"][:, qrow, :])
         assert np.array_equal(xd, np.stack(ea["deq"])[:, prow, :])
         assert np.array_equal(yd, np.stack(eb["deq"])[:, qrow, :])
+
+
+def test_deployment_granularity_weight_side():
+    """Weight (B) side with 128 x block scale blocks and the bfloat16
+    pre-round (Appendix E, weight-scale granularity): the A side is
+    untouched; B codes follow the 2-D quantizer of the pre-rounded
+    combinations; on Gaussian operands at n = 512 the two groupings are
+    nearly the same quantizer (the paper's observation), and coarsening does
+    not lower the error."""
+    rng_inputs = gen.operands("gaussian", 1, 512, 512, 512, seed=4, cfg=8, trial=0)
+    A, B = rng_inputs[0][0], rng_inputs[1][0]
+    tabs = R.tables_f32(R.builtin_f64("tstar"), 1)
+    base = fmm.fmm(A, B, tabs, 1, 128, e4m3.RULE_FP32_AMAX)
+    dep = fmm.fmm(A, B, tabs, 1, 128, e4m3.RULE_FP32_AMAX, b_rows=128, b_bf16=True)
+    assert np.array_equal(base["a"]["codes"], dep["a"]["codes"])
+    # B: re-derive from the pre-rounded combinations
+    blocks = [np.asarray(b, dtype=np.float32) for b in fmm.split(B, 1)]
+    for r in range(tabs[1].shape[0]):
+        y = e4m3.bf16_round(np.ascontiguousarray(fmm.combine(blocks, tabs[1][r]).T))
+        c, st, _, _ = e4m3.quantize_blocks2d(y, 128, 128, e4m3.RULE_FP32_AMAX)
+        assert np.array_equal(dep["b"]["codes"][r], c)
+        assert np.array_equal(dep["b"]["scales"][r].view(np.uint32), st.view(np.uint32))
+        # the scale is constant over each 128-row block
+        assert np.all(st.reshape(2, 128, -1) == st.reshape(2, 128, -1)[:, :1, :])
+    Cref = fmm.reference(A, B)
+    e1 = fmm.error_sums(base["C"], Cref)
+    e2 = fmm.error_sums(dep["C"], Cref)
+    r1, r2 = e1[0] / e1[1], e2[0] / e2[1]
+    assert r2 >= r1 * 0.98 and r2 <= r1 * 1.15, (r1, r2)
