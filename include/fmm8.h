@@ -91,7 +91,19 @@ enum {
    * the bf16 matrix cores (23 retained bits), each block's partial sum is
    * scaled and accumulated in fp32.  Half the peak rate of the default path.
    * FP32_AMAX scales and block 16 always take this path. */
-  FMM_FLAG_EXACT_DOT = 1
+  FMM_FLAG_EXACT_DOT = 1,
+  /* Weight-side deployment granularity (Appendix E, weight-scale
+   * granularity; the real kernel's 128 x 128 weight blocks): one B-side scale
+   * covers 128 consecutive columns of B (rows of y_r^T) x `block` positions
+   * of the contracted axis, its maximum taken over the encoded combination;
+   * the last block of a ragged N / 2 is short.  The stored scales stay one per
+   * (row, block), replicated over each 128-row block.  Depth 1 only
+   * (FMM_ERR_UNSUPPORTED otherwise).  The encoder reads B twice. */
+  FMM_FLAG_B_BLOCK128 = 2,
+  /* Round each encoded B combination to bfloat16 (nearest, ties to even)
+   * before its scale and cast (Appendix E: the real path's pre-round of the
+   * encoded weights).  Depth 1 only. */
+  FMM_FLAG_B_BF16 = 4
 };
 
 typedef struct fmm_real fmm_real;   /* a base realization (U, V, w), R x 4 each, binary64 */

@@ -56,6 +56,8 @@ struct Problem {
   int exact_dot;           // FMM_FLAG_EXACT_DOT requested
   int split;               // large-tile sub-products + separate W-combine (depth 1, tile-aligned MX)
   int layout;              // FMM_LAYOUT_* of the workspace's codes and scales
+  int b_rows;              // rows of y_r^T per B scale block: 1, or 128 (FMM_FLAG_B_BLOCK128)
+  int b_bf16;              // round encoded B combinations to bfloat16 first (FMM_FLAG_B_BF16)
 };
 
 // Bytes of one (batch, term) plane of scales for `rows` rows.
@@ -68,6 +70,7 @@ inline int64_t scale_plane_bytes(const Problem &pb, int64_t rows) {
 struct Workspace {
   size_t a_codes, b_codes, a_scales, b_scales, partial, total;
   size_t products;   // split plans only: the fp32 sub-products P_r
+  size_t b_amax;     // FMM_FLAG_B_BLOCK128 plans: 2-D block maxima [batch][T][ceil(n'/128)][kblocks] u32
 };
 
 // Device copies of the plan's tables (one allocation).

@@ -19,6 +19,8 @@
 //      the lane casts its values and stores their codes.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "device.h"
 #include "internal.h"
 
@@ -181,11 +183,30 @@ __device__ __forceinline__ void store_scale(const Problem &pb, uint8_t *scales, 
 // Depth 1: 16 (A) or 32 (B) rows, one wave per 8 of them, every term; depth 2:
 // 8 rows, four waves, wave w takes terms w, w + 4, ...
 // ---------------------------------------------------------------------------
-template <int SIDE, int DEPTH, int BS, bool F32>
+// Weight-side deployment granularity (FMM_FLAG_B_BLOCK128 / FMM_FLAG_B_BF16,
+// B side at depth 1), in two launches over the same tiles:
+//   MODE 1: combine (and round to bfloat16), then the maximum of |y| over the
+//           block's positions and the wave's 8 rows, merged into the 2-D
+//           block's maximum amax[bt][r][row block][kb] by an integer atomic
+//           maximum on the float bits (non-negative, so the order of the
+//           merges does not matter); nothing else is stored;
+//   MODE 2: combine (and round), take the block maximum from amax (or, with
+//           1-row blocks, from the lanes as in MODE 0), scale, cast, store.
+// MODE 0 is the plain encoder.
+__device__ __forceinline__ float bf16_round(float x) {
+  // nearest bfloat16, ties to even (finite x; a carry past the largest
+  // finite value gives infinity, as the definition does)
+  uint32_t b = __float_as_uint(x);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return __uint_as_float(b & 0xffff0000u);
+}
+
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE>
 __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
-    int64_t tiles_l) {
+    int64_t tiles_l, uint32_t *__restrict__ amax) {
+  static_assert(MODE == 0 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
   using TT = Tile<DEPTH, 16, SIDE>;
   constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads;
   constexpr int WPT = TR * 8 / 64;          // waves per term (2 or 4 at depth 1, 1 at depth 2)
@@ -236,14 +257,39 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
         }
       }
     }
+    if constexpr (MODE != 0) {
+      if (pb.b_bf16) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) x[i] = bf16_round(x[i]);
+      }
+    }
     // block maximum: the lane's 16, then across the lanes of its block
     float m = fmaxf(fabsf(x[0]), fabsf(x[1]));
 #pragma unroll
     for (int i = 2; i < 16; ++i) m = fmaxf(m, fabsf(x[i]));
-    if (BS >= 32) m = fmaxf(m, dpp<0xB1>(m));                 // quad_perm [1, 0, 3, 2]
-    if (BS == 128) {
-      m = fmaxf(m, dpp<0x4E>(m));                             // quad_perm [2, 3, 0, 1]
-      m = fmaxf(m, __shfl_xor(m, 32, 64));
+    // the 2-D block of this lane: row block (row0 + row) / 128 (a tile's rows
+    // lie in one), K block of position l0 + 16 ch
+    const int64_t kb = (l0 + 16 * ch) / pb.block;
+    const int64_t aidx = (((int64_t)bt * T + r) * ((rows + 127) / 128) + row0 / 128) * pb.kblocks + kb;
+    if constexpr (MODE == 1) {
+      // over the wave's 8 rows (lane bits 2..4), then the block's lanes
+      m = fmaxf(m, __shfl_xor(m, 4, 64));
+      m = fmaxf(m, __shfl_xor(m, 8, 64));
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+    }
+    if (MODE != 2 || pb.b_rows == 1) {
+      if (BS >= 32) m = fmaxf(m, dpp<0xB1>(m));                 // quad_perm [1, 0, 3, 2]
+      if (BS == 128) {
+        m = fmaxf(m, dpp<0x4E>(m));                             // quad_perm [2, 3, 0, 1]
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+      }
+    }
+    if constexpr (MODE == 1) {
+      if (((lane >> 2) & 7) == 0 && lead && l0 + 16 * ch < pb.kp) atomicMax(amax + aidx, __float_as_uint(m));
+      continue;
+    }
+    if constexpr (MODE == 2) {
+      if (pb.b_rows > 1) m = o.valid ? __uint_as_float(amax[aidx]) : 0.0f;
     }
     uint32_t w[4];
     uint32_t stored;
@@ -350,17 +396,53 @@ __global__ __launch_bounds__(256) void encode4_kernel(
   }
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32>
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0>
 hipError_t launch16(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
-                    uint8_t *codes, uint8_t *scales, hipStream_t st) {
+                    uint8_t *codes, uint8_t *scales, hipStream_t st, uint32_t *amax = nullptr) {
   using TT = Tile<DEPTH, 16, SIDE>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32>), grid, dim3(TT::threads), 0, st, src, pb, off,
-                     ent, codes, scales, tiles_l);
+  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE>), grid, dim3(TT::threads), 0, st, src, pb, off,
+                     ent, codes, scales, tiles_l, amax);
   return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void zero_u32_kernel(uint32_t *p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0u;
+}
+
+// B side with the weight-side deployment granularity (depth 1): the 2-D
+// block maxima (zeroed, then merged by MODE 1) when blocks span 128 rows,
+// then the quantizing pass.
+template <int BS, bool F32>
+hipError_t launch_b_deploy(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+                           uint8_t *codes, uint8_t *scales, uint32_t *amax, hipStream_t st) {
+  if (pb.b_rows > 1) {
+    const int64_t n = pb.batch * pb.T * ((pb.np + 127) / 128) * pb.kblocks;
+    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, st, amax, n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch16<1, 1, BS, F32, 1>(pb, src, off, ent, codes, scales, st, amax);
+    if (e != hipSuccess) return e;
+  }
+  return launch16<1, 1, BS, F32, 2>(pb, src, off, ent, codes, scales, st, amax);
+}
+
+hipError_t launch_b_deploy_any(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+                               uint8_t *codes, uint8_t *scales, uint32_t *amax, hipStream_t st) {
+  const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
+  switch (pb.block) {
+    case 16: return f32 ? launch_b_deploy<16, true>(pb, src, off, ent, codes, scales, amax, st)
+                        : launch_b_deploy<16, false>(pb, src, off, ent, codes, scales, amax, st);
+    case 32: return f32 ? launch_b_deploy<32, true>(pb, src, off, ent, codes, scales, amax, st)
+                        : launch_b_deploy<32, false>(pb, src, off, ent, codes, scales, amax, st);
+    case 128: return f32 ? launch_b_deploy<128, true>(pb, src, off, ent, codes, scales, amax, st)
+                         : launch_b_deploy<128, false>(pb, src, off, ent, codes, scales, amax, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int SIDE, int DEPTH>
@@ -404,6 +486,9 @@ int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, co
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = launch_side<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, st);
   if (e != hipSuccess) return e;
+  if (pb.b_rows > 1 || pb.b_bf16)
+    return launch_b_deploy_any(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales,
+                               reinterpret_cast<uint32_t *>(ws + wl.b_amax), st);
   return launch_side<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, st);
 }
 

@@ -68,7 +68,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   *out = nullptr;
   if (!d || !desc) return FMM_ERR_ARG;
   const fmm_plan_desc &q = *desc;
-  if ((q.flags & ~FMM_FLAG_EXACT_DOT) != 0 || q.batch < 0 || q.M < 0 || q.K < 0 || q.N < 0) return FMM_ERR_ARG;
+  constexpr int kFlags = FMM_FLAG_EXACT_DOT | FMM_FLAG_B_BLOCK128 | FMM_FLAG_B_BF16;
+  if ((q.flags & ~kFlags) != 0 || q.batch < 0 || q.M < 0 || q.K < 0 || q.N < 0) return FMM_ERR_ARG;
   if (q.depth < 1 || q.depth > fmm::kMaxDepth) return FMM_ERR_ARG;
   if (q.block != 16 && q.block != 32 && q.block != 128) return FMM_ERR_ARG;
   if (q.rule < FMM_RULE_FP32_AMAX || q.rule > FMM_RULE_POW2_OCP) return FMM_ERR_ARG;
@@ -77,6 +78,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if ((q.K / n) % q.block) return FMM_ERR_SHAPE;
   // grid limits of the launches (batch on grid z/y, terms on grid y)
   if (q.batch > 65535) return FMM_ERR_UNSUPPORTED;
+  // the weight-side deployment granularity is built for one level
+  if ((q.flags & (FMM_FLAG_B_BLOCK128 | FMM_FLAG_B_BF16)) && q.depth != 1) return FMM_ERR_UNSUPPORTED;
 
   // the realization, as the C-ABI sees it
   int64_t R = 0, T = 0;
@@ -93,6 +96,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.kblocks = pb.kp / q.block;
   pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
   pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
+  pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
+  pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
   const bool mx = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
   // large-tile path: E8M0 scales applied by the MFMA, one level, 256-row tiles,
   // whole 64-byte (block 32) or 128-byte (block 128) K steps
@@ -117,6 +122,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
   wl.products = off;
   if (pb.split) off = align256(off + B * T * pb.mp * pb.np * sizeof(float));
+  wl.b_amax = off;
+  if (pb.b_rows > 1) off = align256(off + B * T * ((pb.np + 127) / 128) * pb.kblocks * sizeof(uint32_t));
   wl.total = off;
 
   // host tables: fp32 flattened U, V (nonzeros in ascending block order), base w, outer w

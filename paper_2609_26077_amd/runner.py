@@ -18,7 +18,7 @@ class FMM:
     """One planned product shape on one device, with its own workspace."""
 
     def __init__(self, realization, batch, M, K, N, depth=1, block=32, rule="pow2_ceil",
-                 device="cuda:0", exact_dot=False):
+                 device="cuda:0", exact_dot=False, flags=0):
         if not isinstance(realization, Realization):
             realization = fmm_realization_builtin(realization)
         self.real = realization
@@ -26,8 +26,9 @@ class FMM:
         self.shape = (int(batch), int(M), int(K), int(N))
         self.depth, self.block = int(depth), int(block)
         with torch.cuda.device(self.device):
-            self.plan = fmm_plan_create(realization, make_desc(batch, M, K, N, depth, block, rule,
-                                                               exact_dot=exact_dot))
+            desc = make_desc(batch, M, K, N, depth, block, rule, exact_dot=exact_dot)
+            desc.flags |= int(flags)
+            self.plan = fmm_plan_create(realization, desc)
             nbytes = fmm_plan_workspace_size(self.plan)
             self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         self.scale_bytes = 4 if (rule in ("fp32_amax", 0)) else 1

@@ -63,14 +63,14 @@ def uses_mx(bs, rule, exact):
     return (not exact) and rule != e4m3.RULE_FP32_AMAX and bs in (32, 128)
 
 
-def run_gpu(spec, A, B, depth, bs, rule, exact=False):
+def run_gpu(spec, A, B, depth, bs, rule, exact=False, flags=0):
     import torch
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
     batch, M, K = A.shape
     N = B.shape[2]
     dA = torch.from_numpy(A).cuda()
     dB = torch.from_numpy(B).cuda()
-    f = FMM(gpu_realization(spec), batch, M, K, N, depth, bs, rule, exact_dot=exact)
+    f = FMM(gpu_realization(spec), batch, M, K, N, depth, bs, rule, exact_dot=exact, flags=flags)
     C = f.matmul(dA, dB)
     Cref = reference_f64(dA, dB)
     err2, ref2 = error_stats(C, Cref)
@@ -99,21 +99,24 @@ def abs_bound(o, wtab, depth, M, N):
 
 
 def check_case(spec, family, batch, M, K, N, depth, bs, rule, seed=0, cfg=0, trial=0,
-               check_every=None, exact=False, ns=True):
-    """Run one configuration on both sides and assert every bar above."""
+               check_every=None, exact=False, ns=True, b_rows=1, b_bf16=False):
+    """Run one configuration on both sides and assert every bar above.
+    b_rows = 128 / b_bf16: the weight-side deployment granularity
+    (FMM_FLAG_B_BLOCK128 / FMM_FLAG_B_BF16)."""
     mx = uses_mx(bs, rule, exact)
     g_dot = 2.0 ** -10 if mx else 2.0 ** -19
     A, B = gen.operands(family, batch, M, K, N, seed=seed, cfg=cfg, trial=trial)
     D = oracle_realization(spec)
     tabs = R.tables_f32(D, depth)
     T = tabs[0].shape[0]
-    g = run_gpu(spec, A, B, depth, bs, rule, exact)
+    flags = (2 if b_rows == 128 else 0) | (4 if b_bf16 else 0)
+    g = run_gpu(spec, A, B, depth, bs, rule, exact, flags)
     kp = K // 2 ** depth
     errs, refs = [], []
     worst_rel_fro = 0.0
     which = range(batch) if check_every is None else range(0, batch, check_every)
     for b in which:
-        o = fmm.fmm(A[b], B[b], tabs, depth, bs, rule)
+        o = fmm.fmm(A[b], B[b], tabs, depth, bs, rule, b_rows=b_rows, b_bf16=b_bf16)
         compare_operands(g["ops"], o["a"], o["b"], b, rule)
         Co = o["C"]
         Cg = g["C"][b].astype(np.float64)

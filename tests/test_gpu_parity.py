@@ -85,6 +85,26 @@ def test_rebased_realization():
     assert ratio > 1.1
 
 
+@pytest.mark.parametrize("case", [
+    # (rule, block, b_rows, bf16, shape): the paper's real-kernel setting first
+    (0, 128, 128, True, (1, 384, 512, 320)),      # fp32 amax/448, 128 x 128 weight blocks, bf16; ragged 160-row tail
+    (1, 128, 128, True, (2, 256, 512, 640)),      # E8M0 scales on the MX path
+    (1, 32, 128, False, (1, 512, 256, 512)),      # large-tile plan (m', n' = 256)
+    (2, 128, 128, False, (1, 130, 256, 258)),     # ragged everything
+    (1, 16, 1, True, (1, 192, 256, 128)),         # bfloat16 pre-round alone, block 16
+    (0, 32, 1, True, (1, 128, 384, 256)),
+])
+def test_weight_deployment_granularity(case):
+    """Weight-side deployment granularity (Appendix E): 128-row B scale
+    blocks with the maximum after the combine, and the bfloat16 pre-round of
+    the encoded B combinations: codes and scales bit-exact, C and relMSE to
+    the usual bars."""
+    rule, bs, b_rows, bf16, (b, M, K, N) = case
+    r = check_case("tstar", "student_t3", b, M, K, N, 1, bs, rule, seed=3, cfg=9,
+                   b_rows=b_rows, b_bf16=bf16, ns=False)
+    print(case, r, flush=True)
+
+
 def test_rowscaled_family():
     """Per-row log-uniform scales over four decades stress the blocks along K."""
     for depth in (1, 2, 3):
