@@ -122,31 +122,44 @@ def time_arm(f, dA, dB, C, stream, steps, warmup):
 def other_arms(args, dA, dB, C, stream):
     """The comparison arms on the same code path and workload size: the cubic
     (8-product) and Strassen 1969 realizations on the same Gaussian operands,
-    and the default realization on heavy-tailed operands (Student-t, 3 degrees
-    of freedom, unit variance).  Each: effective TFLOP/s from the mean event
-    time of whole steps, and the relative RMS error against fp64."""
+    the default realization on heavy-tailed operands (Student-t, 3 degrees
+    of freedom, unit variance), and the default realization under the real
+    kernel's quantization (block 128, 128 x 128 weight blocks with the
+    bfloat16 pre-round; fp32 amax/448 scales, which take the exact-dot
+    sub-product path, and E8M0 scales on the fp8 path).  Each: effective
+    TFLOP/s from the mean event time of whole steps, and the relative RMS
+    error against fp64."""
     import torch
     import fmm_inputs as gen
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
     n = args.size
     mkn = 2.0 * n ** 3
     out = {}
-    arms = [("cubic8", "gaussian"), ("strassen", "gaussian"), (args.realization, "student_t3")]
-    for real, family in arms:
-        if real == args.realization and family == args.family:
-            continue
+    # (realization, family, rule, block, flags, label)
+    arms = [("cubic8", "gaussian", args.rule, args.block, 0, "cubic8/gaussian"),
+            ("strassen", "gaussian", args.rule, args.block, 0, "strassen/gaussian"),
+            (args.realization, "student_t3", args.rule, args.block, 0, f"{args.realization}/student_t3"),
+            # the real kernel's quantization (Appendix E): fp32 amax/448 scales,
+            # 1 x 128 activation groups, 128 x 128 weight blocks, bfloat16 pre-round
+            (args.realization, "gaussian", "fp32_amax", 128, 2 | 4,
+             f"{args.realization}/gaussian/deployment-fp32amax-b128x128-bf16"),
+            (args.realization, "gaussian", "pow2_ceil", 128, 2 | 4,
+             f"{args.realization}/gaussian/deployment-e8m0-b128x128-bf16")]
+    for real, family, rule, block, flags, label in arms:
         if family != args.family:
             A, B = gen.operands(family, 1, n, n, n, seed=0, cfg=0, trial=0)
             xa, xb = torch.from_numpy(A).to(dA.device), torch.from_numpy(B).to(dA.device)
             del A, B
         else:
             xa, xb = dA, dB
-        f = FMM(real, 1, n, n, n, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
+        if flags and args.depth != 1:
+            continue
+        f = FMM(real, 1, n, n, n, args.depth, block, rule, exact_dot=args.exact_dot, flags=flags)
         mean_ms, med_ms = time_arm(f, xa, xb, C, stream, args.arm_steps, 5)
         Cref = reference_f64(xa, xb)
         err2, ref2 = error_stats(C, Cref)
         del Cref, f
-        out[f"{real}/{family}"] = {"value": mkn / (mean_ms * 1e-3) / 1e12, "unit": "TFLOP/s",
+        out[label] = {"value": mkn / (mean_ms * 1e-3) / 1e12, "unit": "TFLOP/s",
                                    "ms_per_step": mean_ms, "median_ms": med_ms,
                                    "rel_rms_error_vs_fp64": float(np.sqrt(err2.sum() / ref2.sum())),
                                    "steps": args.arm_steps}
