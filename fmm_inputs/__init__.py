@@ -62,6 +62,12 @@ def draw(family: str, shape, rng: np.random.Generator) -> np.ndarray:
         x = rng.standard_normal(shape)  # float64
         f = 10.0 ** rng.uniform(-2.0, 2.0, size=shape[:-1] + (1,))
         return (x * f).astype(np.float32)
+    if family == "rademacher":
+        return np.where(rng.integers(0, 2, size=shape) == 0, -1.0, 1.0).astype(np.float32)
+    if family == "rademacher10":
+        return np.where(rng.integers(0, 2, size=shape) == 0, -10.0, 10.0).astype(np.float32)
+    if family == "laplace":
+        return (rng.laplace(0.0, 1.0 / np.sqrt(2.0), size=shape)).astype(np.float32)
     raise ValueError(f"unknown operand family {family!r}")
 
 

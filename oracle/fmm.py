@@ -80,12 +80,11 @@ def encode_side(M: np.ndarray, table: np.ndarray, depth: int, bs: int,
         x = combine(blocks, table[r])
         if side == "B":
             x = np.ascontiguousarray(x.T)
-        if bf16:
-            x = e4m3.bf16_round(x)
+        xq = e4m3.bf16_round(x) if bf16 else x       # x itself stays the fp32 combination
         if row_block > 1:
-            c, st, s, dq = e4m3.quantize_blocks2d(x, row_block, bs, rule)
+            c, st, s, dq = e4m3.quantize_blocks2d(xq, row_block, bs, rule)
         else:
-            c, st, s, dq = e4m3.quantize_rows(x, bs, rule)
+            c, st, s, dq = e4m3.quantize_rows(xq, bs, rule)
         codes.append(c); scales.append(st); s_all.append(s)
         if want_deq:
             deqs.append(dq); xs.append(x)

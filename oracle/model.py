@@ -34,3 +34,33 @@ def predicted_rel_mse(s_a2: float, s_b2: float, phi: float, depth: int,
         return (s_a2 + s_b2 + s_a2 * s_b2) * phi / mkn
     s2 = 0.5 * (s_a2 + s_b2)
     return 2.0 * s2 * phi / mkn
+
+
+def cross_r_residual(ea, eb, w_table) -> float:
+    """The share of the error's linear part that the diagonal sum defining
+    Phi leaves out (Appendix D, the cross-r covariance measurement).
+
+    With X_r, Y_r the fp32 combinations and dX_r, dY_r their rounding
+    residuals (encode_side outputs, B side transposed back), the part of the
+    sub-product error linear in the residuals is t_r = dX_r Y_r + X_r dY_r,
+    and that of output block q is L_q = sum_r w[r, q] t_r.  Returns
+    (|L|^2 - diag) / |L|^2 with diag = sum_{r,q} w[r, q]^2 |t_r|^2
+    (binary64 throughout)."""
+    w = np.asarray(w_table, dtype=np.float64)
+    T, nq = w.shape
+    t = []
+    for r in range(T):
+        X = np.asarray(ea["x"][r], np.float64)
+        dX = ea["deq"][r] - X
+        Y = np.asarray(eb["x"][r], np.float64).T
+        dY = eb["deq"][r].T - Y
+        t.append(dX @ Y + X @ dY)
+    L2 = 0.0
+    diag = 0.0
+    for q in range(nq):
+        Lq = sum(w[r, q] * t[r] for r in range(T) if w[r, q] != 0.0)
+        if not isinstance(Lq, np.ndarray):
+            continue
+        L2 += float(np.sum(Lq * Lq))
+        diag += sum(float(w[r, q] ** 2 * np.sum(t[r] * t[r])) for r in range(T))
+    return (L2 - diag) / L2

@@ -240,3 +240,37 @@ def test_deployment_granularity_weight_side():
     e2 = fmm.error_sums(dep["C"], Cref)
     r1, r2 = e1[0] / e1[1], e2[0] / e2[1]
     assert r2 >= r1 * 0.98 and r2 <= r1 * 1.15, (r1, r2)
+
+
+def test_cross_r_residual_closed_forms():
+    """Two identical terms feeding one output block: L = (w1 + w2) t, diag =
+    (w1^2 + w2^2) |t|^2, so the residual fraction is 2 w1 w2 / (w1 + w2)^2:
+    0.5 for (1, 1) and -4 for (1, -0.5)."""
+    A, B = gen.operands("gaussian", 1, 64, 64, 64, seed=0, cfg=15, trial=0)
+    U = np.array([[1, 0, 0, 0], [1, 0, 0, 0]], dtype=np.float32)
+    ea = fmm.encode_side(A[0], U, 1, 32, e4m3.RULE_POW2_CEIL, "A")
+    eb = fmm.encode_side(B[0], U, 1, 32, e4m3.RULE_POW2_CEIL, "B")
+    for w, want in (((1.0, 1.0), 0.5), ((1.0, -0.5), -4.0)):
+        W = np.zeros((2, 4))
+        W[:, 0] = w
+        assert model.cross_r_residual(ea, eb, W) == pytest.approx(want, rel=1e-12)
+
+
+def test_cross_r_residual_six_arm_diagnostic():
+    """Appendix D: on six arms at n = 512, iid Gaussian, four seeds, 1 x 128
+    blocks with fp32 amax/448 scales, the armwise mean residual fraction lies
+    between -0.085% and 0.201%.  Arms (the paper does not list them): cubic,
+    Strassen, Winograd raw and rebalanced, T*, and one random orbit member of
+    Strassen; each armwise mean must stay within +-0.3%."""
+    arms = [R.builtin_f64("cubic8"), R.builtin_f64("strassen"), R.builtin_f64("winograd"),
+            R.rebalance_f64(R.builtin_f64("winograd")), R.builtin_f64("tstar"),
+            R.act_f64(R.builtin_f64("strassen"), gen.basis_changes(1, seed=0, cfg=14)[0])]
+    for D in arms:
+        U, V, W = R.tables_f32(D, 1)
+        vals = []
+        for seed in range(4):
+            A, B = gen.operands("gaussian", 1, 512, 512, 512, seed=seed, cfg=14, trial=0)
+            ea = fmm.encode_side(A[0], U, 1, 128, e4m3.RULE_FP32_AMAX, "A")
+            eb = fmm.encode_side(B[0], V, 1, 128, e4m3.RULE_FP32_AMAX, "B")
+            vals.append(model.cross_r_residual(ea, eb, W))
+        assert abs(np.mean(vals)) < 0.003, np.mean(vals)
