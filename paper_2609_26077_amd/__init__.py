@@ -22,6 +22,17 @@ if not os.path.exists(LIB_PATH):
         f"{LIB_PATH} is missing: the HIP library has not been built "
         f"(python {os.path.join(_HERE, '_build.py')})")
 
+# The library's device calls take torch's device pointers and streams, so
+# it must bind to the HIP runtime torch uses.  torch ships its own
+# libamdhip64; importing torch first maps that runtime, and the library's
+# libamdhip64.so.7 dependency then resolves to it (loaded the other way
+# round, the process would hold two runtimes and the library could not see
+# torch's allocations, or the device at all).
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:         # host-only use of the realization calls
+    _torch = None
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ---- constants (mirror include/fmm8.h) -------------------------------------
@@ -106,6 +117,8 @@ _SIGS = {
     "fmm_error_stats": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                        _vp]),
     "fmm_e4m3_quantize": (ctypes.c_int, [_vp, _vp, _i64, _vp]),
+    "fmm_encode_noise_scratch_size": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_size_t)]),
+    "fmm_encode_noise": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "fmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fmm_last_error_detail": (ctypes.c_char_p, []),
     "fmm_device_check": (ctypes.c_int, [ctypes.c_int]),
@@ -311,6 +324,17 @@ def make_desc(batch, M, K, N, depth=1, block=32, rule="pow2_ceil", exact_dot=Fal
         flags = FMM_FLAG_EXACT_DOT if exact_dot else 0
     return fmm_plan_desc(int(batch), int(M), int(K), int(N), int(depth), int(block), int(rule),
                          int(flags))
+
+
+def fmm_encode_noise_scratch_size(p: Plan) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib.fmm_encode_noise_scratch_size(p.handle, ctypes.byref(n)), "fmm_encode_noise_scratch_size")
+    return n.value
+
+
+def fmm_encode_noise(p: Plan, A, B, ws, out, scratch, scratch_bytes: int, stream=None):
+    _check(_lib.fmm_encode_noise(p.handle, _ptr(A), _ptr(B), _ptr(ws), _ptr(out), _ptr(scratch),
+                                 int(scratch_bytes), _stream(stream)), "fmm_encode_noise")
 
 
 def fmm_plan_create(d: Realization, desc: fmm_plan_desc) -> Plan:

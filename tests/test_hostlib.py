@@ -212,3 +212,16 @@ def test_optimize_argument_and_exactness_errors(fm):
     bad = fm.fmm_realization_create(U, V, W, tol=10.0)
     st = lib.fmm_realization_optimize(bad.handle, 1, sp, 100, 1e-10, 1e-9, ctypes.byref(out), ctypes.byref(phi), None)
     assert st == fm.FMM_ERR_NOT_EXACT and not out.value
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Importing the package before torch must not map a second HIP runtime
+    (the library takes torch's device pointers, so both must use one)."""
+    import subprocess
+    import sys
+    code = ("import paper_2609_26077_amd, torch\n"
+            "libs = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(libs))\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1", out.stdout
