@@ -286,6 +286,23 @@ int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const 
 
 /* ---- the codec alone --------------------------------------------------- */
 
+/* Operand-side rounding energy of the encoding in dWs (Appendix D,
+ * eq. D.1: the noise coefficient s^2 = sum (xhat - x)^2 / sum x^2 of the
+ * model of Section 2.2).  Call after fmm_encode with the same dA, dB and
+ * workspace: the combinations x_r are formed again with the encoder's
+ * arithmetic, the stored codes and scales are decoded to xhat_r (exact in
+ * binary64), and dOut (device, [batch][2][T][2] binary64; side 0 = A, 1 = B)
+ * receives, for every batch element, side and flattened term, the sums of
+ * (xhat - x)^2 and of x^2 over the term's positions (binary64, a fixed
+ * summation order, so repeated calls agree bit for bit).  With
+ * FMM_FLAG_B_BF16, x is the combination before the bfloat16 rounding.
+ * dScratch: device, 8-byte aligned, at least fmm_encode_noise_scratch_size
+ * bytes (FMM_ERR_WORKSPACE otherwise).  Depths 1 and 2 (FMM_ERR_UNSUPPORTED
+ * at depth 3).  Asynchronous on stream. */
+int fmm_encode_noise_scratch_size(const fmm_plan *p, size_t *bytes);
+int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const void *dWs, double *dOut,
+                     void *dScratch, size_t scratch_bytes, void *stream);
+
 /* dOut[i] = e4m3 code of dIn[i] at unit scale: round to nearest, ties to the
  * even mantissa field, saturate to +-448, keep the sign (the cast the
  * quantizer applies after dividing by the block scale).  n >= 0; dIn must be

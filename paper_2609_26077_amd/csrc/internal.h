@@ -96,6 +96,11 @@ int launch_combine(const Problem &pb, const DeviceTables &tab, const uint8_t *ws
 int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace &wl, void *stream);
 int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8_t *ws, const Workspace &wl,
                          float *C, void *stream);
+// operand-side rounding energy of the encoding in the workspace (depths 1, 2):
+// out [batch][2 sides][T][2] binary64 = (sum (xhat - x)^2, sum x^2)
+size_t encode_noise_scratch_bytes(const Problem &pb);
+int launch_encode_noise(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
+                        const uint8_t *ws, const Workspace &wl, double *out, void *scratch, void *stream);
 int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *A,
                          const float *B, double *Cref, void *stream);
 size_t error_stats_scratch_bytes(int64_t batch, int64_t M, int64_t N);

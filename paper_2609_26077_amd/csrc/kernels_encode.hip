@@ -193,6 +193,12 @@ __device__ __forceinline__ void store_scale(const Problem &pb, uint8_t *scales, 
 //   MODE 2: combine (and round), take the block maximum from amax (or, with
 //           1-row blocks, from the lanes as in MODE 0), scale, cast, store.
 // MODE 0 is the plain encoder.
+// MODE 3 measures the operand-side rounding energy of an encoding already in
+// the workspace (Appendix D, eq. D.1): it forms x_r exactly as the encoder
+// does, decodes the stored codes and scales to xhat_r (exact in binary64),
+// and writes each wave's sum of (xhat - x)^2 and of x^2 per term to
+// aux[((bt * tiles + tile) * waves + wave) * T + r][2] (binary64, lanes summed
+// in a fixed butterfly order).
 __device__ __forceinline__ float bf16_round(float x) {
   // nearest bfloat16, ties to even (finite x; a carry past the largest
   // finite value gives infinity, as the definition does)
@@ -205,8 +211,9 @@ template <int SIDE, int DEPTH, int BS, bool F32, int MODE>
 __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
     const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
-    int64_t tiles_l, uint32_t *__restrict__ amax) {
-  static_assert(MODE == 0 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
+    int64_t tiles_l, void *__restrict__ aux) {
+  static_assert(MODE == 0 || MODE == 3 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
+  uint32_t *amax = reinterpret_cast<uint32_t *>(aux);
   using TT = Tile<DEPTH, 16, SIDE>;
   constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads;
   constexpr int WPT = TR * 8 / 64;          // waves per term (2 or 4 at depth 1, 1 at depth 2)
@@ -257,7 +264,43 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
         }
       }
     }
-    if constexpr (MODE != 0) {
+    if constexpr (MODE == 3) {
+      double e2 = 0.0, x2 = 0.0;
+      if (o.valid) {
+        const int64_t plane = bt * T + r;
+        const uint4 cw = *reinterpret_cast<const uint4 *>(codes + plane * code_plane + o.code);
+        const double sc = pb.scale_bytes == 4
+                              ? (double)__uint_as_float(reinterpret_cast<const uint32_t *>(scales)[plane * scale_plane + o.scale])
+                              : ldexp(1.0, (int)scales[plane * scale_plane + o.scale] - 127);
+        const int cwv[4] = {(int)cw.x, (int)cw.y, (int)cw.z, (int)cw.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float d0 = __builtin_amdgcn_cvt_f32_fp8(cwv[j], 0), d1 = __builtin_amdgcn_cvt_f32_fp8(cwv[j], 1);
+          const float d2 = __builtin_amdgcn_cvt_f32_fp8(cwv[j], 2), d3 = __builtin_amdgcn_cvt_f32_fp8(cwv[j], 3);
+          const float dec[4] = {d0, d1, d2, d3};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double xv = (double)x[4 * j + i];
+            const double dv = (double)dec[i] * sc - xv;
+            e2 += dv * dv;
+            x2 += xv * xv;
+          }
+        }
+      }
+#pragma unroll
+      for (int sh = 32; sh >= 1; sh >>= 1) {
+        e2 += __shfl_xor(e2, sh, 64);
+        x2 += __shfl_xor(x2, sh, 64);
+      }
+      if (lane == 0) {
+        double *pp = reinterpret_cast<double *>(aux) +
+                     ((((int64_t)bt * gridDim.x + blockIdx.x) * (NT / 64) + wave) * T + r) * 2;
+        pp[0] = e2;
+        pp[1] = x2;
+      }
+      continue;
+    }
+    if constexpr (MODE == 1 || MODE == 2) {
       if (pb.b_bf16) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) x[i] = bf16_round(x[i]);
@@ -398,7 +441,7 @@ __global__ __launch_bounds__(256) void encode4_kernel(
 
 template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0>
 hipError_t launch16(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
-                    uint8_t *codes, uint8_t *scales, hipStream_t st, uint32_t *amax = nullptr) {
+                    uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
   using TT = Tile<DEPTH, 16, SIDE>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
@@ -478,7 +521,82 @@ hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
   return hipErrorInvalidValue;
 }
 
+// ---- operand-side rounding energy (MODE 3) ----------------------------------
+
+template <int SIDE>
+int64_t noise_slots(const Problem &pb) {
+  const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
+  const int64_t tiles = ((pb.kp + kTL - 1) / kTL) * ((rows + (pb.depth == 1 ? Tile<1, 16, SIDE>::TR : Tile<2, 16, SIDE>::TR) - 1) /
+                                                    (pb.depth == 1 ? Tile<1, 16, SIDE>::TR : Tile<2, 16, SIDE>::TR));
+  const int64_t waves = (pb.depth == 1 ? Tile<1, 16, SIDE>::threads : Tile<2, 16, SIDE>::threads) / 64;
+  return pb.batch * tiles * waves * pb.T;
+}
+
+template <int SIDE, int DEPTH>
+hipError_t launch_noise_side(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+                             const uint8_t *codes, const uint8_t *scales, double *partial, hipStream_t st) {
+  uint8_t *c = const_cast<uint8_t *>(codes), *sc = const_cast<uint8_t *>(scales);
+  const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
+  switch (pb.block) {
+    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 3>(pb, src, off, ent, c, sc, st, partial)
+                        : launch16<SIDE, DEPTH, 16, false, 3>(pb, src, off, ent, c, sc, st, partial);
+    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 3>(pb, src, off, ent, c, sc, st, partial)
+                        : launch16<SIDE, DEPTH, 32, false, 3>(pb, src, off, ent, c, sc, st, partial);
+    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 3>(pb, src, off, ent, c, sc, st, partial)
+                         : launch16<SIDE, DEPTH, 128, false, 3>(pb, src, off, ent, c, sc, st, partial);
+  }
+  return hipErrorInvalidValue;
+}
+
+// out[(bt * 2 + side) * T + r][q] = sum over the side's tiles and waves of
+// partial[((bt * tiles + tile) * waves + wave) * T + r][q], in that order.
+__global__ __launch_bounds__(256) void noise_reduce_kernel(const double *__restrict__ partial, double *__restrict__ out,
+                                                           int64_t batch, int64_t T, int64_t per_bt, int side) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;     // (bt, r, q)
+  if (i >= batch * T * 2) return;
+  const int64_t q = i & 1, r = (i >> 1) % T, bt = (i >> 1) / T;
+  double s = 0.0;
+  const double *p = partial + (bt * per_bt * T + r) * 2 + q;
+  for (int64_t k = 0; k < per_bt; ++k) s += p[k * T * 2];
+  out[((bt * 2 + side) * T + r) * 2 + q] = s;
+}
+
 }  // namespace
+
+size_t encode_noise_scratch_bytes(const Problem &pb) {
+  if (pb.depth > 2) return 0;
+  return (size_t)(noise_slots<0>(pb) + noise_slots<1>(pb)) * 2 * sizeof(double);
+}
+
+int launch_encode_noise(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
+                        const uint8_t *ws, const Workspace &wl, double *out, void *scratch, void *stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (pb.batch == 0 || pb.T == 0) return hipSuccess;
+  double *pa = reinterpret_cast<double *>(scratch);
+  double *pbp = pa + noise_slots<0>(pb) * 2;
+  const int64_t n = (noise_slots<0>(pb) + noise_slots<1>(pb)) * 2;
+  // slots a wave does not own (depth 2 deals terms out over the waves) must read as zero
+  hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)std::min<int64_t>((2 * n + 255) / 256, 4096)), dim3(256), 0, st,
+                     reinterpret_cast<uint32_t *>(scratch), 2 * n);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (pb.M > 0 && pb.K > 0) {
+    e = pb.depth == 1 ? launch_noise_side<0, 1>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, pa, st)
+                      : launch_noise_side<0, 2>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, pa, st);
+    if (e != hipSuccess) return e;
+  }
+  if (pb.N > 0 && pb.K > 0) {
+    e = pb.depth == 1 ? launch_noise_side<1, 1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, pbp, st)
+                      : launch_noise_side<1, 2>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, pbp, st);
+    if (e != hipSuccess) return e;
+  }
+  const int64_t tot = pb.batch * pb.T * 2;
+  const dim3 g((unsigned)((tot + 255) / 256));
+  hipLaunchKernelGGL(noise_reduce_kernel, g, dim3(256), 0, st, pa, out, pb.batch, pb.T, noise_slots<0>(pb) / (pb.batch * pb.T), 0);
+  hipLaunchKernelGGL(noise_reduce_kernel, g, dim3(256), 0, st, pbp, out, pb.batch, pb.T, noise_slots<1>(pb) / (pb.batch * pb.T), 1);
+  return hipGetLastError();
+}
+
 
 int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
                   uint8_t *ws, const Workspace &wl, void *stream) {

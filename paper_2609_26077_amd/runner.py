@@ -10,7 +10,7 @@ import torch
 
 from . import (FMM_LAYOUT_TILE128x128, FMM_LAYOUT_TILE256x64, Realization, fmm_combine, fmm_encode, fmm_error_stats,
                fmm_error_stats_scratch_size, fmm_matmul, fmm_multiply, fmm_operand_views,
-               fmm_plan_create, fmm_products,
+               fmm_plan_create, fmm_products, fmm_encode_noise, fmm_encode_noise_scratch_size,
                fmm_plan_workspace_size, fmm_realization_builtin, fmm_reference_f64, make_desc)
 
 
@@ -62,6 +62,19 @@ class FMM:
         """Second half of multiply (the rest of the W-combine); writes C."""
         fmm_combine(self.plan, self.ws, C, stream)
         return C
+
+    def encode_noise(self, A, B, stream=None):
+        """Operand-side rounding energy of the encoding in the workspace (call
+        after encode with the same A, B): numpy [batch][2 sides][T][2] of
+        (sum (xhat - x)^2, sum x^2) per batch element, side and term."""
+        batch, T = self.shape[0], None
+        from . import fmm_realization_terms
+        _, T = fmm_realization_terms(self.real, self.depth)
+        out = torch.empty((batch, 2, T, 2), dtype=torch.float64, device=self.device)
+        nbytes = fmm_encode_noise_scratch_size(self.plan)
+        scratch = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=self.device)
+        fmm_encode_noise(self.plan, A, B, self.ws, out, scratch, nbytes, stream)
+        return out.cpu().numpy()
 
     def operands(self):
         """(a_codes, a_scales, b_codes, b_scales) as [batch][terms][rows][kdim]
