@@ -128,8 +128,9 @@ enum {
    * scales [batch][terms][kblocks][rows]: for each block of the contracted
    * axis, one byte per row, the rows of every 256-row tile permuted so that
    * tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at byte 4 (32 h + j) + i.
-   * Used by plans whose sub-products run on 256 x 256 tiles (depth 1, E8M0
-   * scales, M / 2 and N / 2 multiples of 256). */
+   * Used by plans whose sub-products run on 256-row tiles (depth 1, E8M0
+   * scales at block 32 or 128, M / 2 and N / 2 multiples of 256; the B side
+   * is read as 128-row halves of these tiles). */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
@@ -235,7 +236,9 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
 
 /* Bytes of device workspace fmm_encode/fmm_multiply/fmm_matmul need: the
  * codes and scales of both operands, plus, at depth >= 2, the inner-level
- * partial products.  The workspace must be 256-byte aligned. */
+ * partial products, for large-tile plans the fp32 sub-products P_r, and with
+ * FMM_FLAG_B_BLOCK128 the B side's 2-D block maxima.  The workspace must be
+ * 256-byte aligned. */
 int fmm_plan_workspace_size(const fmm_plan *p, size_t *bytes);
 
 /* Steps "encode + quantize" of both operands (device pointers dA: batch x M x K,
