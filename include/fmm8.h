@@ -103,7 +103,13 @@ enum {
   /* Round each encoded B combination to bfloat16 (nearest, ties to even)
    * before its scale and cast (Appendix E: the real path's pre-round of the
    * encoded weights).  Depth 1 only. */
-  FMM_FLAG_B_BF16 = 4
+  FMM_FLAG_B_BF16 = 4,
+  /* Take the large-tile sub-product path (FMM_LAYOUT_TILE256x64) whenever
+   * the shape allows it.  Without the flag that path is taken only where
+   * K / 2^l >= 1024: it writes every fp32 P_r to the workspace and reads it
+   * back, which costs more than it saves on short contractions.  No effect on
+   * the result's definition; shapes the path cannot take ignore the flag. */
+  FMM_FLAG_LARGE_TILE = 8
 };
 
 typedef struct fmm_real fmm_real;   /* a base realization (U, V, w), R x 4 each, binary64 */
@@ -128,9 +134,10 @@ enum {
    * scales [batch][terms][kblocks][rows]: for each block of the contracted
    * axis, one byte per row, the rows of every 256-row tile permuted so that
    * tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at byte 4 (32 h + j) + i.
-   * Used by plans whose sub-products run on 256-row tiles (depth 1, E8M0
-   * scales at block 32 or 128, M / 2 and N / 2 multiples of 256; the B side
-   * is read as 128-row halves of these tiles). */
+   * Used by plans whose sub-products run on 256-row tiles (depth 1 or 2,
+   * E8M0 scales at block 32 or 128, M / 2^l and N / 2^l multiples of 256,
+   * K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE; the B side is read as 128-row
+   * halves of these tiles). */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
@@ -235,8 +242,9 @@ void fmm_realization_destroy(fmm_real *d);
 int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out);
 
 /* Bytes of device workspace fmm_encode/fmm_multiply/fmm_matmul need: the
- * codes and scales of both operands, plus, at depth >= 2, the inner-level
- * partial products, for large-tile plans the fp32 sub-products P_r, and with
+ * codes and scales of both operands, plus, for large-tile plans the fp32
+ * sub-products P_r, for the others at depth >= 2 the inner-level partial
+ * products, and with
  * FMM_FLAG_B_BLOCK128 the B side's 2-D block maxima.  The workspace must be
  * 256-byte aligned. */
 int fmm_plan_workspace_size(const fmm_plan *p, size_t *bytes);
@@ -256,9 +264,11 @@ int fmm_multiply(const fmm_plan *p, void *dWs, float *dC, void *stream);
 
 /* The first half of fmm_multiply: the T block-scaled fp8 sub-products with
  * fp32 accumulation.  Plans with the large-tile layout (fmm_view.code_layout
- * == FMM_LAYOUT_TILE256x64) write every P_r, fp32, to the workspace; the
- * others fold the base-level w into the sub-product kernel and write C
- * (depth 1) or the per-outer-term partial sums (depth >= 2, workspace). */
+ * == FMM_LAYOUT_TILE256x64) write every P_r, fp32, to the workspace (and
+ * fmm_combine forms C = sum_r w_r (x) P_r over all T terms in one pass, in
+ * ascending r with one fused multiply-add per nonzero weight); the others
+ * fold the base-level w into the sub-product kernel and write C (depth 1) or
+ * the per-outer-term partial sums (depth >= 2, workspace). */
 int fmm_products(const fmm_plan *p, void *dWs, float *dC, void *stream);
 
 /* The second half of fmm_multiply: what remains of the W-combine after

@@ -57,6 +57,7 @@ BUILTINS = {"cubic8": FMM_CUBIC8, "strassen": FMM_STRASSEN, "winograd": FMM_WINO
 FMM_FLAG_EXACT_DOT = 1
 FMM_FLAG_B_BLOCK128 = 2
 FMM_FLAG_B_BF16 = 4
+FMM_FLAG_LARGE_TILE = 8
 FMM_LAYOUT_ROWS = 0
 FMM_LAYOUT_TILE256x64 = 1
 FMM_LAYOUT_TILE128x128 = 2

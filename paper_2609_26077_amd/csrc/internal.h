@@ -12,6 +12,7 @@ constexpr int kMaxRank = 8;    // <2,2,2;R>, R <= 8 (cubic has 8 terms)
 constexpr int kMaxDepth = 3;
 constexpr int kSplitTile = 256;  // A rows per tile of the large-tile sub-product path (and code image rows)
 constexpr int kSplitTileN = 128; // B rows per tile of that path (half a code image)
+constexpr int64_t kSplitMinK = 1024;  // smallest K / 2^l the large-tile path takes by default
 
 struct Realization {
   int R;
@@ -54,7 +55,7 @@ struct Problem {
   int64_t kblocks;         // kp / block
   int scale_bytes;         // 1 (E8M0) or 4 (fp32)
   int exact_dot;           // FMM_FLAG_EXACT_DOT requested
-  int split;               // large-tile sub-products + separate W-combine (depth 1, tile-aligned MX)
+  int split;               // large-tile sub-products + separate W-combine (depth <= 2, tile-aligned MX)
   int layout;              // FMM_LAYOUT_* of the workspace's codes and scales
   int b_rows;              // rows of y_r^T per B scale block: 1, or 128 (FMM_FLAG_B_BLOCK128)
   int b_bf16;              // round encoded B combinations to bfloat16 first (FMM_FLAG_B_BF16)
@@ -81,6 +82,9 @@ struct DeviceTables {
   const CoefEntry *b_ent;
   const float *w_inner;        // R x 4 fp32 base w (the inner-level decoder), zero-padded to kMaxRank x 4
   const float *w_outer;        // To x 4^(l-1) fp32 flattened depth-(l-1) w (depth >= 2)
+  const float *w_full;         // T x 16 fp32 flattened depth-2 w (large-tile plans at depth 2)
+  const float *u_dense;        // T x 4^l fp32 flattened U, zeros included
+  const float *v_dense;        // T x 4^l fp32 flattened V, zeros included
 };
 
 // ---- launchers (kernels_*.hip); return a hipError_t as int ---------------

@@ -28,6 +28,31 @@ namespace fmm {
 
 namespace {
 
+// One operand side's coefficient tables: the nonzero entries of every term in
+// ascending block order (offsets, entries; read at depth 1) and the dense
+// flattened rows, T x 4^l fp32 with zeros (read at depths 2 and 3).
+struct SideTab {
+  const int32_t *off;
+  const CoefEntry *ent;
+  const float *dense;
+};
+inline SideTab a_tab(const DeviceTables &t) { return {t.a_off, t.a_ent, t.u_dense}; }
+inline SideTab b_tab(const DeviceTables &t) { return {t.b_off, t.b_ent, t.v_dense}; }
+
+// The coefficient of block b of a dense row spread one block per lane (b uniform).
+__device__ __forceinline__ float lane_coef(float c, int b) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c), b));
+}
+
+// Takes the lowest set bit of a uniform mask (the next nonzero block in
+// ascending order) or, once the mask is empty, repeats `prev`.
+__device__ __forceinline__ int next_block(uint64_t &mask, int prev) {
+  if (mask == 0) return prev;
+  const int b = __builtin_ctzll(mask);
+  mask &= mask - 1;
+  return b;
+}
+
 constexpr int kTL = 128;            // contracted positions per tile (>= every block size)
 constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slots, odd, so
                                     // 16-byte accesses of 16 lanes in 4 consecutive rows x
@@ -41,7 +66,9 @@ template <int DEPTH, int VEC, int SIDE>
 struct Tile {
   static constexpr int nblk = 1 << (2 * DEPTH);
   static constexpr int TR = VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
-  static constexpr int threads = VEC == 16 && DEPTH == 1 && SIDE == 0 ? 128 : 256;
+  // depth 1: 128 (A) or 256 (B) threads; depths 2 and 3 deal the terms out to
+  // eight waves, which with two workgroups per CU keeps four waves per SIMD
+  static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? 128 : 256) : 512;
   static constexpr int lds_floats = nblk * TR * kStride;   // 33.8 (A) / 67.6 (B), 67.6, 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
 };
@@ -209,8 +236,7 @@ __device__ __forceinline__ float bf16_round(float x) {
 
 template <int SIDE, int DEPTH, int BS, bool F32, int MODE>
 __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_kernel(
-    const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
-    const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
+    const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l, void *__restrict__ aux) {
   static_assert(MODE == 0 || MODE == 3 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
   uint32_t *amax = reinterpret_cast<uint32_t *>(aux);
@@ -240,27 +266,73 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
   const int64_t scale_plane = scale_plane_of(pb, rows);
   const int64_t T = pb.T;
 
+  // depth 2: the term's dense coefficient row (block b in lane b) is loaded
+  // one term ahead by a vector load, so the term loop never waits on scalar
+  // memory; its nonzero blocks come from the wave's ballot in ascending order
+  float cnext = 0.0f;
+  if constexpr (DEPTH >= 2) {
+    const int64_t rf = wave / WPT;
+    if (rf < T && lane < NB) cnext = cf.dense[rf * NB + lane];
+  }
   for (int64_t r = wave / WPT; r < T; r += TSTEP) {
-    const int beg = __builtin_amdgcn_readfirstlane(off[r]);
-    const int nc = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
-    CoefEntry ce[NB];
-#pragma unroll
-    for (int e = 0; e < NB; ++e)
-      if (e < nc) ce[e] = ent[beg + e];
     // x = sum_b c_b a_b in ascending b: products and sums rounded separately
     float x[16];
+    if constexpr (DEPTH >= 2) {
+      const float c = cnext;
+      if (r + TSTEP < T && lane < NB) cnext = cf.dense[(r + TSTEP) * NB + lane];
+      uint64_t mask = __ballot(c != 0.0f);
+      if (mask == 0) {
 #pragma unroll
-    for (int e = 0; e < NB; ++e) {
-      if (e < nc) {
-        const float4 *p = reinterpret_cast<const float4 *>(lrow + ce[e].block * (TR * kStride));
-        const float4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
-        const float a[16] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w,
-                             v2.x, v2.y, v2.z, v2.w, v3.x, v3.y, v3.z, v3.w};
-        const float c = ce[e].coef;
+        for (int i = 0; i < 16; ++i) x[i] = 0.0f;
+      }
+      bool first = true;
+      while (mask != 0) {
+        // two blocks per pass (the second repeats the first when there is none)
+        const int b0 = next_block(mask, 0);
+        const bool two = mask != 0;
+        const int b1 = next_block(mask, b0);
+        const float4 *p0 = reinterpret_cast<const float4 *>(lrow + b0 * (TR * kStride));
+        const float4 *p1 = reinterpret_cast<const float4 *>(lrow + b1 * (TR * kStride));
+        const float4 v[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
+        const float c0 = lane_coef(c, b0), c1 = lane_coef(c, b1);
+        const float *a = reinterpret_cast<const float *>(v);
+        if (first) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float pr = __fmul_rn(c, a[i]);
-          x[i] = e == 0 ? pr : __fadd_rn(x[i], pr);
+          for (int i = 0; i < 16; ++i) x[i] = __fmul_rn(c0, a[i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) x[i] = __fadd_rn(x[i], __fmul_rn(c0, a[i]));
+        }
+        first = false;
+        if (two) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) x[i] = __fadd_rn(x[i], __fmul_rn(c1, a[16 + i]));
+        }
+      }
+    } else {
+      const int beg = __builtin_amdgcn_readfirstlane(cf.off[r]);
+      const int nc = __builtin_amdgcn_readfirstlane(cf.off[r + 1]) - beg;
+      CoefEntry ce[NB];
+#pragma unroll
+      for (int e = 0; e < NB; ++e)
+        if (e < nc) ce[e] = cf.ent[beg + e];
+      if (nc == 0) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) x[i] = 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < NB; ++e) {
+        if (e < nc) {
+          const float4 *p = reinterpret_cast<const float4 *>(lrow + ce[e].block * (TR * kStride));
+          const float4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
+          const float a[16] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w,
+                               v2.x, v2.y, v2.z, v2.w, v3.x, v3.y, v3.z, v3.w};
+          const float c = ce[e].coef;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const float pr = __fmul_rn(c, a[i]);
+            x[i] = e == 0 ? pr : __fadd_rn(x[i], pr);
+          }
         }
       }
     }
@@ -377,14 +449,13 @@ __device__ __forceinline__ float group_max(float m, int gl) {
 }
 
 template <int SIDE>
-__global__ __launch_bounds__(256) void encode4_kernel(
-    const float *__restrict__ src, Problem pb, const int32_t *__restrict__ off,
-    const CoefEntry *__restrict__ ent, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
+__global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
+    const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
   using TT = Tile<3, 4, SIDE>;
-  constexpr int TR = TT::TR;
+  constexpr int TR = TT::TR, NT = TT::threads;
   constexpr int P = TR * (kTL / 4);          // positions (row, 4 consecutive l) per term
-  static_assert(256 % P == 0 && P % 64 == 0, "a wave's 64 items belong to one term; a thread keeps one position");
+  static_assert(P == 64 && TT::nblk == 64, "a wave's 64 items are one term's tile; lane b holds block b's coefficient");
   __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
 
@@ -393,7 +464,7 @@ __global__ __launch_bounds__(256) void encode4_kernel(
   const int64_t row0 = (blockIdx.x / tiles_l) * TR;
   const int64_t l0 = (blockIdx.x % tiles_l) * kTL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  stage_tile<SIDE, TT::nblk, TR, 256>(lds, src, pb, bt, row0, l0, t);
+  stage_tile<SIDE, TT::nblk, TR, NT>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
 
   const int64_t T = pb.T;
@@ -404,23 +475,40 @@ __global__ __launch_bounds__(256) void encode4_kernel(
   const int64_t code_plane = rows * pb.kp;
   const int64_t scale_plane = scale_plane_of(pb, rows);
   const float *lrow = lds + row * kStride + 4 * c4;
-  for (int64_t it = t; it < T * P; it += 256) {
-    const int64_t r = __builtin_amdgcn_readfirstlane((int)(it / P));
-    const int beg = __builtin_amdgcn_readfirstlane(off[r]);
-    const int nc = __builtin_amdgcn_readfirstlane(off[r + 1]) - beg;
+  // the term's dense coefficient row (block b in lane b; 64 blocks) is loaded
+  // one term ahead by a vector load; its nonzero blocks come from the wave's
+  // ballot in ascending order, four per pass
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  constexpr int WSTEP = NT / 64;             // a wave per term
+  float cnext = 0.0f;
+  if (wave < T) cnext = cf.dense[wave * 64 + lane];
+  for (int64_t r = wave; r < T; r += WSTEP) {
+    const float c = cnext;
+    if (r + WSTEP < T) cnext = cf.dense[(r + WSTEP) * 64 + lane];
+    uint64_t mask = __ballot(c != 0.0f);
     float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
-    for (int e0 = 0; e0 < nc; e0 += 4) {
+    bool first = true;
+    while (mask != 0) {
+      int b[4];
+      bool have[4];
+      b[0] = next_block(mask, 0);
+      have[0] = true;
+#pragma unroll
+      for (int j = 1; j < 4; ++j) {
+        have[j] = mask != 0;
+        b[j] = next_block(mask, b[j - 1]);
+      }
       float4 v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (e0 + e < nc) v[e] = *reinterpret_cast<const float4 *>(lrow + ent[beg + e0 + e].block * (TR * kStride));
+      for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4 *>(lrow + b[j] * (TR * kStride));
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (e0 + e < nc) {
-          const float c = ent[beg + e0 + e].coef;
-          const float t0 = __fmul_rn(c, v[e].x), t1 = __fmul_rn(c, v[e].y);
-          const float t2 = __fmul_rn(c, v[e].z), t3 = __fmul_rn(c, v[e].w);
-          if (e0 + e == 0) {
+      for (int j = 0; j < 4; ++j) {
+        if (have[j]) {
+          const float cb = lane_coef(c, b[j]);
+          const float t0 = __fmul_rn(cb, v[j].x), t1 = __fmul_rn(cb, v[j].y);
+          const float t2 = __fmul_rn(cb, v[j].z), t3 = __fmul_rn(cb, v[j].w);
+          if (first && j == 0) {
             x0 = t0; x1 = t1; x2 = t2; x3 = t3;
           } else {
             x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
@@ -428,6 +516,7 @@ __global__ __launch_bounds__(256) void encode4_kernel(
           }
         }
       }
+      first = false;
     }
     const float m = group_max(fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3))), gl);
     const dev::Scale sc = dev::block_scale(m, pb.rule);
@@ -440,15 +529,15 @@ __global__ __launch_bounds__(256) void encode4_kernel(
 }
 
 template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0>
-hipError_t launch16(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
                     uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
   using TT = Tile<DEPTH, 16, SIDE>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE>), grid, dim3(TT::threads), 0, st, src, pb, off,
-                     ent, codes, scales, tiles_l, amax);
+  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE>), grid, dim3(TT::threads), 0, st, src, pb, cf, codes,
+                     scales, tiles_l, amax);
   return hipGetLastError();
 }
 
@@ -460,7 +549,7 @@ __global__ __launch_bounds__(256) void zero_u32_kernel(uint32_t *p, int64_t n) {
 // block maxima (zeroed, then merged by MODE 1) when blocks span 128 rows,
 // then the quantizing pass.
 template <int BS, bool F32>
-hipError_t launch_b_deploy(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+hipError_t launch_b_deploy(const Problem &pb, const float *src, const SideTab &cf,
                            uint8_t *codes, uint8_t *scales, uint32_t *amax, hipStream_t st) {
   if (pb.b_rows > 1) {
     const int64_t n = pb.batch * pb.T * ((pb.np + 127) / 128) * pb.kblocks;
@@ -468,53 +557,54 @@ hipError_t launch_b_deploy(const Problem &pb, const float *src, const int32_t *o
     hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, st, amax, n);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch16<1, 1, BS, F32, 1>(pb, src, off, ent, codes, scales, st, amax);
+    e = launch16<1, 1, BS, F32, 1>(pb, src, cf, codes, scales, st, amax);
     if (e != hipSuccess) return e;
   }
-  return launch16<1, 1, BS, F32, 2>(pb, src, off, ent, codes, scales, st, amax);
+  return launch16<1, 1, BS, F32, 2>(pb, src, cf, codes, scales, st, amax);
 }
 
-hipError_t launch_b_deploy_any(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+hipError_t launch_b_deploy_any(const Problem &pb, const float *src, const SideTab &cf,
                                uint8_t *codes, uint8_t *scales, uint32_t *amax, hipStream_t st) {
   const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
   switch (pb.block) {
-    case 16: return f32 ? launch_b_deploy<16, true>(pb, src, off, ent, codes, scales, amax, st)
-                        : launch_b_deploy<16, false>(pb, src, off, ent, codes, scales, amax, st);
-    case 32: return f32 ? launch_b_deploy<32, true>(pb, src, off, ent, codes, scales, amax, st)
-                        : launch_b_deploy<32, false>(pb, src, off, ent, codes, scales, amax, st);
-    case 128: return f32 ? launch_b_deploy<128, true>(pb, src, off, ent, codes, scales, amax, st)
-                         : launch_b_deploy<128, false>(pb, src, off, ent, codes, scales, amax, st);
+    case 16: return f32 ? launch_b_deploy<16, true>(pb, src, cf, codes, scales, amax, st)
+                        : launch_b_deploy<16, false>(pb, src, cf, codes, scales, amax, st);
+    case 32: return f32 ? launch_b_deploy<32, true>(pb, src, cf, codes, scales, amax, st)
+                        : launch_b_deploy<32, false>(pb, src, cf, codes, scales, amax, st);
+    case 128: return f32 ? launch_b_deploy<128, true>(pb, src, cf, codes, scales, amax, st)
+                         : launch_b_deploy<128, false>(pb, src, cf, codes, scales, amax, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <int SIDE, int DEPTH>
-hipError_t launch_wide(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+hipError_t launch_wide(const Problem &pb, const float *src, const SideTab &cf,
                        uint8_t *codes, uint8_t *scales, hipStream_t st) {
   const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
   switch (pb.block) {
-    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true>(pb, src, off, ent, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 16, false>(pb, src, off, ent, codes, scales, st);
-    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true>(pb, src, off, ent, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 32, false>(pb, src, off, ent, codes, scales, st);
-    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true>(pb, src, off, ent, codes, scales, st)
-                         : launch16<SIDE, DEPTH, 128, false>(pb, src, off, ent, codes, scales, st);
+    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 16, false>(pb, src, cf, codes, scales, st);
+    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 32, false>(pb, src, cf, codes, scales, st);
+    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true>(pb, src, cf, codes, scales, st)
+                         : launch16<SIDE, DEPTH, 128, false>(pb, src, cf, codes, scales, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <int SIDE>
-hipError_t launch_side(const Problem &pb, const float *src, const int32_t *off,
-                       const CoefEntry *ent, uint8_t *codes, uint8_t *scales, hipStream_t st) {
+hipError_t launch_side(const Problem &pb, const float *src, const SideTab &cf,
+                       uint8_t *codes, uint8_t *scales, hipStream_t st) {
   switch (pb.depth) {
-    case 1: return launch_wide<SIDE, 1>(pb, src, off, ent, codes, scales, st);
-    case 2: return launch_wide<SIDE, 2>(pb, src, off, ent, codes, scales, st);
+    case 1: return launch_wide<SIDE, 1>(pb, src, cf, codes, scales, st);
+    case 2: return launch_wide<SIDE, 2>(pb, src, cf, codes, scales, st);
     case 3: {
       const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
       const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
       const int64_t tiles_r = (rows + Tile<3, 4, SIDE>::TR - 1) / Tile<3, 4, SIDE>::TR;
       const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-      hipLaunchKernelGGL((encode4_kernel<SIDE>), grid, dim3(256), 0, st, src, pb, off, ent, codes, scales, tiles_l);
+      hipLaunchKernelGGL((encode4_kernel<SIDE>), grid, dim3(Tile<3, 4, SIDE>::threads), 0, st, src, pb, cf, codes,
+                         scales, tiles_l);
       return hipGetLastError();
     }
   }
@@ -533,17 +623,17 @@ int64_t noise_slots(const Problem &pb) {
 }
 
 template <int SIDE, int DEPTH>
-hipError_t launch_noise_side(const Problem &pb, const float *src, const int32_t *off, const CoefEntry *ent,
+hipError_t launch_noise_side(const Problem &pb, const float *src, const SideTab &cf,
                              const uint8_t *codes, const uint8_t *scales, double *partial, hipStream_t st) {
   uint8_t *c = const_cast<uint8_t *>(codes), *sc = const_cast<uint8_t *>(scales);
   const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
   switch (pb.block) {
-    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 3>(pb, src, off, ent, c, sc, st, partial)
-                        : launch16<SIDE, DEPTH, 16, false, 3>(pb, src, off, ent, c, sc, st, partial);
-    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 3>(pb, src, off, ent, c, sc, st, partial)
-                        : launch16<SIDE, DEPTH, 32, false, 3>(pb, src, off, ent, c, sc, st, partial);
-    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 3>(pb, src, off, ent, c, sc, st, partial)
-                         : launch16<SIDE, DEPTH, 128, false, 3>(pb, src, off, ent, c, sc, st, partial);
+    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 3>(pb, src, cf, c, sc, st, partial)
+                        : launch16<SIDE, DEPTH, 16, false, 3>(pb, src, cf, c, sc, st, partial);
+    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 3>(pb, src, cf, c, sc, st, partial)
+                        : launch16<SIDE, DEPTH, 32, false, 3>(pb, src, cf, c, sc, st, partial);
+    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 3>(pb, src, cf, c, sc, st, partial)
+                         : launch16<SIDE, DEPTH, 128, false, 3>(pb, src, cf, c, sc, st, partial);
   }
   return hipErrorInvalidValue;
 }
@@ -581,13 +671,13 @@ int launch_encode_noise(const Problem &pb, const DeviceTables &tab, const float 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (pb.M > 0 && pb.K > 0) {
-    e = pb.depth == 1 ? launch_noise_side<0, 1>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, pa, st)
-                      : launch_noise_side<0, 2>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, pa, st);
+    e = pb.depth == 1 ? launch_noise_side<0, 1>(pb, A, a_tab(tab), ws + wl.a_codes, ws + wl.a_scales, pa, st)
+                      : launch_noise_side<0, 2>(pb, A, a_tab(tab), ws + wl.a_codes, ws + wl.a_scales, pa, st);
     if (e != hipSuccess) return e;
   }
   if (pb.N > 0 && pb.K > 0) {
-    e = pb.depth == 1 ? launch_noise_side<1, 1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, pbp, st)
-                      : launch_noise_side<1, 2>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, pbp, st);
+    e = pb.depth == 1 ? launch_noise_side<1, 1>(pb, B, b_tab(tab), ws + wl.b_codes, ws + wl.b_scales, pbp, st)
+                      : launch_noise_side<1, 2>(pb, B, b_tab(tab), ws + wl.b_codes, ws + wl.b_scales, pbp, st);
     if (e != hipSuccess) return e;
   }
   const int64_t tot = pb.batch * pb.T * 2;
@@ -602,12 +692,12 @@ int launch_encode(const Problem &pb, const DeviceTables &tab, const float *A, co
                   uint8_t *ws, const Workspace &wl, void *stream) {
   if (pb.batch == 0 || pb.M == 0 || pb.N == 0 || pb.K == 0) return hipSuccess;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = launch_side<0>(pb, A, tab.a_off, tab.a_ent, ws + wl.a_codes, ws + wl.a_scales, st);
+  hipError_t e = launch_side<0>(pb, A, a_tab(tab), ws + wl.a_codes, ws + wl.a_scales, st);
   if (e != hipSuccess) return e;
   if (pb.b_rows > 1 || pb.b_bf16)
-    return launch_b_deploy_any(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales,
+    return launch_b_deploy_any(pb, B, b_tab(tab), ws + wl.b_codes, ws + wl.b_scales,
                                reinterpret_cast<uint32_t *>(ws + wl.b_amax), st);
-  return launch_side<1>(pb, B, tab.b_off, tab.b_ent, ws + wl.b_codes, ws + wl.b_scales, st);
+  return launch_side<1>(pb, B, b_tab(tab), ws + wl.b_codes, ws + wl.b_scales, st);
 }
 
 }  // namespace fmm

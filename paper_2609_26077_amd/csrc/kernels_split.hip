@@ -1,4 +1,4 @@
-// Large-tile sub-products for tile-aligned block-scaled problems at depth 1.
+// Large-tile sub-products for tile-aligned block-scaled problems at depths 1 and 2.
 //
 // The sub-products are the dominant cost; each is a plain block-scaled fp8
 // GEMM P_r = A_r B_r^T with fp32 accumulation.  Large tiles halve the operand
@@ -15,7 +15,8 @@
 //      stored in fp32 with nontemporal stores.
 //   2. combine1_kernel: C block (i, k) = sum_r w[r][2k + i] P_r, ascending r,
 //      one fused multiply-add per nonzero weight (the order of the fused
-//      W-combine of the 128 x 128 path).
+//      W-combine of the 128 x 128 path); combine2_kernel the same over the
+//      T = R^2 flattened terms and 16 blocks of depth 2.
 //
 // Scales of these plans are stored K-block-major by the encoder: for each
 // (term, K block) the E8M0 bytes of all rows, permuted inside every 256-row
@@ -269,6 +270,65 @@ __global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__
   }
 }
 
+// Depth 2: C block (I, K) of batch element bt, rows I m' + p, columns
+// K n' + 4 q4 .. + 3, I, K < 4: sum over the T flattened terms of
+// w[r][4K + I] P_r[p][4 q4 ..], ascending r, fma per nonzero weight, with the
+// 16 blocks' accumulators in registers so that every P_r is read once.  The
+// weights are uniform over the grid (scalar loads).
+template <bool VEC>
+__global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__ P, const float *__restrict__ w,
+                                                       float *__restrict__ C, Problem pb) {
+  const int64_t n4 = pb.np / 4;
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // p * n4 + q4
+  const int64_t bt = blockIdx.y;
+  if (pos >= pb.mp * n4) return;
+  const int64_t p = pos / n4, q4 = pos - p * n4;
+  const int64_t plane = pb.mp * pb.np;
+  const float *src = P + (bt * pb.T * pb.mp + p) * pb.np + 4 * q4;
+  float4 acc[16];
+#pragma unroll
+  for (int b = 0; b < 16; ++b) acc[b] = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int T = (int)pb.T;
+  // eight terms' loads are issued together, ahead of the (uniformly branching)
+  // multiply-adds; past the last term the index is clamped and the load unused
+  for (int r0 = 0; r0 < T; r0 += 8) {
+    f4v x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int r = min(r0 + j, T - 1);
+      x[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(src + r * plane));
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (r0 + j < T) {
+        float wr[16];   // one scalar load of the term's 16 weights
+#pragma unroll
+        for (int b = 0; b < 16; ++b) wr[b] = w[16 * (r0 + j) + b];
+#pragma unroll
+        for (int b = 0; b < 16; ++b) {
+          const float wb = wr[b];
+          if (wb != 0.0f) {
+            acc[b].x = __fmaf_rn(wb, x[j].x, acc[b].x);
+            acc[b].y = __fmaf_rn(wb, x[j].y, acc[b].y);
+            acc[b].z = __fmaf_rn(wb, x[j].z, acc[b].z);
+            acc[b].w = __fmaf_rn(wb, x[j].w, acc[b].w);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < 16; ++b) {
+    const int i = b & 3, k = b >> 2;
+    float *dst = C + bt * pb.M * pb.N + (i * pb.mp + p) * pb.N + k * pb.np + 4 * q4;
+    if (VEC) {
+      *reinterpret_cast<float4 *>(dst) = acc[b];
+    } else {
+      dst[0] = acc[b].x; dst[1] = acc[b].y; dst[2] = acc[b].z; dst[3] = acc[b].w;
+    }
+  }
+}
+
 }  // namespace
 
 int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace &wl, void *stream) {
@@ -296,7 +356,15 @@ int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8
   const float *P = reinterpret_cast<const float *>(ws + wl.products);
   const int64_t npos = pb.mp * (pb.np / 4);
   const dim3 g2((unsigned)((npos + 255) / 256), (unsigned)pb.batch);
-  if ((reinterpret_cast<uintptr_t>(C) & 15) == 0)
+  const bool vec = (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+  if (pb.depth == 2) {
+    if (vec)
+      hipLaunchKernelGGL(combine2_kernel<true>, g2, dim3(256), 0, st, P, tab.w_full, C, pb);
+    else
+      hipLaunchKernelGGL(combine2_kernel<false>, g2, dim3(256), 0, st, P, tab.w_full, C, pb);
+    return hipGetLastError();
+  }
+  if (vec)
     hipLaunchKernelGGL(combine1_kernel<true>, g2, dim3(256), 0, st, P, tab.w_inner, C, pb);
   else
     hipLaunchKernelGGL(combine1_kernel<false>, g2, dim3(256), 0, st, P, tab.w_inner, C, pb);

@@ -68,7 +68,7 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   *out = nullptr;
   if (!d || !desc) return FMM_ERR_ARG;
   const fmm_plan_desc &q = *desc;
-  constexpr int kFlags = FMM_FLAG_EXACT_DOT | FMM_FLAG_B_BLOCK128 | FMM_FLAG_B_BF16;
+  constexpr int kFlags = FMM_FLAG_EXACT_DOT | FMM_FLAG_B_BLOCK128 | FMM_FLAG_B_BF16 | FMM_FLAG_LARGE_TILE;
   if ((q.flags & ~kFlags) != 0 || q.batch < 0 || q.M < 0 || q.K < 0 || q.N < 0) return FMM_ERR_ARG;
   if (q.depth < 1 || q.depth > fmm::kMaxDepth) return FMM_ERR_ARG;
   if (q.block != 16 && q.block != 32 && q.block != 128) return FMM_ERR_ARG;
@@ -99,12 +99,17 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
   pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
   const bool mx = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
-  // large-tile path: E8M0 scales applied by the MFMA, one level, 256-row tiles,
-  // whole 64-byte (block 32) or 128-byte (block 128) K steps
-  pb.split = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
-             q.depth == 1 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
+  // large-tile path: E8M0 scales applied by the MFMA, one or two levels,
+  // 256-row tiles, whole 64-byte (block 32) or 128-byte (block 128) K steps.
+  // It writes every P_r (4 bytes per output of each term) and reads it back,
+  // 8 / k' bytes per flop against the fused path's none: taken by default
+  // where that round trip costs less than the fused path's smaller tiles,
+  // k' >= 1024 (measured: the large tiles win at 1024, lose at 256).
+  const bool split_shape = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
+             q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
              pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
              q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);
+  pb.split = split_shape && (pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
   // fused 128 x 128 path: E8M0 scales, whole 128-row tiles and 128-byte K steps
   const bool tile128 = mx && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 && pb.kp % 128 == 0 &&
                        pb.kp < (int64_t(1) << 26);
@@ -119,7 +124,7 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   wl.a_scales = off; off = align256(off + B * T * fmm::scale_plane_bytes(pb, pb.mp));
   wl.b_scales = off; off = align256(off + B * T * fmm::scale_plane_bytes(pb, pb.np));
   wl.partial = off;
-  if (q.depth >= 2) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
+  if (q.depth >= 2 && !pb.split) off = align256(off + B * pb.To * 4 * pb.mp * pb.np * sizeof(float));
   wl.products = off;
   if (pb.split) off = align256(off + B * T * pb.mp * pb.np * sizeof(float));
   wl.b_amax = off;
@@ -151,15 +156,24 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
     wouter.resize((size_t)pb.To * no);
     fmm_realization_tables(d, q.depth - 1, nullptr, nullptr, wouter.data());
   }
+  // large-tile plans at depth 2 combine all T terms in one pass: the flattened w
+  std::vector<float> wfull;
+  if (pb.split && q.depth == 2) {
+    wfull.resize((size_t)T * 16);
+    fmm_realization_tables(d, 2, nullptr, nullptr, wfull.data());
+  }
 
-  // device copy: [aoff][boff][aent][bent][winner][wouter]
+  // device copy: [aoff][boff][aent][bent][winner][wouter][wfull][U][V]
   const size_t s_aoff = align256((T + 1) * sizeof(int32_t));
   const size_t s_boff = s_aoff;
   const size_t s_aent = align256(std::max<size_t>(1, aent.size()) * sizeof(fmm::CoefEntry));
   const size_t s_bent = align256(std::max<size_t>(1, bent.size()) * sizeof(fmm::CoefEntry));
   const size_t s_wi = align256((size_t)fmm::kMaxRank * 4 * sizeof(float));   // zero-padded to 8 x 4
   const size_t s_wo = align256(std::max<size_t>(1, wouter.size()) * sizeof(float));
-  const size_t tot = s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo;
+  const size_t s_wf = align256(std::max<size_t>(1, wfull.size()) * sizeof(float));
+  const size_t s_ud = align256(U.size() * sizeof(float));   // dense flattened rows (the encoder at depths 2, 3)
+  const size_t o_ud = s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo + s_wf;
+  const size_t tot = o_ud + 2 * s_ud;
   std::vector<uint8_t> host(tot, 0);
   std::memcpy(host.data(), aoff.data(), (T + 1) * sizeof(int32_t));
   std::memcpy(host.data() + s_aoff, boff.data(), (T + 1) * sizeof(int32_t));
@@ -170,6 +184,11 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if (!wouter.empty())
     std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent + s_wi, wouter.data(),
                 wouter.size() * sizeof(float));
+  std::memcpy(host.data() + o_ud, U.data(), U.size() * sizeof(float));
+  std::memcpy(host.data() + o_ud + s_ud, V.data(), V.size() * sizeof(float));
+  if (!wfull.empty())
+    std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo, wfull.data(),
+                wfull.size() * sizeof(float));
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) {
@@ -197,6 +216,9 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   p->tab.b_ent = reinterpret_cast<const fmm::CoefEntry *>(base + s_aoff + s_boff + s_aent);
   p->tab.w_inner = reinterpret_cast<const float *>(base + s_aoff + s_boff + s_aent + s_bent);
   p->tab.w_outer = reinterpret_cast<const float *>(base + s_aoff + s_boff + s_aent + s_bent + s_wi);
+  p->tab.w_full = reinterpret_cast<const float *>(base + s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo);
+  p->tab.u_dense = reinterpret_cast<const float *>(base + o_ud);
+  p->tab.v_dense = reinterpret_cast<const float *>(base + o_ud + s_ud);
   *out = p;
   return FMM_OK;
 }

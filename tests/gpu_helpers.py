@@ -75,8 +75,10 @@ def run_gpu(spec, A, B, depth, bs, rule, exact=False, flags=0):
     Cref = reference_f64(dA, dB)
     err2, ref2 = error_stats(C, Cref)
     ops = [t.cpu().numpy() for t in f.operands()]
+    from paper_2609_26077_amd import fmm_operand_views
+    layout = fmm_operand_views(f.plan, f.ws)[0].code_layout
     out = {"C": C.cpu().numpy(), "err2": err2, "ref2": ref2, "ops": ops,
-           "Cref": Cref.cpu().numpy()}
+           "Cref": Cref.cpu().numpy(), "layout": layout}
     return out
 
 
@@ -99,18 +101,22 @@ def abs_bound(o, wtab, depth, M, N):
 
 
 def check_case(spec, family, batch, M, K, N, depth, bs, rule, seed=0, cfg=0, trial=0,
-               check_every=None, exact=False, ns=True, b_rows=1, b_bf16=False):
+               check_every=None, exact=False, ns=True, b_rows=1, b_bf16=False, flags=0,
+               layout=None):
     """Run one configuration on both sides and assert every bar above.
     b_rows = 128 / b_bf16: the weight-side deployment granularity
-    (FMM_FLAG_B_BLOCK128 / FMM_FLAG_B_BF16)."""
+    (FMM_FLAG_B_BLOCK128 / FMM_FLAG_B_BF16); flags: further FMM_FLAG_* bits;
+    layout: the FMM_LAYOUT_* the plan must take (the sub-product path)."""
     mx = uses_mx(bs, rule, exact)
     g_dot = 2.0 ** -10 if mx else 2.0 ** -19
     A, B = gen.operands(family, batch, M, K, N, seed=seed, cfg=cfg, trial=trial)
     D = oracle_realization(spec)
     tabs = R.tables_f32(D, depth)
     T = tabs[0].shape[0]
-    flags = (2 if b_rows == 128 else 0) | (4 if b_bf16 else 0)
+    flags |= (2 if b_rows == 128 else 0) | (4 if b_bf16 else 0)
     g = run_gpu(spec, A, B, depth, bs, rule, exact, flags)
+    if layout is not None:
+        assert g["layout"] == layout, ("plan took layout", g["layout"])
     kp = K // 2 ** depth
     errs, refs = [], []
     worst_rel_fro = 0.0

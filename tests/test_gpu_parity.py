@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import fmm_inputs as gen
+from paper_2609_26077_amd import FMM_FLAG_LARGE_TILE, FMM_LAYOUT_TILE128x128, FMM_LAYOUT_TILE256x64
 from tests.gpu_helpers import check_case
 
 pytestmark = pytest.mark.gpu
@@ -89,7 +90,7 @@ def test_rebased_realization():
     # (rule, block, b_rows, bf16, shape): the paper's real-kernel setting first
     (0, 128, 128, True, (1, 384, 512, 320)),      # fp32 amax/448, 128 x 128 weight blocks, bf16; ragged 160-row tail
     (1, 128, 128, True, (2, 256, 512, 640)),      # E8M0 scales on the MX path
-    (1, 32, 128, False, (1, 512, 256, 512)),      # large-tile plan (m', n' = 256)
+    (1, 32, 128, False, (1, 512, 256, 512)),      # large-tile plan (m', n' = 256, forced)
     (2, 128, 128, False, (1, 130, 256, 258)),     # ragged everything
     (1, 16, 1, True, (1, 192, 256, 128)),         # bfloat16 pre-round alone, block 16
     (0, 32, 1, True, (1, 128, 384, 256)),
@@ -101,7 +102,7 @@ def test_weight_deployment_granularity(case):
     the usual bars."""
     rule, bs, b_rows, bf16, (b, M, K, N) = case
     r = check_case("tstar", "student_t3", b, M, K, N, 1, bs, rule, seed=3, cfg=9,
-                   b_rows=b_rows, b_bf16=bf16, ns=False)
+                   b_rows=b_rows, b_bf16=bf16, ns=False, flags=FMM_FLAG_LARGE_TILE)
     print(case, r, flush=True)
 
 
@@ -198,20 +199,40 @@ def test_tile_aligned_fast_path(case):
 
 
 @pytest.mark.parametrize("case", [
-    ("tstar", 1, 512, 128, 512, 32, 1),        # one 256 x 256 tile, one 64-byte k-step
-    ("tstar", 1, 1024, 256, 512, 32, 1),       # 2 x 1 tiles, two k-steps
-    ("strassen", 2, 512, 384, 1024, 32, 2),    # batch of two, 1 x 2 tiles, three k-steps, OCP
-    ("cubic8", 1, 1024, 640, 1024, 32, 1),     # eight terms, 2 x 2 tiles, five k-steps
-    ("winograd", 1, 512, 1024, 512, 128, 1),   # block 128, eight k-steps
-    ("tstar", 1, 512, 512, 1536, 128, 2),      # block 128, OCP, 1 x 3 tiles
+    ("tstar", 1, 512, 128, 512, 1, 32, 1),        # one 256 x 256 tile, one 64-byte k-step
+    ("tstar", 1, 1024, 256, 512, 1, 32, 1),       # 2 x 1 tiles, two k-steps
+    ("strassen", 2, 512, 384, 1024, 1, 32, 2),    # batch of two, 1 x 2 tiles, three k-steps, OCP
+    ("cubic8", 1, 1024, 640, 1024, 1, 32, 1),     # eight terms, 2 x 2 tiles, five k-steps
+    ("winograd", 1, 512, 1024, 512, 1, 128, 1),   # block 128, eight k-steps
+    ("tstar", 1, 512, 512, 1536, 1, 128, 2),      # block 128, OCP, 1 x 3 tiles
+    ("tstar", 1, 1024, 256, 1024, 2, 32, 1),      # depth 2: 49 terms, 16-block combine
+    ("strassen", 2, 1024, 768, 2048, 2, 32, 2),   # depth 2, batch of two, 1 x 4 tiles, three k-steps
+    ("cubic8", 1, 1024, 1024, 1024, 2, 128, 1),   # depth 2, 64 terms, block 128
 ])
 def test_large_tile_split_path(case):
-    """Shapes the large-tile path takes (depth 1, E8M0 scales, m' and n'
-    multiples of 256, k' a multiple of 64, or of 128 at block 128): every
-    prologue and tail branch of its transfer ring (one, two, three, five and
-    eight k-steps), several tiles along both edges, batches, eight terms."""
-    name, b, M, K, N, bs, rule = case
-    r = check_case(name, "gaussian", b, M, K, N, 1, bs, rule, seed=14, cfg=10)
+    """Shapes the large-tile path takes (depth 1 or 2, E8M0 scales, m' and
+    n' multiples of 256, k' a multiple of 64, or of 128 at block 128; forced
+    below k' = 2048): every prologue and tail branch of its transfer ring (one,
+    two, three, five and eight k-steps), several tiles along both edges,
+    batches, eight terms, and the one-pass combine of all R^2 terms."""
+    name, b, M, K, N, depth, bs, rule = case
+    r = check_case(name, "gaussian", b, M, K, N, depth, bs, rule, seed=14, cfg=10,
+                   flags=FMM_FLAG_LARGE_TILE, layout=FMM_LAYOUT_TILE256x64)
+    print(case, r, flush=True)
+
+
+@pytest.mark.parametrize("case", [
+    ("tstar", 1, 512, 1024, 512, 1, FMM_LAYOUT_TILE128x128),    # k' = 512: fused 128 x 128 path
+    ("tstar", 1, 512, 2048, 512, 1, FMM_LAYOUT_TILE256x64),     # k' = 1024: large tiles
+    ("tstar", 1, 1024, 2048, 1024, 2, FMM_LAYOUT_TILE128x128),  # depth 2, k' = 512
+    ("tstar", 1, 1024, 4096, 1024, 2, FMM_LAYOUT_TILE256x64),   # depth 2, k' = 1024
+])
+def test_default_path_choice(case):
+    """Without FMM_FLAG_LARGE_TILE the large-tile path is taken from
+    k' = 1024 on; both choices meet the parity bars."""
+    name, b, M, K, N, depth, layout = case
+    r = check_case(name, "gaussian", b, M, K, N, depth, 32, 1, seed=17, cfg=10, layout=layout,
+                   ns=False)
     print(case, r, flush=True)
 
 
@@ -222,7 +243,7 @@ def test_large_tile_split_path_unaligned_output():
     from paper_2609_26077_amd.runner import FMM
     A, B = gen.operands("gaussian", 1, 512, 256, 512, seed=15)
     dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
-    f = FMM("tstar", 1, 512, 256, 512, 1, 32, "pow2_ceil")
+    f = FMM("tstar", 1, 512, 256, 512, 1, 32, "pow2_ceil", flags=FMM_FLAG_LARGE_TILE)
     C1 = f.matmul(dA, dB).clone()
     buf = torch.full((1 + 512 * 512,), float("nan"), device="cuda:0")
     C2 = buf[1:].view(1, 512, 512)
@@ -231,16 +252,17 @@ def test_large_tile_split_path_unaligned_output():
     assert torch.equal(C1, C2)
 
 
-@pytest.mark.parametrize("shape,depth", [((1, 512, 256, 512), 1),    # large-tile plan
-                                         ((1, 256, 256, 384), 1),    # combine fused into the GEMM
-                                         ((2, 256, 512, 256), 2)])   # outer combine
-def test_products_then_combine_equals_multiply(shape, depth):
+@pytest.mark.parametrize("shape,depth,flags", [((1, 512, 256, 512), 1, 8),    # large-tile plan
+                                               ((1, 1024, 512, 1024), 2, 8),  # large tiles, depth 2
+                                               ((1, 256, 256, 384), 1, 0),    # combine fused into the GEMM
+                                               ((2, 256, 512, 256), 2, 0)])   # outer combine
+def test_products_then_combine_equals_multiply(shape, depth, flags):
     import torch
     from paper_2609_26077_amd.runner import FMM
     b, M, K, N = shape
     A, B = gen.operands("gaussian", b, M, K, N, seed=16)
     dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
-    f = FMM("tstar", b, M, K, N, depth, 32, "pow2_ceil")
+    f = FMM("tstar", b, M, K, N, depth, 32, "pow2_ceil", flags=flags)
     f.encode(dA, dB)
     C1 = f.multiply().clone()
     C2 = torch.full_like(C1, float("nan"))

@@ -130,7 +130,7 @@ def test_create_checks_exactness(fm):
     (dict(batch=1, M=256, K=256, N=256, depth=3, block=128), -2),   # k' = 32 not / 128
     (dict(batch=1, M=256, K=96, N=256, block=32), -2),        # k' = 48 not / 32
     (dict(batch=70000, M=2, K=64, N=2), -3),                  # batch beyond the grid
-    (dict(batch=1, M=256, K=256, N=256, flags=8), -1),        # unknown flag bit
+    (dict(batch=1, M=256, K=256, N=256, flags=16), -1),       # unknown flag bit
     (dict(batch=1, M=256, K=256, N=256, depth=2, flags=2), -3),   # 128-row B blocks: depth 1 only
     (dict(batch=1, M=256, K=256, N=256, depth=2, flags=4), -3),   # bfloat16 pre-round: depth 1 only
 ])
