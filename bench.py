@@ -303,7 +303,7 @@ def main():
                    "M": M, "K": K, "N": N, "depth": args.depth, "terms": T, "block": args.block,
                    "rule": args.rule, "realization": args.realization, "family": args.family,
                    "exact_dot": bool(args.exact_dot),
-                   "subproduct_path": "256x256 tiles + separate W-combine" if split
+                   "subproduct_path": "256x128 tiles + separate W-combine" if split
                    else "128x128 tiles with the W-combine fused"},
         "rel_rms_error_vs_fp64": float(np.sqrt(rel_mse)),
         "rel_mse_vs_fp64": rel_mse,

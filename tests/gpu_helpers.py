@@ -38,11 +38,12 @@ MSE_REL_TOL = 0.01
 
 def oracle_realization(spec):
     """spec: a builtin name, (name, (X, Y, Z)) for a transformed one, or
-    ("coeffs", (U, V, w)) for explicit binary64 coefficient arrays."""
+    ("coeffs", (U, V, w)) for explicit binary64 coefficient arrays
+    (("unchecked", (U, V, w)): the same, not required to be a realization)."""
     if isinstance(spec, str):
         return R.builtin_f64(spec)
     name, g = spec
-    if name == "coeffs":
+    if name in ("coeffs", "unchecked"):
         return tuple(np.asarray(M, dtype=np.float64) for M in g)
     return R.act_f64(R.builtin_f64(name), g)
 
@@ -52,9 +53,9 @@ def gpu_realization(spec):
     if isinstance(spec, str):
         return fm.fmm_realization_builtin(spec)
     name, g = spec
-    if name == "coeffs":
+    if name in ("coeffs", "unchecked"):
         U, V, W = g
-        return fm.fmm_realization_create(U, V, W, tol=1e-9)
+        return fm.fmm_realization_create(U, V, W, tol=1e-9 if name == "coeffs" else float("inf"))
     X, Y, Z = g
     return fm.fmm_realization_transform(fm.fmm_realization_builtin(name), X, Y, Z)
 

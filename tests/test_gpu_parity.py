@@ -11,6 +11,7 @@ import pytest
 
 import fmm_inputs as gen
 from paper_2609_26077_amd import FMM_FLAG_LARGE_TILE, FMM_LAYOUT_TILE128x128, FMM_LAYOUT_TILE256x64
+from oracle import realizations as R
 from tests.gpu_helpers import check_case
 
 pytestmark = pytest.mark.gpu
@@ -104,6 +105,20 @@ def test_weight_deployment_granularity(case):
     r = check_case("tstar", "student_t3", b, M, K, N, 1, bs, rule, seed=3, cfg=9,
                    b_rows=b_rows, b_bf16=bf16, ns=False, flags=FMM_FLAG_LARGE_TILE)
     print(case, r, flush=True)
+
+
+@pytest.mark.parametrize("depth,flags", [(1, 0), (1, 8), (2, 0), (2, 8), (3, 0)])
+def test_term_without_coefficients(depth, flags):
+    """A term whose U row is all zero combines to +0 on the A side: zero
+    codes and the clamp scale (every encoder path), and the products and
+    combine carry on as for any other term."""
+    U, V, W = (np.array(M, dtype=np.float64) for M in R.builtin_f64("strassen"))
+    U[4, :] = 0.0
+    n = 2 ** depth
+    M = K = N = 256 * n if flags else 32 * n
+    r = check_case(("unchecked", (U, V, W)), "gaussian", 1, M, K, N, depth, 32, 1, seed=21, cfg=7,
+                   flags=flags, ns=False)
+    print(depth, flags, r, flush=True)
 
 
 def test_rowscaled_family():
