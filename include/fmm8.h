@@ -132,12 +132,14 @@ enum {
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
    * at chunk c ^ ((t >> 2) & 3) of that row.
    * scales [batch][terms][kblocks][rows]: for each block of the contracted
-   * axis, one byte per row, the rows of every 256-row tile permuted so that
-   * tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at byte 4 (32 h + j) + i.
+   * axis, one scale per row.  E8M0 bytes have the rows of every 256-row tile
+   * permuted so that tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at
+   * byte 4 (32 h + j) + i; fp32 scales (FMM_RULE_FP32_AMAX) are in row order.
    * Used by plans whose sub-products run on 256-row tiles (depth 1 or 2,
-   * E8M0 scales at block 32 or 128, M / 2^l and N / 2^l multiples of 256,
-   * K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE; the B side is read as 128-row
-   * halves of these tiles). */
+   * block 32 or 128, E8M0 scales on the fp8 matrix cores or fp32 scales on
+   * the exact-dot kernel, M / 2^l and N / 2^l multiples of 256, K / 2^l >=
+   * 1024 or FMM_FLAG_LARGE_TILE; the B side is read as 128-row halves of
+   * these tiles). */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits

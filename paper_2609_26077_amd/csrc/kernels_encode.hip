@@ -152,9 +152,10 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 // term's plane (the same for every term, so computed once per lane):
 //   codes : row-major p k' + l, or (large-tile plans) the 256-row x 64-byte
 //           tile image, chunk c of tile row t at c ^ ((t >> 2) & 3)
-//   scales: row-major p kblocks + kb, or (large-tile plans) K-block-major with
-//           rows permuted inside each 256-row tile: row 128 wm + 32 i + r at
-//           byte 4 (32 wm + r) + i of the tile
+//   scales: row-major p kblocks + kb, or (large-tile plans) K-block-major,
+//           E8M0 bytes with rows permuted inside each 256-row tile (row
+//           128 wm + 32 i + r at byte 4 (32 wm + r) + i of the tile), fp32
+//           values in row order
 //   128 x 128 tiles: codes as the 128-row x 128-byte tile image (chunk c of
 //           tile row t at c ^ (t & 7) ^ ((t >> 3) & 1)); scales 4 bytes per
 //           tile row and 128-byte step (blocks 0, 2, 1, 3 at block 32; the
@@ -173,7 +174,7 @@ __device__ __forceinline__ Out out_of(const Problem &pb, int64_t rows, int64_t p
   if (pb.layout == FMM_LAYOUT_TILE256x64) {
     const int64_t t = p & 255, c = (l >> 4) & 3;
     o.code = ((((p >> 8) * (kp >> 6) + (l >> 6)) << 14) + t * 64 + 16 * (c ^ ((t >> 2) & 3)) + (l & 15));
-    o.scale = kb * rows + ((p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3)));
+    o.scale = kb * rows + (pb.scale_bytes == 4 ? p : ((p & ~int64_t(255)) | ((((p >> 7) & 1) * 32 + (p & 31)) * 4 + ((p >> 5) & 3))));
   } else if (pb.layout == FMM_LAYOUT_TILE128x128) {
     const int64_t t = p & 127, c = (l >> 4) & 7, tile = (p >> 7) * (kp >> 7) + (l >> 7);
     o.code = (tile << 14) + t * 128 + 16 * (c ^ (t & 7) ^ ((t >> 3) & 1)) + (l & 15);

@@ -28,6 +28,8 @@
 // bytes 128 h .. 128 h + 127 of each K block's scales.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 #include "lds_dma.h"
@@ -222,6 +224,225 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
       }
 }
 
+// ---------------------------------------------------------------------------
+// Exact-dot large-tile sub-products (fp32 amax/448 scales, blocks 32 and 128).
+//
+// The scales are arbitrary fp32 numbers, which the scaled fp8 MFMA cannot
+// apply, and the fp8 matrix cores' dot product is narrower than fp32; so each
+// block's partial sum of code products is formed exactly on the bf16 matrix
+// cores (e4m3 -> bf16 is exact, products of two codes are exact in fp32) and
+// promoted into the fp32 accumulator as acc += (sA sB) partial.  Per block
+// and output that is two VALU operations against 32 (block 32) or 128 (block
+// 128) multiply-adds on the matrix cores, so at block 32 the promotes, not
+// the matrix cores, bound the kernel.
+//
+// One workgroup of eight waves per (batch, term, 256 x 128 tile), each wave a
+// 64 x 64 quarter-column (2 x 2 tiles of v_mfma_f32_32x32x16_bf16), one
+// workgroup per CU.  The codes arrive through a 64-byte-step LDS ring like the
+// fp8 kernel's (four slots here, two steps ahead); each slot also holds the
+// step's fp32 scales: 2 K blocks x 256 A rows and 2 x 128 B rows (block 128:
+// the step's one block, twice).  Scales of these plans are stored K-block-major
+// in row order: [batch][term][kblocks][rows] fp32.
+//
+// A fragment of 64 bytes (frag64) gives lane (r, h) bytes 16h..16h+15 and
+// 32+16h..32+16h+15 of row r.  The bf16 instruction takes 8 consecutive
+// contracted positions per lane half, so the four instructions of a step take
+// bytes {8t + 16h + 0..7} (t = 0, 1) of the first 32 and the same of the second
+// 32: each instruction's 16 positions lie in one block of 32, the same
+// positions on both operands, so every partial sum is over exactly one block.
+namespace ex {
+constexpr int kThreadsX = 512;
+constexpr int kScaleAX = 2 * TM * 4;             // 2 blocks x 256 rows of fp32
+constexpr int kScaleBX = 2 * TN * 4;             // 2 blocks x 128 rows of fp32
+constexpr int kSlotX = kCodeA + kCodeB + kScaleAX + kScaleBX;   // 27648 B
+constexpr int kSlotsX = 4;                       // two in flight, the current one, the previous one
+static_assert(kSlotsX * kSlotX <= 160 * 1024, "one workgroup per CU");
+}  // namespace ex
+
+// eight e4m3 codes (little-endian in two words) -> eight bf16, exactly
+typedef __bf16 v8bfx __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bfx __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ v8bfx codes8_to_bf16(uint32_t lo, uint32_t hi) {
+  const v2bfx a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, 1.0f, false);
+  const v2bfx b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, 1.0f, true);
+  const v2bfx c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, 1.0f, false);
+  const v2bfx d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, 1.0f, true);
+  v8bfx r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
+  r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
+  return r;
+}
+
+template <int BS>
+__global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(SplitArgs g) {
+  __shared__ uint4 lds_raw[ex::kSlotsX * ex::kSlotX / 16];
+  const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
+  const uint32_t lds_base = dma::lds_addr(lds_raw);
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = wave >> 1, wn = wave & 1;       // A rows 64 wm.., B rows 64 wn.. of the tile
+  const int r32 = lane & 31, h = lane >> 5;
+  const int64_t nitems = (int64_t)gridDim.x;
+  int64_t bt, r;
+  int tm, tn;
+  work_of(blockIdx.x, nitems, g.T, g.tiles_m, g.tiles_n, bt, r, tm, tn);
+  const int64_t pm0 = (int64_t)tm * TM, pn0 = (int64_t)tn * TN;
+  const int hb = tn & 1;
+  const int nk = (int)(g.kp / SK);
+  const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kImage;
+  const uint8_t *xb = g.xb + ((bt * g.T + r) * (g.tiles_n / 2) + (tn >> 1)) * (int64_t)nk * kImage + hb * kCodeB;
+  const uint32_t code_off = 16u * (uint32_t)lane;
+  // the three 1 KB code regions wave w moves each step: 3 w .. 3 w + 2
+  const uint8_t *csrc[3];
+  uint32_t cdst[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const int region = wave * 3 + j;
+    csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
+    cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
+  }
+  // one scale transfer per wave and step (1 KB):
+  //   wave 0 / 1: A scales (256 rows) of K block 2 step + wave (block 32) or step / 2
+  //   waves 2..7: B scales (128 rows) of K blocks 2 step + h (block 32) or step / 2
+  //               into half h; waves 3..7 repeat wave 2's transfer
+  const bool s_is_a = wave < 2;
+  const uint8_t *sbase = s_is_a ? g.sat + ((bt * g.T + r) * g.kblocks * g.mp + pm0) * 4
+                                : g.sbt + ((bt * g.T + r) * g.kblocks * g.np + pn0) * 4;
+  const int64_t splane = (s_is_a ? g.mp : g.np) * 4;   // bytes per K block
+  const uint32_t s_off = s_is_a ? 16u * (uint32_t)lane : 16u * (uint32_t)r32;
+  const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_a ? (BS == 32 ? wave * TM * 4 : 0) : ex::kScaleAX));
+
+  auto issue = [&](int step) {
+    const uint32_t m0 = lds_base + (uint32_t)(step % ex::kSlotsX) * ex::kSlotX;
+    const int64_t src = (int64_t)step * kImage;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
+    int64_t kb;
+    if (s_is_a) kb = BS == 32 ? 2 * (int64_t)step + wave : step / 2;
+    else kb = BS == 32 ? 2 * (int64_t)step : step / 2;
+    // B lanes of half h read block kb + h (block 32) into bytes 512 h ..
+    const uint32_t hoff = (!s_is_a && BS == 32) ? (uint32_t)(h * splane) : 0u;
+    dma::copy16(s_off + hoff, sbase + kb * splane, m0 + sdst);
+  };
+
+  v16f acc[2][2], part[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = (v16f){};
+      part[i][j] = (v16f){};
+    }
+
+  // A block's promote waits until the next block's first instructions, so
+  // that its VALU work overlaps their matrix-core work.  Its scales are still
+  // in LDS then: the ring has four slots and refills the one of step s - 2
+  // during step s, so the previous step's slot stays intact.
+  auto promote = [&](const uint8_t *slot, int hs) {
+    const float *lsa = reinterpret_cast<const float *>(slot + kCodeA + kCodeB) + hs * TM;
+    const float *lsb = reinterpret_cast<const float *>(slot + kCodeA + kCodeB + ex::kScaleAX) + hs * TN;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const float sbv = lsb[wn * 64 + 32 * j + r32];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // rows 64 wm + 32 i + 8 q + 4 h + u, u = 0..3: registers 4 q + u
+          const float4 sa4 = *reinterpret_cast<const float4 *>(lsa + wm * 64 + 32 * i + 8 * q + 4 * h);
+          const float sav[4] = {sa4.x, sa4.y, sa4.z, sa4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            acc[i][j][4 * q + u] = __fmaf_rn(sav[u] * sbv, part[i][j][4 * q + u], acc[i][j][4 * q + u]);
+        }
+      }
+    }
+  };
+
+  // the four instructions per tile of one K-step; the first instruction of a
+  // block starts from zero (an inline constant: no register clears) and is
+  // preceded by the previous block's promote.  FRESH: the step opens a block
+  // of 128.  prev: the previous step's slot.
+  auto mfma_step = [&](const uint8_t *la, const uint8_t *prev, auto FRESH) {
+    constexpr bool fresh = decltype(FRESH)::value;
+    const uint8_t *lb = la + kCodeA;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      // this half's 16 bytes of each fragment row (bytes 32 half + 16 h ..)
+      uint4 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        fa[i] = *reinterpret_cast<const uint4 *>(la + swz64(wm * 64 + 32 * i + r32, 2 * half + h));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        fb[j] = *reinterpret_cast<const uint4 *>(lb + swz64(wn * 64 + 32 * j + r32, 2 * half + h));
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const bool opens = BS == 32 ? tt == 0 : (fresh && half == 0 && tt == 0);
+        v8bfx a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = tt == 0 ? codes8_to_bf16(fa[i].x, fa[i].y) : codes8_to_bf16(fa[i].z, fa[i].w);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = tt == 0 ? codes8_to_bf16(fb[j].x, fb[j].y) : codes8_to_bf16(fb[j].z, fb[j].w);
+        if (opens) {
+          // block 32: the previous block is the other half (this step's, or
+          // the previous step's second); block 128: the previous step's
+          if (BS == 32) promote(half == 0 ? prev : la, half == 0 ? 1 : 0);
+          else promote(prev, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], opens ? (v16f){} : part[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  // Step s: wait for this wave's own transfers of step s (four a step; those
+  // of step s + 1 may stay in flight), barrier, start step s + 2 into the
+  // slot of step s - 2, multiply step s.
+  auto slot_of = [&](int step) { return lds + (step & (ex::kSlotsX - 1)) * ex::kSlotX; };
+  auto begin_step = [&](int step) -> const uint8_t * {
+    if (step + 1 < nk) dma::wait_vmcnt<4>(); else dma::wait_vmcnt<0>();
+    __syncthreads();
+    if (step + 2 < nk) issue(step + 2);
+    return slot_of(step);
+  };
+  // the first block's "previous" promote reads the scales of the last slot,
+  // which step 3 fills only after the first two barriers: zero them (and
+  // part is zero), so that it adds 0 x 0
+  {
+    float *z = reinterpret_cast<float *>(lds_raw) + ((ex::kSlotsX - 1) * ex::kSlotX + kCodeA + kCodeB) / 4;
+    for (int e = t; e < (ex::kScaleAX + ex::kScaleBX) / 4; e += ex::kThreadsX) z[e] = 0.0f;
+  }
+  issue(0);
+  if (nk > 1) issue(1);
+  if (BS == 32) {
+    for (int step = 0; step < nk; ++step) mfma_step(begin_step(step), slot_of(step + ex::kSlotsX - 1), std::false_type{});
+    promote(slot_of(nk - 1), 1);
+  } else {
+    // a block of 128 is two steps (k' is a multiple of 128)
+    for (int step = 0; step < nk; step += 2) {
+      mfma_step(begin_step(step), slot_of(step + ex::kSlotsX - 1), std::true_type{});
+      mfma_step(begin_step(step + 1), slot_of(step), std::false_type{});
+    }
+    promote(slot_of(nk - 1), 0);
+  }
+
+  // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32.
+  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 64) * g.np + pn0 + wn * 64 + r32;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
+      }
+}
+
 // C block (i, k) of batch element bt, rows i m' + p, columns k n' + 4 q4 .. + 3:
 //   sum over r of w[r][2k + i] P_r[p][4 q4 ..], ascending r, fma per nonzero weight.
 template <bool VEC>
@@ -343,6 +564,13 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
   g.tiles_m = (int)(pb.mp / TM);
   g.tiles_n = (int)(pb.np / TN);
   const int64_t items = pb.batch * pb.T * g.tiles_m * g.tiles_n;
+  if (pb.scale_bytes == 4) {
+    if (pb.block == 32)
+      hipLaunchKernelGGL(gemm_exact256x128_kernel<32>, dim3((unsigned)items), dim3(ex::kThreadsX), 0, st, g);
+    else
+      hipLaunchKernelGGL(gemm_exact256x128_kernel<128>, dim3((unsigned)items), dim3(ex::kThreadsX), 0, st, g);
+    return hipGetLastError();
+  }
   if (pb.block == 32)
     hipLaunchKernelGGL(gemm_tile256x128_kernel<32>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
   else

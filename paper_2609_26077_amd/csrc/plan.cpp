@@ -105,7 +105,9 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   // 8 / k' bytes per flop against the fused path's none: taken by default
   // where that round trip costs less than the fused path's smaller tiles,
   // k' >= 1024 (measured: the large tiles win at 1024, lose at 256).
-  const bool split_shape = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128) &&
+  // (E8M0 scales on the fp8 matrix cores, or fp32 scales on the exact-dot kernel)
+  const bool split_shape = ((!pb.exact_dot && pb.scale_bytes == 1) || pb.scale_bytes == 4) &&
+             (q.block == 32 || q.block == 128) &&
              q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
              pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
              q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);

@@ -91,7 +91,11 @@ class FMM:
             raw = self.ws[c0:c0 + nc]
             if v.code_layout == FMM_LAYOUT_TILE256x64:
                 codes = _untile256x64(raw, v.batch, v.terms, v.rows, v.kdim)
-                scales = _unpermute_scales256(self.ws[s0:s0 + ns], v.batch, v.terms, v.rows, v.kblocks)
+                if v.scale_bytes == 4:
+                    scales = (self.ws[s0:s0 + 4 * ns].view(torch.float32)
+                              .view(v.batch, v.terms, v.kblocks, v.rows).permute(0, 1, 3, 2).contiguous())
+                else:
+                    scales = _unpermute_scales256(self.ws[s0:s0 + ns], v.batch, v.terms, v.rows, v.kblocks)
             elif v.code_layout == FMM_LAYOUT_TILE128x128:
                 codes = _untile128x128(raw, v.batch, v.terms, v.rows, v.kdim)
                 nrec = v.batch * v.terms * v.rows * (v.kdim // 128) * 4

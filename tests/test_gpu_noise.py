@@ -45,6 +45,7 @@ def oracle_noise(A, B, name, depth, bs, rule, b_rows=1, b_bf16=False):
     ("tstar", "uniform", 1, 256, 512, 256, 2, 32, 2, 0),           # depth 2
     ("winograd", "gaussian", 1, 512, 256, 512, 1, 32, 1, 8),       # large-tile layout (forced)
     ("tstar", "gaussian", 1, 1024, 512, 1024, 2, 32, 1, 8),        # large-tile layout at depth 2
+    ("strassen", "gaussian", 1, 512, 256, 512, 1, 32, 0, 8),       # large-tile layout, fp32 scales
     ("tstar", "rowscaled", 1, 256, 512, 256, 1, 128, 1, 0),        # 128 x 128 tile layout, block 128
     ("tstar", "student_t3", 1, 384, 512, 320, 1, 128, 0, 2 | 4),   # deployment granularity
 ])

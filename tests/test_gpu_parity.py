@@ -95,6 +95,8 @@ def test_rebased_realization():
     (2, 128, 128, False, (1, 130, 256, 258)),     # ragged everything
     (1, 16, 1, True, (1, 192, 256, 128)),         # bfloat16 pre-round alone, block 16
     (0, 32, 1, True, (1, 128, 384, 256)),
+    (0, 128, 128, True, (1, 512, 512, 512)),      # the paper's real-kernel setting on the large tiles
+    (0, 32, 1, False, (2, 512, 256, 512)),        # fp32 scales on the large tiles, block 32
 ])
 def test_weight_deployment_granularity(case):
     """Weight-side deployment granularity (Appendix E): 128-row B scale
@@ -223,13 +225,20 @@ def test_tile_aligned_fast_path(case):
     ("tstar", 1, 1024, 256, 1024, 2, 32, 1),      # depth 2: 49 terms, 16-block combine
     ("strassen", 2, 1024, 768, 2048, 2, 32, 2),   # depth 2, batch of two, 1 x 4 tiles, three k-steps
     ("cubic8", 1, 1024, 1024, 1024, 2, 128, 1),   # depth 2, 64 terms, block 128
+    # fp32 amax/448 scales: the exact-dot large-tile kernel
+    ("tstar", 1, 512, 128, 512, 1, 32, 0),        # one k-step
+    ("strassen", 2, 512, 384, 1024, 1, 32, 0),    # batch of two, 1 x 2 tiles, three k-steps
+    ("cubic8", 1, 1024, 640, 1024, 1, 32, 0),     # eight terms, 2 x 2 tiles, five k-steps
+    ("winograd", 1, 512, 1024, 512, 1, 128, 0),   # block 128: one promote every two k-steps
+    ("tstar", 1, 1024, 512, 1024, 2, 32, 0),      # depth 2
 ])
 def test_large_tile_split_path(case):
-    """Shapes the large-tile path takes (depth 1 or 2, E8M0 scales, m' and
-    n' multiples of 256, k' a multiple of 64, or of 128 at block 128; forced
-    below k' = 2048): every prologue and tail branch of its transfer ring (one,
-    two, three, five and eight k-steps), several tiles along both edges,
-    batches, eight terms, and the one-pass combine of all R^2 terms."""
+    """Shapes the large-tile path takes (depth 1 or 2, E8M0 scales on the fp8
+    kernel or fp32 scales on the exact-dot kernel, m' and n' multiples of 256,
+    k' a multiple of 64, or of 128 at block 128; forced below k' = 1024):
+    every prologue and tail branch of the transfer rings (one, two, three,
+    five and eight k-steps), several tiles along both edges, batches, eight
+    terms, and the one-pass combine of all R^2 terms."""
     name, b, M, K, N, depth, bs, rule = case
     r = check_case(name, "gaussian", b, M, K, N, depth, bs, rule, seed=14, cfg=10,
                    flags=FMM_FLAG_LARGE_TILE, layout=FMM_LAYOUT_TILE256x64)
