@@ -25,6 +25,19 @@ def test_config1_shape_all_realizations(name, exact):
     print(name, r, flush=True)
 
 
+def test_config1_hundred_trials():
+    """The 256^3 configuration at its full trial count: 100 seeded N(0,1)
+    products in one batch, cubic and Strassen 1969, block 32, power-of-two
+    scales; every trial bit-exact in codes and scales and within the C bar,
+    the relative MSE over all trials within 1% of the oracle's, and Strassen's
+    above cubic's by about the model's Phi ratio (32 / 8)."""
+    r = {name: check_case(name, "gaussian", 100, 256, 256, 256, 1, 32, 1, seed=0, cfg=1)
+         for name in ("cubic8", "strassen")}
+    ratio = r["strassen"]["rel_mse_gpu"] / r["cubic8"]["rel_mse_gpu"]
+    print(r, "ratio", ratio, flush=True)
+    assert 3.6 < ratio < 4.4
+
+
 @pytest.mark.parametrize("rule", [0, 1, 2])
 @pytest.mark.parametrize("bs", [16, 32, 128])
 def test_rules_and_blocks(rule, bs):
@@ -163,6 +176,27 @@ def test_degenerate_blocks():
     B0 = torch.zeros((1, 0, 64), device="cuda:0")
     C = f.matmul(A0, B0)
     assert torch.count_nonzero(C).item() == 0
+
+
+@pytest.mark.parametrize("shape,depth,flags", [((0, 512, 512, 512), 1, 8),   # no products
+                                               ((1, 0, 256, 512), 1, 0),     # no rows of A
+                                               ((1, 512, 256, 0), 1, 8),     # no columns of B
+                                               ((2, 256, 0, 256), 2, 0),     # nothing to contract
+                                               ((1, 0, 0, 0), 3, 0),
+                                               ((3, 64, 0, 128), 3, 0)])
+def test_empty_shapes(shape, depth, flags):
+    """Empty operands: every call succeeds, C has its shape and, with nothing
+    to contract, is zero."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    b, M, K, N = shape
+    f = FMM("tstar", b, M, K, N, depth, 32, "pow2_ceil", flags=flags)
+    A = torch.zeros((b, M, K), device="cuda:0")
+    B = torch.zeros((b, K, N), device="cuda:0")
+    C = f.matmul(A, B)
+    assert tuple(C.shape) == (b, M, N)
+    if C.numel():
+        assert torch.count_nonzero(C).item() == 0
 
 
 def test_batch_of_small_products():
