@@ -90,7 +90,8 @@ enum {
    * with this flag the codes are converted exactly to bf16 and multiplied on
    * the bf16 matrix cores (23 retained bits), each block's partial sum is
    * scaled and accumulated in fp32.  Half the peak rate of the default path.
-   * FP32_AMAX scales and block 16 always take this path. */
+   * FP32_AMAX scales and block 16 always take this path; tile-aligned plans
+   * (FMM_LAYOUT_TILE256x64) on it run on 256 x 128 tiles whatever K. */
   FMM_FLAG_EXACT_DOT = 1,
   /* Weight-side deployment granularity (Appendix E, weight-scale
    * granularity; the real kernel's 128 x 128 weight blocks): one B-side scale
@@ -105,10 +106,12 @@ enum {
    * encoded weights).  Depth 1 only. */
   FMM_FLAG_B_BF16 = 4,
   /* Take the large-tile sub-product path (FMM_LAYOUT_TILE256x64) whenever
-   * the shape allows it.  Without the flag that path is taken only where
-   * K / 2^l >= 1024: it writes every fp32 P_r to the workspace and reads it
-   * back, which costs more than it saves on short contractions.  No effect on
-   * the result's definition; shapes the path cannot take ignore the flag. */
+   * the shape allows it.  Without the flag, plans on the fp8 matrix cores
+   * take that path only where K / 2^l >= 1024: it writes every fp32 P_r to
+   * the workspace and reads it back, which costs more than it saves on short
+   * contractions (exact-dot plans take it whenever the shape allows).  No
+   * effect on the result's definition; shapes the path cannot take ignore
+   * the flag. */
   FMM_FLAG_LARGE_TILE = 8
 };
 
@@ -135,11 +138,12 @@ enum {
    * axis, one scale per row.  E8M0 bytes have the rows of every 256-row tile
    * permuted so that tile row 128 h + 32 i + j (h < 2, i < 4, j < 32) sits at
    * byte 4 (32 h + j) + i; fp32 scales (FMM_RULE_FP32_AMAX) are in row order.
-   * Used by plans whose sub-products run on 256-row tiles (depth 1 or 2,
-   * block 32 or 128, E8M0 scales on the fp8 matrix cores or fp32 scales on
-   * the exact-dot kernel, M / 2^l and N / 2^l multiples of 256, K / 2^l >=
-   * 1024 or FMM_FLAG_LARGE_TILE; the B side is read as 128-row halves of
-   * these tiles). */
+   * Used by plans whose sub-products run on 256-row tiles: depth 1 or 2,
+   * M / 2^l and N / 2^l multiples of 256, K / 2^l a multiple of 64 (of 128
+   * at block 128), and either the exact-dot path (fp32 scales, block 16, or
+   * FMM_FLAG_EXACT_DOT) or E8M0 scales at block 32 or 128 on the fp8 matrix
+   * cores with K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE.  The B side is read as
+   * 128-row halves of these tiles. */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits

@@ -61,6 +61,10 @@ struct Problem {
   int b_bf16;              // round encoded B combinations to bfloat16 first (FMM_FLAG_B_BF16)
 };
 
+// Large-tile plans whose sub-products take the exact-dot kernel: fp32
+// scales, block 16, or the exact-dot flag.
+inline bool exact_split(const Problem &pb) { return pb.exact_dot || pb.scale_bytes == 4 || pb.block == 16; }
+
 // Bytes of one (batch, term) plane of scales for `rows` rows.
 inline int64_t scale_plane_bytes(const Problem &pb, int64_t rows) {
   if (pb.layout == FMM_LAYOUT_TILE128x128) return rows * (pb.kp / 128) * 4;

@@ -225,38 +225,46 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 }
 
 // ---------------------------------------------------------------------------
-// Exact-dot large-tile sub-products (fp32 amax/448 scales, blocks 32 and 128).
+// Exact-dot large-tile sub-products (fp32 amax/448 scales, block 16, or the
+// exact-dot flag; blocks 16, 32 and 128; fp32 or E8M0 scales).
 //
-// The scales are arbitrary fp32 numbers, which the scaled fp8 MFMA cannot
-// apply, and the fp8 matrix cores' dot product is narrower than fp32; so each
-// block's partial sum of code products is formed exactly on the bf16 matrix
-// cores (e4m3 -> bf16 is exact, products of two codes are exact in fp32) and
-// promoted into the fp32 accumulator as acc += (sA sB) partial.  Per block
-// and output that is two VALU operations against 32 (block 32) or 128 (block
-// 128) multiply-adds on the matrix cores, so at block 32 the promotes, not
-// the matrix cores, bound the kernel.
+// fp32 scales are arbitrary numbers, which the scaled fp8 MFMA cannot apply,
+// blocks of 16 are finer than its scale granularity, and the fp8 matrix
+// cores' dot product is narrower than fp32; so each block's partial sum of
+// code products is formed exactly on the bf16 matrix cores (e4m3 -> bf16 is
+// exact, products of two codes are exact in fp32) and promoted into the fp32
+// accumulator as acc += (sA sB) partial.  Per block and output that is two
+// VALU operations against `block` multiply-adds on the matrix cores, so at
+// blocks 16 and 32 the promotes, not the matrix cores, bound the kernel.
 //
 // One workgroup of eight waves per (batch, term, 256 x 128 tile), each wave a
 // 64 x 64 quarter-column (2 x 2 tiles of v_mfma_f32_32x32x16_bf16), one
 // workgroup per CU.  The codes arrive through a 64-byte-step LDS ring like the
 // fp8 kernel's (four slots here, two steps ahead); each slot also holds the
-// step's fp32 scales: 2 K blocks x 256 A rows and 2 x 128 B rows (block 128:
-// the step's one block, twice).  Scales of these plans are stored K-block-major
-// in row order: [batch][term][kblocks][rows] fp32.
+// step's scales: NB = max(1, 64 / block) K blocks of the 256 A rows and
+// max(2, NB) of the 128 B rows (block 128: the step's one block, repeated).
+// Scales are stored as the layout defines them: fp32 in row order, E8M0 bytes
+// with the rows of each 256-row tile permuted.
 //
-// A fragment of 64 bytes (frag64) gives lane (r, h) bytes 16h..16h+15 and
-// 32+16h..32+16h+15 of row r.  The bf16 instruction takes 8 consecutive
-// contracted positions per lane half, so the four instructions of a step take
-// bytes {8t + 16h + 0..7} (t = 0, 1) of the first 32 and the same of the second
-// 32: each instruction's 16 positions lie in one block of 32, the same
+// Each instruction's 16 contracted positions lie in one block, the same
 // positions on both operands, so every partial sum is over exactly one block.
+// Blocks 32 and 128: a lane's 16-byte read of bytes 32 c + 16 h of its row
+// (c = 0, 1) feeds two instructions, bytes 32 c + 16 h + 8 t + 0..7 (t = 0, 1)
+// in the lane half h, i.e. positions {8 t + 0..7, 16 + 8 t + 0..7} of the
+// 32-byte group c.  Block 16: the instruction of block b takes bytes
+// 16 b + 8 h + 0..7 (an 8-byte read).
 namespace ex {
 constexpr int kThreadsX = 512;
-constexpr int kScaleAX = 2 * TM * 4;             // 2 blocks x 256 rows of fp32
-constexpr int kScaleBX = 2 * TN * 4;             // 2 blocks x 128 rows of fp32
-constexpr int kSlotX = kCodeA + kCodeB + kScaleAX + kScaleBX;   // 27648 B
 constexpr int kSlotsX = 4;                       // two in flight, the current one, the previous one
-static_assert(kSlotsX * kSlotX <= 160 * 1024, "one workgroup per CU");
+template <int BS, int SB>
+struct Geo {
+  static constexpr int NB = BS >= 64 ? 1 : 64 / BS;       // K blocks per step
+  static constexpr int NBB = NB < 2 ? 2 : NB;             // B scale blocks held per slot
+  static constexpr int kScaleA = NB * TM * SB;
+  static constexpr int kScaleB = NBB * TN * SB;
+  static constexpr int kSlot = kCodeA + kCodeB + kScaleA + kScaleB;
+  static_assert(kSlotsX * kSlot <= 160 * 1024, "one workgroup per CU");
+};
 }  // namespace ex
 
 // eight e4m3 codes (little-endian in two words) -> eight bf16, exactly
@@ -273,9 +281,14 @@ __device__ __forceinline__ v8bfx codes8_to_bf16(uint32_t lo, uint32_t hi) {
   return r;
 }
 
-template <int BS>
+// the value of a stored E8M0 byte (e + 127; e >= -126 for every scale the rules produce)
+__device__ __forceinline__ float e8m0_value(uint32_t byte) { return __uint_as_float(byte << 23); }
+
+template <int BS, int SB>
 __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(SplitArgs g) {
-  __shared__ uint4 lds_raw[ex::kSlotsX * ex::kSlotX / 16];
+  using G = ex::Geo<BS, SB>;
+  constexpr int NB = G::NB;
+  __shared__ uint4 lds_raw[ex::kSlotsX * G::kSlot / 16];
   const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
   const uint32_t lds_base = dma::lds_addr(lds_raw);
   const int t = threadIdx.x, lane = t & 63;
@@ -301,28 +314,33 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
     csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
     cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
   }
-  // one scale transfer per wave and step (1 KB):
-  //   wave 0 / 1: A scales (256 rows) of K block 2 step + wave (block 32) or step / 2
-  //   waves 2..7: B scales (128 rows) of K blocks 2 step + h (block 32) or step / 2
-  //               into half h; waves 3..7 repeat wave 2's transfer
-  const bool s_is_a = wave < 2;
-  const uint8_t *sbase = s_is_a ? g.sat + ((bt * g.T + r) * g.kblocks * g.mp + pm0) * 4
-                                : g.sbt + ((bt * g.T + r) * g.kblocks * g.np + pn0) * 4;
-  const int64_t splane = (s_is_a ? g.mp : g.np) * 4;   // bytes per K block
-  const uint32_t s_off = s_is_a ? 16u * (uint32_t)lane : 16u * (uint32_t)r32;
-  const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_a ? (BS == 32 ? wave * TM * 4 : 0) : ex::kScaleAX));
+  // one scale transfer per wave and step (fp32: 16 bytes a lane, E8M0: 4):
+  //   waves 0..3: the 256 A rows of K block NB step + (wave mod NB) (block
+  //               128: of block step / 2; the extra waves repeat a transfer)
+  //   waves 4..7: the 128 B rows of K blocks NB step + 2 p + h into lane half
+  //               h, p = (wave - 4) mod (NB / 2) (blocks 32 and 128: p = 0;
+  //               block 128: both halves take block step / 2)
+  const bool s_is_a = wave < 4;
+  const int sblk = s_is_a ? wave % NB : 2 * ((wave - 4) % (G::NBB / 2));
+  const int64_t srows = s_is_a ? g.mp : g.np;
+  const uint8_t *sbase = (s_is_a ? g.sat + (bt * g.T + r) * g.kblocks * g.mp * SB + pm0 * SB
+                                 : g.sbt + (bt * g.T + r) * g.kblocks * g.np * SB + pn0 * SB);
+  const int64_t splane = srows * SB;                   // bytes per K block
+  const uint32_t s_off = (uint32_t)(SB == 4 ? 16 : 4) * (uint32_t)(s_is_a ? lane : r32);
+  const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_a ? sblk * TM * SB : G::kScaleA + sblk * TN * SB));
 
   auto issue = [&](int step) {
-    const uint32_t m0 = lds_base + (uint32_t)(step % ex::kSlotsX) * ex::kSlotX;
+    const uint32_t m0 = lds_base + (uint32_t)(step % ex::kSlotsX) * G::kSlot;
     const int64_t src = (int64_t)step * kImage;
 #pragma unroll
     for (int j = 0; j < 3; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
-    int64_t kb;
-    if (s_is_a) kb = BS == 32 ? 2 * (int64_t)step + wave : step / 2;
-    else kb = BS == 32 ? 2 * (int64_t)step : step / 2;
-    // B lanes of half h read block kb + h (block 32) into bytes 512 h ..
-    const uint32_t hoff = (!s_is_a && BS == 32) ? (uint32_t)(h * splane) : 0u;
-    dma::copy16(s_off + hoff, sbase + kb * splane, m0 + sdst);
+    const int64_t kb = BS >= 64 ? step / 2 : (int64_t)NB * step + sblk;
+    // B lanes of half h read the next block (blocks 16, 32)
+    const uint32_t hoff = (!s_is_a && BS < 64) ? (uint32_t)(h * splane) : 0u;
+    if (SB == 4)
+      dma::copy16(s_off + hoff, sbase + kb * splane, m0 + sdst);
+    else
+      dma::copy4(s_off + hoff, sbase + kb * splane, m0 + sdst);
   };
 
   v16f acc[2][2], part[2][2];
@@ -338,63 +356,102 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
   // that its VALU work overlaps their matrix-core work.  Its scales are still
   // in LDS then: the ring has four slots and refills the one of step s - 2
   // during step s, so the previous step's slot stays intact.
-  auto promote = [&](const uint8_t *slot, int hs) {
-    const float *lsa = reinterpret_cast<const float *>(slot + kCodeA + kCodeB) + hs * TM;
-    const float *lsb = reinterpret_cast<const float *>(slot + kCodeA + kCodeB + ex::kScaleAX) + hs * TN;
+  auto promote = [&](const uint8_t *slot, int blk) {
+    const uint8_t *sa = slot + kCodeA + kCodeB + blk * TM * SB;
+    const uint8_t *sb = slot + kCodeA + kCodeB + G::kScaleA + blk * TN * SB;
+    // sB of the lane's column in column tile j
+    float sbv[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const float sbv = lsb[wn * 64 + 32 * j + r32];
+      if (SB == 4)
+        sbv[j] = reinterpret_cast<const float *>(sb)[wn * 64 + 32 * j + r32];
+      else   // tile-half row 64 wn + 32 j + r32 at byte 4 r32 + 2 wn + j
+        sbv[j] = e8m0_value(sb[4 * r32 + 2 * wn + j]);
+    }
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 2; ++i) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          // rows 64 wm + 32 i + 8 q + 4 h + u, u = 0..3: registers 4 q + u
-          const float4 sa4 = *reinterpret_cast<const float4 *>(lsa + wm * 64 + 32 * i + 8 * q + 4 * h);
-          const float sav[4] = {sa4.x, sa4.y, sa4.z, sa4.w};
+      for (int q = 0; q < 4; ++q) {
+        // rows 64 wm + 32 i + 8 q + 4 h + u, u = 0..3: registers 4 q + u
+        float sav[4];
+        if (SB == 4) {
+          const float4 sa4 = *reinterpret_cast<const float4 *>(sa + 4 * (wm * 64 + 32 * i + 8 * q + 4 * h));
+          sav[0] = sa4.x; sav[1] = sa4.y; sav[2] = sa4.z; sav[3] = sa4.w;
+        } else {
+          // tile row 128 H + 32 I + J at byte 4 (32 H + J) + I: here H = wm / 2,
+          // I = (2 wm + i) mod 4, J = 8 q + 4 h + u: byte I of four consecutive words
+          const uint4 w4 = *reinterpret_cast<const uint4 *>(sa + 128 * (wm >> 1) + 32 * q + 16 * h);
+          const int sh = 8 * ((2 * wm + i) & 3);
+          sav[0] = e8m0_value((w4.x >> sh) & 0xffu); sav[1] = e8m0_value((w4.y >> sh) & 0xffu);
+          sav[2] = e8m0_value((w4.z >> sh) & 0xffu); sav[3] = e8m0_value((w4.w >> sh) & 0xffu);
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            acc[i][j][4 * q + u] = __fmaf_rn(sav[u] * sbv, part[i][j][4 * q + u], acc[i][j][4 * q + u]);
-        }
+            acc[i][j][4 * q + u] = __fmaf_rn(sav[u] * sbv[j], part[i][j][4 * q + u], acc[i][j][4 * q + u]);
       }
     }
   };
 
-  // the four instructions per tile of one K-step; the first instruction of a
-  // block starts from zero (an inline constant: no register clears) and is
-  // preceded by the previous block's promote.  FRESH: the step opens a block
-  // of 128.  prev: the previous step's slot.
+  // one K-step.  The first instruction of a block starts from zero (an
+  // inline constant: no register clears) and is preceded by the previous
+  // block's promote.  FRESH: the step opens a block of 128.  prev: the
+  // previous step's slot.
+  auto mfma_group = [&](const v8bfx (&a)[2], const v8bfx (&b)[2], bool opens) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], opens ? (v16f){} : part[i][j], 0, 0, 0);
+  };
   auto mfma_step = [&](const uint8_t *la, const uint8_t *prev, auto FRESH) {
     constexpr bool fresh = decltype(FRESH)::value;
     const uint8_t *lb = la + kCodeA;
+    if (BS == 16) {
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      // this half's 16 bytes of each fragment row (bytes 32 half + 16 h ..)
-      uint4 fa[2], fb[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        fa[i] = *reinterpret_cast<const uint4 *>(la + swz64(wm * 64 + 32 * i + r32, 2 * half + h));
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        fb[j] = *reinterpret_cast<const uint4 *>(lb + swz64(wn * 64 + 32 * j + r32, 2 * half + h));
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const bool opens = BS == 32 ? tt == 0 : (fresh && half == 0 && tt == 0);
+      for (int blk = 0; blk < 4; ++blk) {
         v8bfx a[2], b[2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = tt == 0 ? codes8_to_bf16(fa[i].x, fa[i].y) : codes8_to_bf16(fa[i].z, fa[i].w);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) b[j] = tt == 0 ? codes8_to_bf16(fb[j].x, fb[j].y) : codes8_to_bf16(fb[j].z, fb[j].w);
-        if (opens) {
-          // block 32: the previous block is the other half (this step's, or
-          // the previous step's second); block 128: the previous step's
-          if (BS == 32) promote(half == 0 ? prev : la, half == 0 ? 1 : 0);
-          else promote(prev, 0);
+        for (int i = 0; i < 2; ++i) {
+          const uint2 w = *reinterpret_cast<const uint2 *>(la + swz64(wm * 64 + 32 * i + r32, blk) + 8 * h);
+          a[i] = codes8_to_bf16(w.x, w.y);
         }
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < 2; ++j) {
+          const uint2 w = *reinterpret_cast<const uint2 *>(lb + swz64(wn * 64 + 32 * j + r32, blk) + 8 * h);
+          b[j] = codes8_to_bf16(w.x, w.y);
+        }
+        promote(blk == 0 ? prev : la, blk == 0 ? 3 : blk - 1);
+        mfma_group(a, b, true);
+      }
+    } else {
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], opens ? (v16f){} : part[i][j], 0, 0, 0);
+      for (int half = 0; half < 2; ++half) {
+        // this half's 16 bytes of each fragment row (bytes 32 half + 16 h ..)
+        uint4 fa[2], fb[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          fa[i] = *reinterpret_cast<const uint4 *>(la + swz64(wm * 64 + 32 * i + r32, 2 * half + h));
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          fb[j] = *reinterpret_cast<const uint4 *>(lb + swz64(wn * 64 + 32 * j + r32, 2 * half + h));
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) {
+          const bool opens = BS == 32 ? tt == 0 : (fresh && half == 0 && tt == 0);
+          v8bfx a[2], b[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) a[i] = tt == 0 ? codes8_to_bf16(fa[i].x, fa[i].y) : codes8_to_bf16(fa[i].z, fa[i].w);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) b[j] = tt == 0 ? codes8_to_bf16(fb[j].x, fb[j].y) : codes8_to_bf16(fb[j].z, fb[j].w);
+          if (opens) {
+            // block 32: the previous block is the other half (this step's, or
+            // the previous step's second); block 128: the previous step's
+            if (BS == 32) promote(half == 0 ? prev : la, half == 0 ? 1 : 0);
+            else promote(prev, 0);
+          }
+          mfma_group(a, b, opens);
+        }
       }
     }
   };
@@ -402,7 +459,7 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
   // Step s: wait for this wave's own transfers of step s (four a step; those
   // of step s + 1 may stay in flight), barrier, start step s + 2 into the
   // slot of step s - 2, multiply step s.
-  auto slot_of = [&](int step) { return lds + (step & (ex::kSlotsX - 1)) * ex::kSlotX; };
+  auto slot_of = [&](int step) { return lds + (step & (ex::kSlotsX - 1)) * G::kSlot; };
   auto begin_step = [&](int step) -> const uint8_t * {
     if (step + 1 < nk) dma::wait_vmcnt<4>(); else dma::wait_vmcnt<0>();
     __syncthreads();
@@ -413,14 +470,14 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
   // which step 3 fills only after the first two barriers: zero them (and
   // part is zero), so that it adds 0 x 0
   {
-    float *z = reinterpret_cast<float *>(lds_raw) + ((ex::kSlotsX - 1) * ex::kSlotX + kCodeA + kCodeB) / 4;
-    for (int e = t; e < (ex::kScaleAX + ex::kScaleBX) / 4; e += ex::kThreadsX) z[e] = 0.0f;
+    uint32_t *z = reinterpret_cast<uint32_t *>(lds_raw) + ((ex::kSlotsX - 1) * G::kSlot + kCodeA + kCodeB) / 4;
+    for (int e = t; e < (G::kScaleA + G::kScaleB) / 4; e += ex::kThreadsX) z[e] = 0u;
   }
   issue(0);
   if (nk > 1) issue(1);
-  if (BS == 32) {
+  if (BS < 64) {
     for (int step = 0; step < nk; ++step) mfma_step(begin_step(step), slot_of(step + ex::kSlotsX - 1), std::false_type{});
-    promote(slot_of(nk - 1), 1);
+    promote(slot_of(nk - 1), NB - 1);
   } else {
     // a block of 128 is two steps (k' is a multiple of 128)
     for (int step = 0; step < nk; step += 2) {
@@ -564,11 +621,17 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
   g.tiles_m = (int)(pb.mp / TM);
   g.tiles_n = (int)(pb.np / TN);
   const int64_t items = pb.batch * pb.T * g.tiles_m * g.tiles_n;
-  if (pb.scale_bytes == 4) {
-    if (pb.block == 32)
-      hipLaunchKernelGGL(gemm_exact256x128_kernel<32>, dim3((unsigned)items), dim3(ex::kThreadsX), 0, st, g);
-    else
-      hipLaunchKernelGGL(gemm_exact256x128_kernel<128>, dim3((unsigned)items), dim3(ex::kThreadsX), 0, st, g);
+  if (exact_split(pb)) {
+    const dim3 grid((unsigned)items), block(ex::kThreadsX);
+    if (pb.scale_bytes == 4) {
+      if (pb.block == 16) hipLaunchKernelGGL((gemm_exact256x128_kernel<16, 4>), grid, block, 0, st, g);
+      else if (pb.block == 32) hipLaunchKernelGGL((gemm_exact256x128_kernel<32, 4>), grid, block, 0, st, g);
+      else hipLaunchKernelGGL((gemm_exact256x128_kernel<128, 4>), grid, block, 0, st, g);
+    } else {
+      if (pb.block == 16) hipLaunchKernelGGL((gemm_exact256x128_kernel<16, 1>), grid, block, 0, st, g);
+      else if (pb.block == 32) hipLaunchKernelGGL((gemm_exact256x128_kernel<32, 1>), grid, block, 0, st, g);
+      else hipLaunchKernelGGL((gemm_exact256x128_kernel<128, 1>), grid, block, 0, st, g);
+    }
     return hipGetLastError();
   }
   if (pb.block == 32)

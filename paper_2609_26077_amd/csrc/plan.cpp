@@ -99,19 +99,21 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
   pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
   const bool mx = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
-  // large-tile path: E8M0 scales applied by the MFMA, one or two levels,
-  // 256-row tiles, whole 64-byte (block 32) or 128-byte (block 128) K steps.
-  // It writes every P_r (4 bytes per output of each term) and reads it back,
-  // 8 / k' bytes per flop against the fused path's none: taken by default
-  // where that round trip costs less than the fused path's smaller tiles,
-  // k' >= 1024 (measured: the large tiles win at 1024, lose at 256).
-  // (E8M0 scales on the fp8 matrix cores, or fp32 scales on the exact-dot kernel)
-  const bool split_shape = ((!pb.exact_dot && pb.scale_bytes == 1) || pb.scale_bytes == 4) &&
-             (q.block == 32 || q.block == 128) &&
-             q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
-             pb.kp > 0 && pb.kp % (q.block == 32 ? 64 : 128) == 0 && pb.kp < (int64_t(1) << 26) &&
+  // large-tile path: one or two levels, 256-row tiles, whole 64-byte (blocks
+  // 16, 32) or 128-byte (block 128) K steps; E8M0 scales at blocks 32 and 128
+  // on the fp8 matrix cores, the exact-dot plans (fp32 scales, block 16, the
+  // flag) on the exact kernel.  It writes every P_r (4 bytes per output of
+  // each term) and reads it back, 8 / k' bytes per flop against the fused
+  // path's none: the fp8 plans take it by default where that round trip
+  // costs less than the fused path's smaller tiles, k' >= 1024 (measured:
+  // the large tiles win at 1024, lose at 512 and below); the exact-dot plans
+  // whenever the shape allows (the fused exact-dot kernel is slower at every
+  // measured k').
+  const bool split_shape = q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
+             pb.kp > 0 && pb.kp % (q.block == 128 ? 128 : 64) == 0 && pb.kp < (int64_t(1) << 26) &&
              q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);
-  pb.split = split_shape && (pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
+  pb.split = split_shape &&
+             (fmm::exact_split(pb) || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
   // fused 128 x 128 path: E8M0 scales, whole 128-row tiles and 128-byte K steps
   const bool tile128 = mx && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 && pb.kp % 128 == 0 &&
                        pb.kp < (int64_t(1) << 26);

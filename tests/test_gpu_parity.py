@@ -280,6 +280,25 @@ def test_large_tile_split_path(case):
 
 
 @pytest.mark.parametrize("case", [
+    ("tstar", 1, 512, 128, 512, 1, 16, 1, False),       # block 16, E8M0: one k-step, four blocks
+    ("strassen", 2, 512, 384, 1024, 1, 16, 0, False),   # block 16, fp32 scales, batch of two, three k-steps
+    ("winograd", 1, 512, 256, 512, 1, 32, 1, True),     # the exact-dot flag with E8M0 scales
+    ("tstar", 1, 512, 1024, 512, 1, 128, 2, True),      # the flag, OCP scales, block 128
+    ("cubic8", 1, 1024, 512, 1024, 2, 16, 1, False),    # depth 2, 64 terms, block 16
+    ("tstar", 1, 512, 640, 1536, 1, 32, 1, True),       # five k-steps, 1 x 3 tiles
+])
+def test_exact_large_tile_path(case):
+    """The exact-dot large-tile kernel (bf16 matrix cores on exactly
+    converted codes, one promote per block and output) at every block size,
+    with fp32 and E8M0 scales, at its default choice (exact-dot plans take the
+    large tiles whenever the shape allows)."""
+    name, b, M, K, N, depth, bs, rule, exact = case
+    r = check_case(name, "student_t3", b, M, K, N, depth, bs, rule, seed=18, cfg=10, exact=exact,
+                   layout=FMM_LAYOUT_TILE256x64)
+    print(case, r, flush=True)
+
+
+@pytest.mark.parametrize("case", [
     ("tstar", 1, 512, 1024, 512, 1, FMM_LAYOUT_TILE128x128),    # k' = 512: fused 128 x 128 path
     ("tstar", 1, 512, 2048, 512, 1, FMM_LAYOUT_TILE256x64),     # k' = 1024: large tiles
     ("tstar", 1, 1024, 2048, 1024, 2, FMM_LAYOUT_TILE128x128),  # depth 2, k' = 512
