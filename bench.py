@@ -40,6 +40,9 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--size", type=int, default=8192, help="M = K = N")
+    p.add_argument("--shape", type=int, nargs=3, metavar=("M", "K", "N"),
+                   help="a rectangular product instead of --size (the other configurations)")
+    p.add_argument("--batch", type=int, default=1, help="independent products per step")
     p.add_argument("--depth", type=int, default=1)
     p.add_argument("--block", type=int, default=32)
     p.add_argument("--rule", default="pow2_ceil")
@@ -247,13 +250,17 @@ def main():
 
     dev = torch.device("cuda:0")
     n = args.size
-    M = K = N = n
-    A, B = gen.operands(args.family, 1, M, K, N, seed=0, cfg=0, trial=0)
+    M, K, N = args.shape if args.shape else (n, n, n)
+    nb = args.batch
+    # the comparison arms, the paper context and the oracle baseline go with
+    # the headline shape (one cubic product)
+    headline = args.shape is None and nb == 1
+    A, B = gen.operands(args.family, nb, M, K, N, seed=0, cfg=0, trial=0)
     dA = torch.from_numpy(A).to(dev)
     dB = torch.from_numpy(B).to(dev)
     del A, B
-    f = FMM(args.realization, 1, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
-    C = torch.empty((1, M, N), dtype=torch.float32, device=dev)
+    f = FMM(args.realization, nb, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
+    C = torch.empty((nb, M, N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     for _ in range(args.warmup):
@@ -292,19 +299,19 @@ def main():
     phi = fmm_realization_metrics(real, args.depth)["phi"]
     a_view, _ = fmm_operand_views(f.plan, f.ws)
     split = a_view.code_layout == FMM_LAYOUT_TILE256x64
-    mkn = 2.0 * M * N * K
+    mkn = 2.0 * nb * M * N * K
     mfma_flop = mkn * T / 8.0 ** args.depth
     mp, kp, np_ = M // 2 ** args.depth, K // 2 ** args.depth, N // 2 ** args.depth
     sb = 4 if args.rule == "fp32_amax" else 1
-    code_bytes = T * (mp + np_) * kp
-    scale_bytes = T * (mp + np_) * (kp // args.block) * sb
-    enc_bytes = 4 * (M * K + K * N) + code_bytes + scale_bytes
-    prod_bytes = T * mp * np_ * 4 if split else 4 * M * N
-    comb_bytes = prod_bytes + 4 * M * N if split else 0
+    code_bytes = nb * T * (mp + np_) * kp
+    scale_bytes = nb * T * (mp + np_) * (kp // args.block) * sb
+    enc_bytes = 4 * nb * (M * K + K * N) + code_bytes + scale_bytes
+    prod_bytes = nb * T * mp * np_ * 4 if split else 4 * nb * M * N
+    comb_bytes = prod_bytes + 4 * nb * M * N if split else 0
     peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \
         else FP8_DENSE_PEAK_TFLOPS
     achieved = mfma_flop / (prod_ms * 1e-3) / 1e12
-    traffic = recorded_traffic("gemm_tile256x128" if split else "gemm_mx_fast", M, args)
+    traffic = recorded_traffic("gemm_tile256x128" if split else "gemm_mx_fast", M, args) if headline else None
 
     def hbm(nbytes, ms):
         gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
@@ -324,7 +331,7 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8",
         "data": "synthetic",
-        "config": {"workload": f"{M}x{K}x{N} product, depth {args.depth}, realization "
+        "config": {"workload": (f"batch {nb} x " if nb > 1 else "") + f"{M}x{K}x{N} product, depth {args.depth}, realization "
                                f"{args.realization} (Phi={phi:.4f}), e4m3 block {args.block} along K, "
                                f"{args.rule} scales, {args.family} operands"
                                + (", exact-dot" if args.exact_dot else ""),
@@ -348,10 +355,12 @@ def main():
     }
     if split:
         line["combine_roofline"] = hbm(comb_bytes, comb_ms)
-    if not args.no_arms:
+    if nb > 1:
+        line["config"]["batch"] = nb
+    if not args.no_arms and headline:
         line["arms"] = other_arms(args, dA, dB, C, stream)
         line["paper_context"] = paper_context()
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and headline:
         del dA, dB, C
         torch.cuda.empty_cache()
         line["cpu_baseline"] = cpu_baseline(args)
