@@ -287,7 +287,7 @@ def test_large_tile_split_path(case):
     ("cubic8", 1, 1024, 512, 1024, 2, 16, 1, False),    # depth 2, 64 terms, block 16
     ("tstar", 1, 512, 640, 1536, 1, 32, 1, True),       # five k-steps, 1 x 3 tiles
     ("strassen", 1, 1024, 1024, 1024, 2, 128, 1, True), # depth 2, the flag, block 128
-    ("winograd", 2, 1024, 256, 512, 2, 32, 0, False),   # depth 2, fp32 scales, batch of two, one k-step
+    ("winograd", 2, 1024, 256, 1024, 2, 32, 0, False),  # depth 2, fp32 scales, batch of two, one k-step
 ])
 def test_exact_large_tile_path(case):
     """The exact-dot large-tile kernel (bf16 matrix cores on exactly
