@@ -250,9 +250,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
 /* Bytes of device workspace fmm_encode/fmm_multiply/fmm_matmul need: the
  * codes and scales of both operands, plus, for large-tile plans the fp32
  * sub-products P_r, for the others at depth >= 2 the inner-level partial
- * products, and with
- * FMM_FLAG_B_BLOCK128 the B side's 2-D block maxima.  The workspace must be
- * 256-byte aligned. */
+ * products, and with FMM_FLAG_B_BLOCK128 the B side's 2-D block maxima.
+ * The workspace must be 256-byte aligned. */
 int fmm_plan_workspace_size(const fmm_plan *p, size_t *bytes);
 
 /* Steps "encode + quantize" of both operands (device pointers dA: batch x M x K,
