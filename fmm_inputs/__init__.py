@@ -68,6 +68,10 @@ def draw(family: str, shape, rng: np.random.Generator) -> np.ndarray:
         return np.where(rng.integers(0, 2, size=shape) == 0, -10.0, 10.0).astype(np.float32)
     if family == "laplace":
         return (rng.laplace(0.0, 1.0 / np.sqrt(2.0), size=shape)).astype(np.float32)
+    if family == "ones":
+        # a control, not a workload: every encoded combination of a term is
+        # one constant, so every code of the term is the same byte
+        return np.ones(shape, dtype=np.float32)
     raise ValueError(f"unknown operand family {family!r}")
 
 
