@@ -699,6 +699,60 @@ __global__ __launch_bounds__(256) void outer_combine_kernel(const float *__restr
   }
 }
 
+// The same with four consecutive columns per thread (n' a multiple of 4, C
+// 16-byte aligned): each Q plane read once as float4, eight outer terms'
+// loads issued together ahead of the multiply-adds, each term's NO weights
+// as one scalar block.  Same arithmetic and order as above.
+template <int NO>
+__global__ __launch_bounds__(256) void outer_combine4_kernel(const float *__restrict__ Q,
+                                                             const float *__restrict__ wo,
+                                                             float *__restrict__ C, Problem pb) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  constexpr int no = NO == 4 ? 2 : 4;   // 2^(l-1)
+  const int64_t n4 = pb.np / 4;
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // p * n4 + q4
+  const int iq = blockIdx.y;                                           // inner quadrant 2k + i
+  const int64_t bt = blockIdx.z;
+  if (pos >= pb.mp * n4) return;
+  const int64_t p = pos / n4, q4 = pos - p * n4;
+  const int64_t plane = 4 * pb.mp * pb.np;                             // floats per outer term
+  const float *src = Q + ((bt * pb.To * 4 + iq) * pb.mp + p) * pb.np + 4 * q4;
+  f4v acc[NO];
+#pragma unroll
+  for (int o = 0; o < NO; ++o) acc[o] = (f4v){0.f, 0.f, 0.f, 0.f};
+  const int To = (int)pb.To;
+  for (int r0 = 0; r0 < To; r0 += 8) {
+    f4v v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ro = min(r0 + j, To - 1);     // past the last term: a repeated, unused load
+      v[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(src + ro * plane));
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (r0 + j < To) {
+        float w[NO];
+#pragma unroll
+        for (int o = 0; o < NO; ++o) w[o] = wo[(r0 + j) * NO + o];
+#pragma unroll
+        for (int o = 0; o < NO; ++o) {
+          acc[o].x = __fmaf_rn(w[o], v[j].x, acc[o].x);
+          acc[o].y = __fmaf_rn(w[o], v[j].y, acc[o].y);
+          acc[o].z = __fmaf_rn(w[o], v[j].z, acc[o].z);
+          acc[o].w = __fmaf_rn(w[o], v[j].w, acc[o].w);
+        }
+      }
+    }
+  }
+  const int i = iq & 1, k = iq >> 1;
+#pragma unroll
+  for (int o = 0; o < NO; ++o) {
+    const int Ko = o / no, Io = o % no;
+    const int64_t I = 2 * Io + i, K = 2 * Ko + k;
+    *reinterpret_cast<f4v *>(C + bt * pb.M * pb.N + (I * pb.mp + p) * pb.N + K * pb.np + 4 * q4) = acc[o];
+  }
+}
+
 }  // namespace
 
 int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *ws,
@@ -739,6 +793,15 @@ int launch_combine(const Problem &pb, const DeviceTables &tab, const uint8_t *ws
   if (pb.depth == 1) return hipSuccess;     // fused into the sub-product kernel
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const float *Q = reinterpret_cast<const float *>(ws + wl.partial);
+  if (pb.np % 4 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0) {
+    const int64_t npos4 = pb.mp * (pb.np / 4);
+    const dim3 g4((unsigned)((npos4 + 255) / 256), 4, (unsigned)pb.batch);
+    if (pb.depth == 2)
+      hipLaunchKernelGGL(outer_combine4_kernel<4>, g4, dim3(256), 0, st, Q, tab.w_outer, C, pb);
+    else
+      hipLaunchKernelGGL(outer_combine4_kernel<16>, g4, dim3(256), 0, st, Q, tab.w_outer, C, pb);
+    return hipGetLastError();
+  }
   const int64_t npos = pb.mp * pb.np;
   const dim3 g2((unsigned)((npos + 255) / 256), 4, (unsigned)pb.batch);
   if (pb.depth == 2)
