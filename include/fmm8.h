@@ -57,7 +57,7 @@ enum {
   FMM_OK = 0,
   FMM_ERR_ARG = -1,          /* null pointer, out-of-range enum, bad tolerance */
   FMM_ERR_SHAPE = -2,        /* dimensions not divisible as required */
-  FMM_ERR_UNSUPPORTED = -3,  /* a shape/rule/block/depth this build does not run */
+  FMM_ERR_UNSUPPORTED = -3,  /* a shape/rule/block/depth the library does not run */
   FMM_ERR_NOT_EXACT = -4,    /* Brent residual above the tolerance */
   FMM_ERR_SINGULAR = -5,     /* a basis change with |det| < 1e-12 */
   FMM_ERR_HIP = -6,          /* a HIP runtime call or a kernel launch failed */

@@ -5,8 +5,7 @@ point it calls and forwards plain pointers and sizes.  Device memory and
 streams come from PyTorch (``torch.Tensor.data_ptr()``,
 ``torch.cuda.Stream.cuda_stream``); every computation runs in the library's
 HIP kernels.  Importing this module loads the library and fails loudly if it
-has not been built (run ``python paper_2609_26077_amd/_build.py`` or
-``__graft_entry__.build()``).
+has not been built (run ``python paper_2609_26077_amd/_build.py``).
 """
 from __future__ import annotations
 
