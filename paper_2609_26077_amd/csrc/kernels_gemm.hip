@@ -354,6 +354,32 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int &
   tn = in / gm;
 }
 
+// The (tile, outer term, batch) item of this workgroup.  Grids whose tile
+// count is not a multiple of eight (small batched products: 2 x 2 tiles of a
+// 256 x 256 sub-product) would spread the tiles of one item over four XCDs,
+// each fetching the item's codes into its own L2; there the linear dispatch
+// index L (x fastest) is remapped, as for the large-tile kernel, so that XCD
+// L mod 8 takes a contiguous range of items and all tiles of each (1024
+// products of 512^3: 0.64 -> 0.54 ms).  Grids of fewer than 2048 workgroups
+// (eight rounds of the 256 the chip holds) keep the plain order, which
+// measured slightly faster there.
+__device__ __forceinline__ void item_of(int tiles_m, int tiles_n, int &tm, int &tn, int64_t &ro, int64_t &bt) {
+  const int ntiles = tiles_m * tiles_n;
+  const int64_t total = (int64_t)ntiles * gridDim.y * gridDim.z;
+  if ((ntiles & 7) == 0 || (total & 7) != 0 || total < 2048) {
+    tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    ro = blockIdx.y;
+    bt = blockIdx.z;
+    return;
+  }
+  const int64_t L = blockIdx.x + (int64_t)ntiles * (blockIdx.y + (int64_t)gridDim.y * blockIdx.z);
+  const int64_t id = (L & 7) * (total >> 3) + (L >> 3);
+  const int64_t item = id / ntiles;
+  tile_of((int)(id - item * ntiles), tiles_m, tiles_n, tm, tn);
+  ro = item % gridDim.y;
+  bt = item / gridDim.y;
+}
+
 // Operands of one K step for one wave: fragments [substep s][tile i] and,
 // for each of its A and B row tiles, the two E8M0 scale bytes of the lane's
 // blocks (byte s: substep s).
@@ -374,8 +400,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
   const int wm = wave >> 1, wn = wave & 1;
   const int r32 = lane & 31, h = lane >> 5;
   int tm, tn;
-  tile_of(blockIdx.x, tiles_m, g.tiles_n, tm, tn);
-  const int64_t ro = blockIdx.y, bt = blockIdx.z;
+  int64_t ro, bt;
+  item_of(tiles_m, g.tiles_n, tm, tn, ro, bt);
   const int64_t pm0 = (int64_t)tm * BM, pn0 = (int64_t)tn * BN;
   const uint32_t kp = (uint32_t)g.kp, kblocks = (uint32_t)g.kblocks;
   const int nk = (int)(g.kp / FBK);
