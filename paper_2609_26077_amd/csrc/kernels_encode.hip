@@ -77,6 +77,13 @@ template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
+// The same permutation of a 32-bit pattern.  Maxima of non-negative finite
+// floats are taken on their bit patterns, which order like the unsigned
+// integers: one unsigned maximum with the permutation folded in per step.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
 
 // Read the tile into LDS ([block][row][l], row stride kStride floats).  Every
 // load is issued before the first LDS write, so the workgroup waits for HBM
@@ -394,10 +401,14 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
       m = fmaxf(m, __shfl_xor(m, 16, 64));
     }
     if (MODE != 2 || pb.b_rows == 1) {
-      if (BS >= 32) m = fmaxf(m, dpp<0xB1>(m));                 // quad_perm [1, 0, 3, 2]
-      if (BS == 128) {
-        m = fmaxf(m, dpp<0x4E>(m));                             // quad_perm [2, 3, 0, 1]
-        m = fmaxf(m, __shfl_xor(m, 32, 64));
+      if (BS >= 32) {
+        uint32_t mb = __float_as_uint(m);                       // m >= 0
+        mb = max(mb, dpp_u<0xB1>(mb));                          // quad_perm [1, 0, 3, 2]
+        if (BS == 128) {
+          mb = max(mb, dpp_u<0x4E>(mb));                        // quad_perm [2, 3, 0, 1]
+          mb = max(mb, (uint32_t)__shfl_xor((int)mb, 32, 64));
+        }
+        m = __uint_as_float(mb);
       }
     }
     if constexpr (MODE == 1) {
@@ -449,7 +460,38 @@ __device__ __forceinline__ float group_max(float m, int gl) {
   return m;
 }
 
-template <int SIDE>
+// The same over the bit patterns of non-negative finite values (equal to the
+// floating-point maximum), one unsigned maximum per step.
+template <int GL>
+__device__ __forceinline__ uint32_t group_max_bits(uint32_t m) {
+  m = max(m, dpp_u<0xB1>(m));
+  m = max(m, dpp_u<0x4E>(m));
+  if (GL >= 8) m = max(m, dpp_u<0x141>(m));
+  if (GL >= 16) m = max(m, dpp_u<0x140>(m));
+  if (GL >= 32) m = max(m, (uint32_t)__shfl_xor((int)m, 16, 64));
+  return m;
+}
+
+// Scale and codes of a lane's 4 values of a block whose maximum is m: the
+// fp32 rule divides (IEEE), the power-of-two rules scale exactly inside the
+// conversion.
+template <bool F32>
+__device__ __forceinline__ uint32_t quantize4(const Problem &pb, float m, float x0, float x1, float x2, float x3,
+                                              uint32_t &stored) {
+  if constexpr (F32) {
+    const dev::Scale sc = dev::block_scale(m, dev::RULE_FP32_AMAX);
+    stored = sc.stored;
+    return dev::e4m3_pack4(__fdiv_rn(x0, sc.div), __fdiv_rn(x1, sc.div), __fdiv_rn(x2, sc.div),
+                           __fdiv_rn(x3, sc.div));
+  } else {
+    const dev::Scale sc =
+        dev::block_scale(m, pb.rule == dev::RULE_POW2_CEIL ? dev::RULE_POW2_CEIL : dev::RULE_POW2_OCP);
+    stored = sc.stored;
+    return dev::e4m3_pack4_pow2(x0, x1, x2, x3, __uint_as_float(sc.stored << 23));
+  }
+}
+
+template <int SIDE, int BS, bool F32>
 __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
@@ -469,10 +511,10 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
   __syncthreads();
 
   const int64_t T = pb.T;
-  const int gl = pb.block / 4;               // lanes per block
+  constexpr int GL = BS / 4;                 // lanes per block
   const int pos = t % P;
   const int row = pos / (kTL / 4), c4 = pos % (kTL / 4);
-  const Out o = out_of(pb, rows, row0 + row, l0 + 4 * c4, (c4 % gl) == 0);
+  const Out o = out_of(pb, rows, row0 + row, l0 + 4 * c4, (c4 % GL) == 0);
   const int64_t code_plane = rows * pb.kp;
   const int64_t scale_plane = scale_plane_of(pb, rows);
   const float *lrow = lds + row * kStride + 4 * c4;
@@ -519,13 +561,14 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
       }
       first = false;
     }
-    const float m = group_max(fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3))), gl);
-    const dev::Scale sc = dev::block_scale(m, pb.rule);
-    const uint32_t w = dev::e4m3_pack4(dev::scaled(x0, sc, pb.rule), dev::scaled(x1, sc, pb.rule),
-                                       dev::scaled(x2, sc, pb.rule), dev::scaled(x3, sc, pb.rule));
+    const float m = __uint_as_float(
+        group_max_bits<GL>(__float_as_uint(fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3))))));
+    uint32_t stored;
+    const uint32_t w = quantize4<F32>(pb, m, x0, x1, x2, x3, stored);
+    // the plane's base is uniform; a lane's offset inside it fits in 32 bits
     const int64_t plane = bt * T + r;
-    if (o.valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + o.code) = w;
-    if (o.leader) store_scale(pb, scales, plane * scale_plane + o.scale, sc.stored);
+    if (o.valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + (uint32_t)o.code) = w;
+    if (o.leader) store_scale(pb, scales, plane * scale_plane + (uint32_t)o.scale, stored);
   }
 }
 
@@ -604,8 +647,24 @@ hipError_t launch_side(const Problem &pb, const float *src, const SideTab &cf,
       const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
       const int64_t tiles_r = (rows + Tile<3, 4, SIDE>::TR - 1) / Tile<3, 4, SIDE>::TR;
       const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-      hipLaunchKernelGGL((encode4_kernel<SIDE>), grid, dim3(Tile<3, 4, SIDE>::threads), 0, st, src, pb, cf, codes,
-                         scales, tiles_l);
+      const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
+      const dim3 blk(Tile<3, 4, SIDE>::threads);
+      switch (pb.block) {
+        case 16:
+          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 16, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          else hipLaunchKernelGGL((encode4_kernel<SIDE, 16, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          break;
+        case 32:
+          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 32, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          else hipLaunchKernelGGL((encode4_kernel<SIDE, 32, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          break;
+        case 128:
+          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 128, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          else hipLaunchKernelGGL((encode4_kernel<SIDE, 128, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+          break;
+        default:
+          return hipErrorInvalidValue;
+      }
       return hipGetLastError();
     }
   }
