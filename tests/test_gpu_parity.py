@@ -348,3 +348,31 @@ def test_products_then_combine_equals_multiply(shape, depth, flags):
     f.products(C2)
     f.combine(C2)
     assert torch.equal(C1, C2)
+
+
+def test_fused_and_large_tile_paths_agree_on_a_large_batch():
+    """512 products of 512^3 (k' = 256): the fused 128 x 128 path, whose
+    grid of 2 x 2-tile items is large enough to take the XCD-grouped item
+    order, and the large-tile path (forced by the flag) give C bit for bit
+    alike: both accumulate every sub-product over K in the same order on the
+    same scaled fp8 instruction and add w_r P_r in ascending r by fused
+    multiply-adds, so a tile computed twice or skipped by the item order
+    would show as a difference."""
+    import torch
+    from paper_2609_26077_amd import fmm_operand_views
+    from paper_2609_26077_amd.runner import FMM
+    b = 512
+    A, B = gen.operands("gaussian", b, 512, 512, 512, seed=21)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    del A, B
+    f1 = FMM("strassen", b, 512, 512, 512, 1, 32, "pow2_ceil")
+    f2 = FMM("strassen", b, 512, 512, 512, 1, 32, "pow2_ceil", flags=FMM_FLAG_LARGE_TILE)
+    assert fmm_operand_views(f1.plan, f1.ws)[0].code_layout == FMM_LAYOUT_TILE128x128
+    assert fmm_operand_views(f2.plan, f2.ws)[0].code_layout == FMM_LAYOUT_TILE256x64
+    C1 = torch.full((b, 512, 512), float("nan"), device="cuda:0")
+    C2 = torch.full_like(C1, float("nan"))
+    f1.matmul(dA, dB, C1)
+    f2.matmul(dA, dB, C2)
+    torch.cuda.synchronize()
+    assert not torch.isnan(C1).any()
+    assert torch.equal(C1, C2)
