@@ -61,16 +61,22 @@ constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slot
 
 // Tile geometry.  VEC = contracted positions per lane (16 at depths 1-2, 4 at
 // depth 3).  At depth 1 the B side takes 32 columns (its rows of B are read as
-// 128-byte segments) with four waves, the A side 16 rows with two.
-template <int DEPTH, int VEC, int SIDE>
+// 128-byte segments) with four waves, the A side 16 rows with two.  The
+// NARROW form (depth 2, B side, blocks of 16 and 32) takes 16 columns x 64
+// positions instead of 8 x 128, so B's rows are read as 64-byte segments
+// rather than 32-byte ones and a wave writes whole 64-byte code runs.
+template <int DEPTH, int VEC, int SIDE, bool NARROW = false>
 struct Tile {
   static constexpr int nblk = 1 << (2 * DEPTH);
-  static constexpr int TR = VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
+  static constexpr int TL = NARROW ? 64 : kTL;           // contracted positions per tile
+  static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
+  static constexpr int TR = NARROW ? 16 : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
   // depth 1: 128 (A) or 256 (B) threads; depths 2 and 3 deal the terms out to
   // eight waves, which with two workgroups per CU keeps four waves per SIMD
   static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? 128 : 256) : 512;
-  static constexpr int lds_floats = nblk * TR * kStride;   // 33.8 (A) / 67.6 (B), 67.6, 67.6 KB
+  static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B), 67.6 (69.6 narrow), 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
+  static_assert(!NARROW || (DEPTH == 2 && SIDE == 1 && VEC == 16), "the narrow tile is the depth-2 B side's");
 };
 
 template <int CTRL>
@@ -85,7 +91,7 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
 
-// Read the tile into LDS ([block][row][l], row stride kStride floats).  Every
+// Read the tile into LDS ([block][row][l], row stride TL + 4 floats).  Every
 // load is issued before the first LDS write, so the workgroup waits for HBM
 // once, not once per element.  The fp32 operands are read exactly once, so
 // the loads are nontemporal (they do not displace the codes, which the
@@ -93,12 +99,13 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
 // operand read as zero.
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-template <int SIDE, int NB, int TR, int NT>
+template <int SIDE, int NB, int TR, int NT, int TL = kTL>
 __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__ src, const Problem &pb,
                                            int64_t bt, int64_t row0, int64_t l0, int t) {
   constexpr int n = NB == 4 ? 2 : NB == 16 ? 4 : 8;
-  constexpr int kPer = NB * TR * (kTL / 4) / NT;      // float4s per thread
-  static_assert(NB * TR * (kTL / 4) % NT == 0, "the tile splits evenly over the threads");
+  constexpr int kStr = TL + 4;
+  constexpr int kPer = NB * TR * (TL / 4) / NT;       // float4s per thread
+  static_assert(NB * TR * (TL / 4) % NT == 0, "the tile splits evenly over the threads");
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t kp = pb.kp;
   float4 stage[kPer];
@@ -108,9 +115,9 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int e = t + NT * k;
-      const int b = e / (TR * (kTL / 4));
-      const int rem = e % (TR * (kTL / 4));
-      const int64_t p = row0 + rem / (kTL / 4), l = l0 + 4 * (rem % (kTL / 4));
+      const int b = e / (TR * (TL / 4));
+      const int rem = e % (TR * (TL / 4));
+      const int64_t p = row0 + rem / (TL / 4), l = l0 + 4 * (rem % (TL / 4));
       stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (p < rows && l < kp) {
         const int I = b / n, J = b % n;
@@ -121,9 +128,9 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int e = t + NT * k;
-      const int b = e / (TR * (kTL / 4));
-      const int rem = e % (TR * (kTL / 4));
-      *reinterpret_cast<float4 *>(lds + (b * TR + rem / (kTL / 4)) * kStride + 4 * (rem % (kTL / 4))) = stage[k];
+      const int b = e / (TR * (TL / 4));
+      const int rem = e % (TR * (TL / 4));
+      *reinterpret_cast<float4 *>(lds + (b * TR + rem / (TL / 4)) * kStr + 4 * (rem % (TL / 4))) = stage[k];
     }
   } else {
     // B (K x N): block b = J n + K holds rows J k' + l, columns K n' + q;
@@ -132,8 +139,8 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int e = t + NT * k;
-      const int b = e / (TR * (kTL / 4));
-      const int rem = e % (TR * (kTL / 4));
+      const int b = e / (TR * (TL / 4));
+      const int rem = e % (TR * (TL / 4));
       const int64_t qq = row0 + rem % TR, l = l0 + 4 * (rem / TR);
       stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
       if (qq < rows && l < kp) {
@@ -148,9 +155,9 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       const int e = t + NT * k;
-      const int b = e / (TR * (kTL / 4));
-      const int rem = e % (TR * (kTL / 4));
-      *reinterpret_cast<float4 *>(lds + (b * TR + rem % TR) * kStride + 4 * (rem / TR)) = stage[k];
+      const int b = e / (TR * (TL / 4));
+      const int rem = e % (TR * (TL / 4));
+      *reinterpret_cast<float4 *>(lds + (b * TR + rem % TR) * kStr + 4 * (rem / TR)) = stage[k];
     }
   }
 }
@@ -242,15 +249,21 @@ __device__ __forceinline__ float bf16_round(float x) {
   return __uint_as_float(b & 0xffff0000u);
 }
 
+// The plain depth-2 B-side encoder at blocks of 16 and 32 takes the narrow tile.
+constexpr bool narrow_b(int side, int depth, int bs, int mode) {
+  return side == 1 && depth == 2 && bs <= 32 && mode == 0;
+}
+
 template <int SIDE, int DEPTH, int BS, bool F32, int MODE>
-__global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_kernel(
+__global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l, void *__restrict__ aux) {
   static_assert(MODE == 0 || MODE == 3 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
   uint32_t *amax = reinterpret_cast<uint32_t *>(aux);
-  using TT = Tile<DEPTH, 16, SIDE>;
-  constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads;
-  constexpr int WPT = TR * 8 / 64;          // waves per term (2 or 4 at depth 1, 1 at depth 2)
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>;
+  constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads, TL = TT::TL, STR = TT::stride;
+  constexpr int RPW = 64 * 16 / TL;         // rows per wave: 8, or 16 in the narrow tile
+  constexpr int WPT = TR / RPW;             // waves per term (2 or 4 at depth 1, 1 at depth 2)
   constexpr int TSTEP = NT / 64 / WPT;      // terms a workgroup works on at once
   __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
@@ -258,16 +271,18 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
   const int t = threadIdx.x;
   const int64_t bt = blockIdx.y;
   const int64_t row0 = (blockIdx.x / tiles_l) * TR;
-  const int64_t l0 = (blockIdx.x % tiles_l) * kTL;
+  const int64_t l0 = (blockIdx.x % tiles_l) * TL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  stage_tile<SIDE, NB, TR, NT>(lds, src, pb, bt, row0, l0, t);
+  stage_tile<SIDE, NB, TR, NT, TL>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
 
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int ch = ((lane >> 5) << 2) | (lane & 3);            // 16-position run of the row
-  const int row = 8 * (wave % WPT) + ((lane >> 2) & 7);
-  const float *lrow = lds + row * kStride + 16 * ch;
+  // 16-position run of the row and the row: lane = 32 h + 4 r + c' (run 4 h + c'),
+  // or in the narrow tile lane = 4 r + c' (run c')
+  const int ch = TL == 64 ? (lane & 3) : ((lane >> 5) << 2) | (lane & 3);
+  const int row = RPW * (wave % WPT) + (TL == 64 ? (lane >> 2) : ((lane >> 2) & 7));
+  const float *lrow = lds + row * STR + 16 * ch;
   const bool lead = BS == 16 ? true : BS == 32 ? (ch & 1) == 0 : ch == 0;
   const Out o = out_of(pb, rows, row0 + row, l0 + 16 * ch, lead);
   const int64_t code_plane = rows * pb.kp;
@@ -299,8 +314,8 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
         const int b0 = next_block(mask, 0);
         const bool two = mask != 0;
         const int b1 = next_block(mask, b0);
-        const float4 *p0 = reinterpret_cast<const float4 *>(lrow + b0 * (TR * kStride));
-        const float4 *p1 = reinterpret_cast<const float4 *>(lrow + b1 * (TR * kStride));
+        const float4 *p0 = reinterpret_cast<const float4 *>(lrow + b0 * (TR * STR));
+        const float4 *p1 = reinterpret_cast<const float4 *>(lrow + b1 * (TR * STR));
         const float4 v[8] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
         const float c0 = lane_coef(c, b0), c1 = lane_coef(c, b1);
         const float *a = reinterpret_cast<const float *>(v);
@@ -331,7 +346,7 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE>::threads)) void encode16_ker
 #pragma unroll
       for (int e = 0; e < NB; ++e) {
         if (e < nc) {
-          const float4 *p = reinterpret_cast<const float4 *>(lrow + ce[e].block * (TR * kStride));
+          const float4 *p = reinterpret_cast<const float4 *>(lrow + ce[e].block * (TR * STR));
           const float4 v0 = p[0], v1 = p[1], v2 = p[2], v3 = p[3];
           const float a[16] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w,
                                v2.x, v2.y, v2.z, v2.w, v3.x, v3.y, v3.z, v3.w};
@@ -575,9 +590,9 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
 template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0>
 hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
                     uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
-  using TT = Tile<DEPTH, 16, SIDE>;
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
+  const int64_t tiles_l = (pb.kp + TT::TL - 1) / TT::TL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
   hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE>), grid, dim3(TT::threads), 0, st, src, pb, cf, codes,
