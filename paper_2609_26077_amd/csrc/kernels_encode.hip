@@ -65,18 +65,21 @@ constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slot
 // NARROW form (depth 2, B side, blocks of 16 and 32) takes 16 columns x 64
 // positions instead of 8 x 128, so B's rows are read as 64-byte segments
 // rather than 32-byte ones and a wave writes whole 64-byte code runs.
+constexpr int kB3Rows = 8;          // depth-3 B-side tile rows (columns of B), 32 positions each, at blocks <= 32
+
 template <int DEPTH, int VEC, int SIDE, bool NARROW = false>
 struct Tile {
   static constexpr int nblk = 1 << (2 * DEPTH);
-  static constexpr int TL = NARROW ? 64 : kTL;           // contracted positions per tile
+  static constexpr int TL = NARROW ? (DEPTH == 3 ? 256 / kB3Rows : 64) : kTL;   // contracted positions per tile
   static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
-  static constexpr int TR = NARROW ? 16 : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
+  static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? 32 : 16) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
   // depth 1: 128 (A) or 256 (B) threads; depths 2 and 3 deal the terms out to
   // eight waves, which with two workgroups per CU keeps four waves per SIMD
   static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? 128 : 256) : 512;
   static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B), 67.6 (69.6 narrow), 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
-  static_assert(!NARROW || (DEPTH == 2 && SIDE == 1 && VEC == 16), "the narrow tile is the depth-2 B side's");
+  static_assert(!NARROW || (DEPTH == 2 && SIDE == 1 && VEC == 16) || (DEPTH == 3 && SIDE == 1 && VEC == 4),
+                "the narrow tiles are the depth-2 and depth-3 B sides'");
 };
 
 template <int CTRL>
@@ -506,13 +509,15 @@ __device__ __forceinline__ uint32_t quantize4(const Problem &pb, float m, float 
   }
 }
 
+constexpr bool narrow_b3(int side, int bs) { return side == 1 && bs <= 256 / kB3Rows; }
+
 template <int SIDE, int BS, bool F32>
-__global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
+__global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) void encode4_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
-  using TT = Tile<3, 4, SIDE>;
-  constexpr int TR = TT::TR, NT = TT::threads;
-  constexpr int P = TR * (kTL / 4);          // positions (row, 4 consecutive l) per term
+  using TT = Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>;
+  constexpr int TR = TT::TR, NT = TT::threads, TL = TT::TL, STR = TT::stride;
+  constexpr int P = TR * (TL / 4);           // positions (row, 4 consecutive l) per term
   static_assert(P == 64 && TT::nblk == 64, "a wave's 64 items are one term's tile; lane b holds block b's coefficient");
   __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
@@ -520,19 +525,20 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
   const int t = threadIdx.x;
   const int64_t bt = blockIdx.y;
   const int64_t row0 = (blockIdx.x / tiles_l) * TR;
-  const int64_t l0 = (blockIdx.x % tiles_l) * kTL;
+  const int64_t l0 = (blockIdx.x % tiles_l) * TL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  stage_tile<SIDE, TT::nblk, TR, NT>(lds, src, pb, bt, row0, l0, t);
+  stage_tile<SIDE, TT::nblk, TR, NT, TL>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
 
   const int64_t T = pb.T;
   constexpr int GL = BS / 4;                 // lanes per block
   const int pos = t % P;
-  const int row = pos / (kTL / 4), c4 = pos % (kTL / 4);
+  const int row = pos / (TL / 4), c4 = pos % (TL / 4);
+  static_assert(BS <= TL, "a block lies in one row of the tile");
   const Out o = out_of(pb, rows, row0 + row, l0 + 4 * c4, (c4 % GL) == 0);
   const int64_t code_plane = rows * pb.kp;
   const int64_t scale_plane = scale_plane_of(pb, rows);
-  const float *lrow = lds + row * kStride + 4 * c4;
+  const float *lrow = lds + row * STR + 4 * c4;
   // the term's dense coefficient row (block b in lane b; 64 blocks) is loaded
   // one term ahead by a vector load; its nonzero blocks come from the wave's
   // ballot in ascending order, four per pass
@@ -559,7 +565,7 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE>::threads)) void encode4_kernel(
       }
       float4 v[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4 *>(lrow + b[j] * (TR * kStride));
+      for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4 *>(lrow + b[j] * (TR * STR));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (have[j]) {
@@ -659,8 +665,11 @@ hipError_t launch_side(const Problem &pb, const float *src, const SideTab &cf,
     case 2: return launch_wide<SIDE, 2>(pb, src, cf, codes, scales, st);
     case 3: {
       const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-      const int64_t tiles_l = (pb.kp + kTL - 1) / kTL;
-      const int64_t tiles_r = (rows + Tile<3, 4, SIDE>::TR - 1) / Tile<3, 4, SIDE>::TR;
+      // the B side's tile at blocks <= 256 / kB3Rows (its narrow form), else the common one
+      const bool nar = SIDE == 1 && pb.block <= 256 / kB3Rows;
+      const int TL = nar ? Tile<3, 4, 1, true>::TL : kTL, TR = nar ? Tile<3, 4, 1, true>::TR : Tile<3, 4, SIDE>::TR;
+      const int64_t tiles_l = (pb.kp + TL - 1) / TL;
+      const int64_t tiles_r = (rows + TR - 1) / TR;
       const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
       const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
       const dim3 blk(Tile<3, 4, SIDE>::threads);
