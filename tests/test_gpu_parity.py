@@ -67,6 +67,16 @@ def test_depths(depth, name):
                    cfg=4, exact=exact)
 
 
+@pytest.mark.parametrize("bs,rule,exact", [(16, 0, False), (128, 2, False), (32, 1, True), (16, 1, False)])
+def test_depth3_blocks_rules(bs, rule, exact):
+    """Depth 3 at every block size and scale rule: m' = 60 and n' = 52, so
+    the B side's tiles of 8 columns (blocks 16 and 32) or 2 columns (block
+    128) and the A side's 2-row tiles end partway, with k' covering two or
+    more 32-position tiles."""
+    K = 1024 if bs == 128 else 512
+    check_case("tstar", "gaussian", 1, 480, K, 416, 3, bs, rule, seed=23, cfg=6, exact=exact)
+
+
 def test_depth2_rules_blocks():
     check_case("winograd", "gaussian", 2, 264, 512, 200, 2, 16, 0, seed=4, cfg=5)
     for exact in (False, True):
