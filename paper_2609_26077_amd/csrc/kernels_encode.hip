@@ -1,7 +1,8 @@
 // Fused operand combine + block quantization (the encoder of Assumption 1).
 //
-// One workgroup owns a tile of TR "rows" x 128 contracted positions of the
-// sub-block grid and produces the codes and scales of every flattened term
+// One workgroup owns a tile of TR "rows" x TL contracted positions of the
+// sub-block grid (TL = 128, or 64 / 32 for the B side's narrow tiles at
+// depths 2 / 3) and produces the codes and scales of every flattened term
 // for that tile.  A rows are rows of A's sub-blocks; B rows are columns of
 // B's sub-blocks, so both outputs have the contracted axis last.
 //
@@ -463,29 +464,21 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MO
 }
 
 // ---------------------------------------------------------------------------
-// Depth 3: 4 positions per lane (2 rows x 128 positions per tile, 64 items of
-// one term per wave).
+// Depth 3: 4 positions per lane (2 rows x 128 positions per tile, or on the B
+// side at blocks 16 and 32 8 rows x 32 positions; 64 items of one term per
+// wave).
 // ---------------------------------------------------------------------------
-// max over each group of gl aligned lanes (gl = block / 4: 4, 8 or 32), every
-// lane receiving its group's maximum: quad permutations (xor 1, xor 2), then
-// the half-row and row mirrors, then across the two rows of 32 lanes.
-__device__ __forceinline__ float group_max(float m, int gl) {
-  m = fmaxf(m, dpp<0xB1>(m));        // quad_perm [1, 0, 3, 2]
-  m = fmaxf(m, dpp<0x4E>(m));        // quad_perm [2, 3, 0, 1]
-  if (gl >= 8) m = fmaxf(m, dpp<0x141>(m));   // row_half_mirror: lane i <- 7 - i within 8
-  if (gl >= 16) m = fmaxf(m, dpp<0x140>(m));  // row_mirror: lane i <- 15 - i within 16
-  if (gl >= 32) m = fmaxf(m, __shfl_xor(m, 16, 64));
-  return m;
-}
-
-// The same over the bit patterns of non-negative finite values (equal to the
+// Maximum over each group of GL aligned lanes (GL = block / 4: 4, 8 or 32),
+// every lane receiving its group's maximum: quad permutations (xor 1, xor 2),
+// then the half-row and row mirrors, then across the two rows of 32 lanes.
+// Taken on the bit patterns of non-negative finite values (equal to the
 // floating-point maximum), one unsigned maximum per step.
 template <int GL>
 __device__ __forceinline__ uint32_t group_max_bits(uint32_t m) {
-  m = max(m, dpp_u<0xB1>(m));
-  m = max(m, dpp_u<0x4E>(m));
-  if (GL >= 8) m = max(m, dpp_u<0x141>(m));
-  if (GL >= 16) m = max(m, dpp_u<0x140>(m));
+  m = max(m, dpp_u<0xB1>(m));                         // quad_perm [1, 0, 3, 2]
+  m = max(m, dpp_u<0x4E>(m));                         // quad_perm [2, 3, 0, 1]
+  if (GL >= 8) m = max(m, dpp_u<0x141>(m));           // row_half_mirror: lane i <- 7 - i within 8
+  if (GL >= 16) m = max(m, dpp_u<0x140>(m));          // row_mirror: lane i <- 15 - i within 16
   if (GL >= 32) m = max(m, (uint32_t)__shfl_xor((int)m, 16, 64));
   return m;
 }
