@@ -62,14 +62,15 @@ constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slot
 
 // Tile geometry.  VEC = contracted positions per lane (16 at depths 1-2, 4 at
 // depth 3).  At depth 1 the B side takes 32 columns (its rows of B are read as
-// 128-byte segments) with four waves, the A side 8 rows with two waves that
+// 128-byte segments) with eight waves (two terms at once), the A side 8 rows
+// with two waves that
 // split the terms between them (8-row tiles leave room for more workgroups
 // per CU than 16-row ones and measured 5-7% faster).  The
 // NARROW form (depth 2, B side, blocks of 16 and 32) takes 16 columns x 64
 // positions instead of 8 x 128, so B's rows are read as 64-byte segments
 // rather than 32-byte ones and a wave writes whole 64-byte code runs.
 constexpr int kA1Rows = 8, kA1Threads = 128;   // depth-1 A-side tile rows and threads
-constexpr int kB1Rows = 32, kB1Threads = 256;  // depth-1 B-side tile rows (columns of B) and threads
+constexpr int kB1Rows = 32, kB1Threads = 512;  // depth-1 B-side tile rows (columns of B) and threads
 constexpr int kB3Rows = 8;          // depth-3 B-side tile rows (columns of B), 32 positions each, at blocks <= 32
 
 template <int DEPTH, int VEC, int SIDE, bool NARROW = false>
@@ -78,7 +79,7 @@ struct Tile {
   static constexpr int TL = NARROW ? (DEPTH == 3 ? 256 / kB3Rows : 64) : kTL;   // contracted positions per tile
   static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
   static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? kB1Rows : kA1Rows) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
-  // depth 1: 128 (A) or 256 (B) threads; depths 2 and 3 deal the terms out to
+  // depth 1: 128 (A) or 512 (B) threads; depths 2 and 3 deal the terms out to
   // eight waves, which with two workgroups per CU keeps four waves per SIMD
   static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? kA1Threads : kB1Threads) : 512;
   static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B), 67.6 (69.6 narrow), 67.6 KB
