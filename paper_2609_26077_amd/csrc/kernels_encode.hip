@@ -80,8 +80,8 @@ struct Tile {
   static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
   static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? kB1Rows : kA1Rows) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
   // depth 1: 128 (A) or 512 (B) threads; depths 2 and 3 deal the terms out to
-  // eight waves, which with two workgroups per CU keeps four waves per SIMD
-  static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? kA1Threads : kB1Threads) : 512;
+  // sixteen waves, which with two workgroups per CU keeps eight waves per SIMD
+  static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? kA1Threads : kB1Threads) : 1024;
   static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B), 67.6 (69.6 narrow), 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
   static_assert(!NARROW || (DEPTH == 2 && SIDE == 1 && VEC == 16) || (DEPTH == 3 && SIDE == 1 && VEC == 4),
@@ -230,9 +230,12 @@ __device__ __forceinline__ void store_scale(const Problem &pb, uint8_t *scales, 
 // A wave covers 8 rows x 128 positions of one term: lane = 32 h + 4 r + c'
 // holds row r, positions 16 (4 h + c') .. +15, so a 16-lane group reads 4
 // rows x 4 slots (conflict-free at the odd stride) and a block of 32 is a lane
-// pair (lane, lane ^ 1), a block of 128 the quad plus its partner 32 lanes on.
-// Depth 1: 16 (A) or 32 (B) rows, one wave per 8 of them, every term; depth 2:
-// 8 rows, four waves, wave w takes terms w, w + 4, ...
+// pair (lane, lane ^ 1), a block of 128 the quad plus its partner 32 lanes on
+// (the narrow tiles: 16 rows x 64 positions, lane = 4 r + c').  The waves that
+// cover a tile's rows work on one term and the workgroup's wave groups take
+// the terms in turn: depth 1 A 8 rows (one wave per term, two terms at once),
+// B 32 rows (four waves per term, two terms at once); depth 2 one wave per
+// term, sixteen terms at once.
 // ---------------------------------------------------------------------------
 // Weight-side deployment granularity (FMM_FLAG_B_BLOCK128 / FMM_FLAG_B_BF16,
 // B side at depth 1), in two launches over the same tiles:
