@@ -104,8 +104,9 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
 // load is issued before the first LDS write, so the workgroup waits for HBM
 // once, not once per element.  The fp32 operands are read exactly once, so
 // the loads are nontemporal (they do not displace the codes, which the
-// sub-product kernel reads next, from the caches).  Positions outside the
-// operand read as zero.
+// sub-product kernel reads next, from the caches), except where a tile takes
+// only part of each cache line (B tiles narrower than 32 columns).  Positions
+// outside the operand read as zero.
 typedef float f4v __attribute__((ext_vector_type(4)));
 
 template <int SIDE, int NB, int TR, int NT, int TL = kTL>
@@ -155,10 +156,20 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
       if (qq < rows && l < kp) {
         const int J = b / n, Kb = b % n;
         const float *p = Bb + (J * kp + l) * pb.N + Kb * pb.np + qq;
-        stage[k].x = __builtin_nontemporal_load(p);
-        stage[k].y = __builtin_nontemporal_load(p + pb.N);
-        stage[k].z = __builtin_nontemporal_load(p + 2 * pb.N);
-        stage[k].w = __builtin_nontemporal_load(p + 3 * pb.N);
+        if constexpr (TR < 32) {
+          // tiles narrower than 32 columns read each 128-byte line of B in
+          // parts, the rest by the tiles of the neighbouring columns, which
+          // run at the same time on the same XCD: keep the lines in L2
+          stage[k].x = p[0];
+          stage[k].y = p[pb.N];
+          stage[k].z = p[2 * pb.N];
+          stage[k].w = p[3 * pb.N];
+        } else {
+          stage[k].x = __builtin_nontemporal_load(p);
+          stage[k].y = __builtin_nontemporal_load(p + pb.N);
+          stage[k].z = __builtin_nontemporal_load(p + 2 * pb.N);
+          stage[k].w = __builtin_nontemporal_load(p + 3 * pb.N);
+        }
       }
     }
 #pragma unroll
