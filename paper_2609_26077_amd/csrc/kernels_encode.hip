@@ -293,8 +293,14 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MO
 
   const int t = threadIdx.x;
   const int64_t bt = blockIdx.y;
-  const int64_t row0 = (blockIdx.x / tiles_l) * TR;
-  const int64_t l0 = (blockIdx.x % tiles_l) * TL;
+  // depth-1 B side: the column tile varies fastest over the workgroups, so
+  // neighbouring workgroups read adjacent 128-byte pieces of the same rows of
+  // B at about the same time (the narrower tiles of depths 2 and 3 instead
+  // rely on the neighbouring columns' tile running on the same XCD)
+  const int64_t tiles_r = gridDim.x / tiles_l;
+  constexpr bool qfast = SIDE == 1 && DEPTH == 1 && MODE != 3;
+  const int64_t row0 = (qfast ? blockIdx.x % tiles_r : blockIdx.x / tiles_l) * TR;
+  const int64_t l0 = (qfast ? blockIdx.x / tiles_r : blockIdx.x % tiles_l) * TL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   stage_tile<SIDE, NB, TR, NT, TL>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
