@@ -302,6 +302,23 @@ int fmm_error_stats_scratch_size(int64_t batch, int64_t M, int64_t N, size_t *by
 int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const double *dCref,
                     double *dOut, void *dScratch, size_t scratch_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fmm_error_stats without the scratch argument.  The reduction's partials
+ * live in a static device array of the library (8 MiB on every device the
+ * library runs on, held until the process ends), so at most
+ * FMM_ERROR_STATS_NOALLOC_MAX_BATCH products per call; a larger batch fails
+ * with FMM_ERR_WORKSPACE (fmm_last_error_detail() says why) before any device
+ * call.  Same kernels, same fixed order and results as fmm_error_stats.  The
+ * call itself allocates nothing; its first call on a device looks up the
+ * array's device address there.  Calls on one device share the array: calls
+ * that overlap in time on one device (other streams, other threads) race and
+ * must be serialized by the caller.  Every partial is written before it is
+ * read, so a call does not depend on what an earlier call left there. */
+#define FMM_ERROR_STATS_NOALLOC_MAX_BATCH 1024
+int fmm_error_stats_noalloc(int64_t batch, int64_t M, int64_t N, const float *dC, const double *dCref,
+                            double *dOut, void *stream);
+
 /* ---- the codec alone --------------------------------------------------- */
 
 /* Operand-side rounding energy of the encoding in dWs (Appendix D,

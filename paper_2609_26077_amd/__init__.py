@@ -116,6 +116,7 @@ _SIGS = {
                                                     ctypes.POINTER(ctypes.c_size_t)]),
     "fmm_error_stats": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                        _vp]),
+    "fmm_error_stats_noalloc": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp]),
     "fmm_e4m3_quantize": (ctypes.c_int, [_vp, _vp, _i64, _vp]),
     "fmm_encode_noise_scratch_size": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_size_t)]),
     "fmm_encode_noise": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
@@ -136,7 +137,7 @@ class FmmError(RuntimeError):
     def __init__(self, status: int, call: str):
         detail = _lib.fmm_last_error_detail().decode()
         msg = f"{call}: {_lib.fmm_status_string(status).decode()} ({status})"
-        if status == FMM_ERR_HIP and detail:
+        if status in (FMM_ERR_HIP, FMM_ERR_WORKSPACE) and detail:
             msg += f": {detail}"
         super().__init__(msg)
         self.status = status
@@ -401,6 +402,14 @@ def fmm_error_stats_scratch_size(batch, M, N) -> int:
 def fmm_error_stats(batch, M, N, C, Cref, out, scratch, scratch_bytes, stream=None) -> None:
     _check(_lib.fmm_error_stats(batch, M, N, _ptr(C), _ptr(Cref), _ptr(out), _ptr(scratch),
                                 int(scratch_bytes), _stream(stream)), "fmm_error_stats")
+
+
+FMM_ERROR_STATS_NOALLOC_MAX_BATCH = 1024
+
+
+def fmm_error_stats_noalloc(batch, M, N, C, Cref, out, stream=None) -> None:
+    _check(_lib.fmm_error_stats_noalloc(batch, M, N, _ptr(C), _ptr(Cref), _ptr(out), _stream(stream)),
+           "fmm_error_stats_noalloc")
 
 
 def fmm_e4m3_quantize(x, out, n, stream=None) -> None:

@@ -114,6 +114,10 @@ int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const f
 size_t error_stats_scratch_bytes(int64_t batch, int64_t M, int64_t N);
 int launch_error_stats(int64_t batch, int64_t M, int64_t N, const float *C, const double *Cref,
                        double *out, void *scratch, void *stream);
+// the allocation-free reduction: products per call, and the device address of
+// its static scratch on the current device (a hipError_t)
+constexpr int64_t kStaticErrorBatch = 1024;
+int static_error_scratch(void **ptr);
 int launch_e4m3_quantize(const float *in, uint8_t *out, int64_t n, void *stream);
 
 }  // namespace fmm

@@ -8,7 +8,11 @@
 //   binary64 by a fixed grid of workgroups (each a fixed-order strided sum and
 //   a fixed LDS tree), then one workgroup per product adds the partials in
 //   index order.  No atomics, so results are identical run to run.
+// The allocation-free form of the reduction keeps its partials in `scratch`,
+//   a static device array of this file (one copy per device).
 #include <hip/hip_runtime.h>
+
+#include <mutex>
 
 #include "device.h"
 #include "internal.h"
@@ -68,6 +72,11 @@ __global__ __launch_bounds__(256) void reference_f64_kernel(const float *__restr
 
 constexpr int kRedThreads = 256;
 constexpr int kRedBlocks = 512;   // partials per product
+
+// Partials of the allocation-free reduction: kStaticErrorBatch products of
+// kRedBlocks (err2, ref2) pairs, 8 MiB.  Every partial is written before it
+// is read, so nothing needs clearing between calls.
+static __device__ __align__(256) double scratch[kStaticErrorBatch * kRedBlocks * 2];
 
 __device__ __forceinline__ void tree_sum2(double *s0, double *s1, int t) {
   for (int w = kRedThreads / 2; w > 0; w >>= 1) {
@@ -166,6 +175,30 @@ int launch_error_stats(int64_t batch, int64_t M, int64_t N, const float *C, cons
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(error_totals_kernel, dim3((unsigned)batch), dim3(kRedThreads), 0, st, part, out);
   return hipGetLastError();
+}
+
+// The device address of `scratch` on the current device, looked up once per
+// device (each device holds its own copy of the array at its own address).
+// In host code the array's name is only a stand-in for the symbol, never an
+// address a kernel may be given.
+int static_error_scratch(void **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 int launch_e4m3_quantize(const float *in, uint8_t *out, int64_t n, void *stream) {

@@ -334,6 +334,22 @@ int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const 
   return hip_status(fmm::launch_error_stats(batch, M, N, dC, dCref, dOut, dScratch, stream));
 }
 
+int fmm_error_stats_noalloc(int64_t batch, int64_t M, int64_t N, const float *dC, const double *dCref,
+                            double *dOut, void *stream) {
+  if (batch < 0 || M < 0 || N < 0) return FMM_ERR_ARG;
+  if (batch > fmm::kStaticErrorBatch) {
+    g_detail = "fmm_error_stats_noalloc: batch " + std::to_string(batch) + " exceeds the static scratch (" +
+               std::to_string(fmm::kStaticErrorBatch) + " products)";
+    return FMM_ERR_WORKSPACE;
+  }
+  if (batch == 0) return FMM_OK;
+  if (!dOut || (M * N > 0 && (!dC || !dCref))) return FMM_ERR_ARG;
+  void *scratch = nullptr;
+  const int e = fmm::static_error_scratch(&scratch);
+  if (e != hipSuccess) return hip_status(e);
+  return hip_status(fmm::launch_error_stats(batch, M, N, dC, dCref, dOut, scratch, stream));
+}
+
 int fmm_encode_noise_scratch_size(const fmm_plan *p, size_t *bytes) {
   if (!p || !bytes) return FMM_ERR_ARG;
   if (p->pb.depth > 2) return FMM_ERR_UNSUPPORTED;

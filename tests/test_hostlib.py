@@ -225,3 +225,15 @@ def test_one_hip_runtime_whatever_the_import_order():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1", out.stdout
+
+
+def test_noalloc_error_stats_rejects_before_any_device_call(fm):
+    """The allocation-free reduction refuses a batch beyond its static
+    scratch, and bad sizes, without touching a device (this runs on a CPU)."""
+    n = fm.FMM_ERROR_STATS_NOALLOC_MAX_BATCH + 1
+    st = fm._lib.fmm_error_stats_noalloc(n, 4, 4, None, None, None, None)
+    assert st == fm.FMM_ERR_WORKSPACE
+    assert b"exceeds the static scratch" in fm._lib.fmm_last_error_detail()
+    assert fm._lib.fmm_error_stats_noalloc(-1, 4, 4, None, None, None, None) == fm.FMM_ERR_ARG
+    assert fm._lib.fmm_error_stats_noalloc(0, 4, 4, None, None, None, None) == fm.FMM_OK
+    assert fm._lib.fmm_error_stats_noalloc(2, 4, 4, None, None, None, None) == fm.FMM_ERR_ARG
