@@ -175,12 +175,15 @@ typedef struct {
 /* A named realization.  *out receives a new handle. */
 int fmm_realization_builtin(int which, fmm_real **out);
 
-/* A realization of <2,2,2;R> (1 <= R <= 8) from caller arrays U, V, w, each
- * R x 4 row-major binary64 in the conventions above.  If the Brent residual
- * max|sum_r U_r (x) V_r (x) w_r - <2,2,2>| exceeds tol the call fails with
- * FMM_ERR_NOT_EXACT (tol < 0 is FMM_ERR_ARG). */
-int fmm_realization_create(int R, const double *U, const double *V, const double *w,
-                           double tol, fmm_real **out);
+/* A realization of <m,k,n;R> (Section 2.1: R rank-one terms of the matrix
+ * multiplication tensor of an m x k by k x n product) from caller arrays U, V,
+ * w, each R x (m k), R x (k n), R x (n m) row-major binary64 in the
+ * conventions above.  The library runs <2,2,2;R>, 1 <= R <= 8: any other
+ * m, k, n >= 1 returns FMM_ERR_UNSUPPORTED (m, k or n < 1: FMM_ERR_ARG).  If
+ * the Brent residual max|sum_r U_r (x) V_r (x) w_r - <2,2,2>| exceeds tol the
+ * call fails with FMM_ERR_NOT_EXACT (tol < 0 is FMM_ERR_ARG). */
+int fmm_realization_create(int m, int k, int n, int R, const double *U, const double *V,
+                           const double *w, double tol, fmm_real **out);
 
 /* D . g for g = (X, Y, Z) in GL(2)^3 (eq. A.1):
  *   u -> u (X (x) Y^-T), v -> v (Y (x) Z^-T), w -> w (Z (x) X^-T),

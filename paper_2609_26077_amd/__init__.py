@@ -88,8 +88,8 @@ class fmm_view(ctypes.Structure):
 
 _SIGS = {
     "fmm_realization_builtin": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(_vp)]),
-    "fmm_realization_create": (ctypes.c_int, [ctypes.c_int, _dp, _dp, _dp, ctypes.c_double,
-                                              ctypes.POINTER(_vp)]),
+    "fmm_realization_create": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                              _dp, _dp, _dp, ctypes.c_double, ctypes.POINTER(_vp)]),
     "fmm_realization_transform": (ctypes.c_int, [_vp, _dp, _dp, _dp, ctypes.POINTER(_vp)]),
     "fmm_realization_rebalance": (ctypes.c_int, [_vp, ctypes.POINTER(_vp)]),
     "fmm_realization_optimize": (ctypes.c_int, [_vp, ctypes.c_int, _dp, ctypes.c_int, ctypes.c_double,
@@ -203,14 +203,17 @@ def _darr(a, n):
     return a, a.ctypes.data_as(_dp)
 
 
-def fmm_realization_create(U, V, w, tol: float = 1e-9) -> Realization:
+def fmm_realization_create(U, V, w, tol: float = 1e-9, shape=(2, 2, 2)) -> Realization:
+    """A realization of <m,k,n;R> from R x mk, R x kn, R x nm coefficient
+    arrays; shape = (m, k, n) (the library runs (2, 2, 2) only)."""
     import numpy as np
+    m, k, n = (int(x) for x in shape)
     R = int(np.asarray(U).shape[0])
-    Ua, Up = _darr(U, 4 * R)
-    Va, Vp = _darr(V, 4 * R)
-    Wa, Wp = _darr(w, 4 * R)
+    Ua, Up = _darr(U, m * k * R)
+    Va, Vp = _darr(V, k * n * R)
+    Wa, Wp = _darr(w, n * m * R)
     h = _vp()
-    _check(_lib.fmm_realization_create(R, Up, Vp, Wp, float(tol), ctypes.byref(h)),
+    _check(_lib.fmm_realization_create(m, k, n, R, Up, Vp, Wp, float(tol), ctypes.byref(h)),
            "fmm_realization_create")
     return Realization(h.value)
 

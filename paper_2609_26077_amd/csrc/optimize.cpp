@@ -351,7 +351,7 @@ int fmm_realization_optimize(const fmm_real *d, int nstarts, const double *start
   st = fmm::realization_optimize(D, nstarts, starts, max_iter, gtol, tol, best, best_phi, start_phi);
   if (st != FMM_OK) return st;
   // exactness was checked against tol above; the handle takes the coefficients as they are
-  st = fmm_realization_create(best.R, &best.U[0][0], &best.V[0][0], &best.W[0][0],
+  st = fmm_realization_create(2, 2, 2, best.R, &best.U[0][0], &best.V[0][0], &best.W[0][0],
                               std::numeric_limits<double>::infinity(), out);
   if (st == FMM_OK && phi) *phi = best_phi;
   return st;

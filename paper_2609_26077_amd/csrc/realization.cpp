@@ -268,10 +268,12 @@ int fmm_realization_builtin(int which, fmm_real **out) {
   return FMM_OK;
 }
 
-int fmm_realization_create(int R, const double *U, const double *V, const double *w, double tol,
-                           fmm_real **out) {
+int fmm_realization_create(int m, int k, int n, int R, const double *U, const double *V, const double *w,
+                           double tol, fmm_real **out) {
   if (!out) return FMM_ERR_ARG;
   *out = nullptr;
+  if (m < 1 || k < 1 || n < 1) return FMM_ERR_ARG;
+  if (m != 2 || k != 2 || n != 2) return FMM_ERR_UNSUPPORTED;   // <2,2,2;R> only
   if (!U || !V || !w || R < 1 || R > fmm::kMaxRank || !(tol >= 0.0)) return FMM_ERR_ARG;
   fmm_real *h = new (std::nothrow) fmm_real;
   if (!h) return FMM_ERR_NOMEM;

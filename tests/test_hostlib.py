@@ -121,6 +121,25 @@ def test_create_checks_exactness(fm):
         fm.fmm_realization_create(U, V, W, tol=-1.0)
 
 
+def test_create_accepts_only_222(fm):
+    """<m,k,n;R> other than <2,2,2> is refused as unsupported (e.g. the
+    <2,2,3;11> shape of Table E.1), before the coefficients are read; sizes
+    below one are argument errors."""
+    import ctypes
+    U, V, W = R.builtin_f64("strassen")
+    for shape, R_, status in (((2, 2, 3), 11, fm.FMM_ERR_UNSUPPORTED), ((3, 3, 3), 23, fm.FMM_ERR_UNSUPPORTED),
+                              ((2, 3, 2), 11, fm.FMM_ERR_UNSUPPORTED), ((0, 2, 2), 7, fm.FMM_ERR_ARG)):
+        m, k, n = shape
+        h = ctypes.c_void_p()
+        st = fm._lib.fmm_realization_create(m, k, n, R_, None, None, None, 0.0, ctypes.byref(h))
+        assert st == status and not h.value, (shape, st)
+    with pytest.raises(fm.FmmError) as e:
+        fm.fmm_realization_create(np.zeros((11, 6)), np.zeros((11, 6)), np.zeros((11, 4)), shape=(2, 3, 2))
+    assert e.value.status == fm.FMM_ERR_UNSUPPORTED
+    d = fm.fmm_realization_create(U, V, W, tol=0.0, shape=(2, 2, 2))
+    assert fm.fmm_realization_terms(d, 1) == (7, 7)
+
+
 @pytest.mark.parametrize("desc,status", [
     (dict(batch=1, M=256, K=256, N=256, depth=4), -1),        # depth out of range
     (dict(batch=1, M=256, K=256, N=256, block=64), -1),       # block not 16/32/128
