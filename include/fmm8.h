@@ -347,6 +347,16 @@ int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const 
  * 16-byte and dOut 4-byte aligned. */
 int fmm_e4m3_quantize(const float *dIn, uint8_t *dOut, int64_t n, void *stream);
 
+/* dOut[i] = e4m3 code of dIn[i] / 2^e: the cast the power-of-two scale rules
+ * (FMM_RULE_POW2_CEIL, FMM_RULE_POW2_OCP; E8M0 byte e + 127) apply to every
+ * element of a block, through the same device routine as the encoder.  The
+ * quotient is the binary32 value fl32(x / 2^e), then cast as above: round to
+ * nearest, ties to the even mantissa field, saturate to +-448 (a quotient
+ * beyond the binary32 range included), keep the sign.  e in [-126, 127] (the
+ * rules produce -48 .. 120; FMM_ERR_ARG otherwise); n >= 0; dIn 16-byte and
+ * dOut 4-byte aligned.  Asynchronous on stream. */
+int fmm_e4m3_quantize_pow2(const float *dIn, uint8_t *dOut, int64_t n, int32_t e, void *stream);
+
 /* ---- misc ---------------------------------------------------------------- */
 
 const char *fmm_status_string(int status);

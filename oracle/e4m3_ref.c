@@ -62,3 +62,23 @@ void oracle_e4m3_sweep(uint32_t start, size_t n, uint8_t *out)
         out[i] = encode_one(v);
     }
 }
+
+/* codes of x / 2^e for the n consecutive float32 bit patterns start,
+ * start+1, ... (the cast under a power-of-two block scale s = 2^e): the
+ * quotient x 2^-e is exact in binary64 for every finite x and e in
+ * [-126, 127], the conversion to float is the single binary32 rounding
+ * fl32(x / 2^e), and a quotient beyond the binary32 range (infinite after
+ * that rounding) saturates to 448 like every magnitude above it. */
+void oracle_e4m3_sweep_pow2(uint32_t start, size_t n, int e, uint8_t *out)
+{
+    for (size_t i = 0; i < n; ++i) {
+        uint32_t b = start + (uint32_t)i;
+        float v;
+        memcpy(&v, &b, 4);
+        float q = (float)ldexp((double)v, -e);
+        if (isinf(q))
+            out[i] = (uint8_t)(((b >> 31) << 7) | 0x7E);
+        else
+            out[i] = encode_one(q);
+    }
+}

@@ -118,6 +118,7 @@ _SIGS = {
                                        _vp]),
     "fmm_error_stats_noalloc": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp]),
     "fmm_e4m3_quantize": (ctypes.c_int, [_vp, _vp, _i64, _vp]),
+    "fmm_e4m3_quantize_pow2": (ctypes.c_int, [_vp, _vp, _i64, ctypes.c_int32, _vp]),
     "fmm_encode_noise_scratch_size": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_size_t)]),
     "fmm_encode_noise": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "fmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -417,6 +418,11 @@ def fmm_error_stats_noalloc(batch, M, N, C, Cref, out, stream=None) -> None:
 
 def fmm_e4m3_quantize(x, out, n, stream=None) -> None:
     _check(_lib.fmm_e4m3_quantize(_ptr(x), _ptr(out), int(n), _stream(stream)), "fmm_e4m3_quantize")
+
+
+def fmm_e4m3_quantize_pow2(x, out, n, e, stream=None) -> None:
+    _check(_lib.fmm_e4m3_quantize_pow2(_ptr(x), _ptr(out), int(n), int(e), _stream(stream)),
+           "fmm_e4m3_quantize_pow2")
 
 
 def fmm_status_string(status: int) -> str:

@@ -119,5 +119,6 @@ int launch_error_stats(int64_t batch, int64_t M, int64_t N, const float *C, cons
 constexpr int64_t kStaticErrorBatch = 1024;
 int static_error_scratch(void **ptr);
 int launch_e4m3_quantize(const float *in, uint8_t *out, int64_t n, void *stream);
+int launch_e4m3_quantize_pow2(const float *in, uint8_t *out, int64_t n, int e, void *stream);
 
 }  // namespace fmm

@@ -148,6 +148,23 @@ __global__ __launch_bounds__(256) void e4m3_quantize_kernel(const float *__restr
   }
 }
 
+// The cast of the power-of-two scale rules: codes of in[i] / s, s = 2^e,
+// through the routine the encoder applies to every block with an E8M0 scale.
+__global__ __launch_bounds__(256) void e4m3_quantize_pow2_kernel(const float *__restrict__ in,
+                                                                 uint8_t *__restrict__ out, int64_t n,
+                                                                 float s) {
+  const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 + 3 < n) {
+    const float4 v = *reinterpret_cast<const float4 *>(in + i4);
+    *reinterpret_cast<uint32_t *>(out + i4) = dev::e4m3_pack4_pow2(v.x, v.y, v.z, v.w, s);
+  } else if (i4 < n) {
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; i4 + k < n; ++k) v[k] = in[i4 + k];
+    const uint32_t w = dev::e4m3_pack4_pow2(v[0], v[1], v[2], v[3], s);
+    for (int k = 0; i4 + k < n; ++k) out[i4 + k] = (uint8_t)(w >> (8 * k));
+  }
+}
+
 }  // namespace
 
 int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *A,
@@ -207,6 +224,18 @@ int launch_e4m3_quantize(const float *in, uint8_t *out, int64_t n, void *stream)
   const int64_t groups = (n + 3) / 4;
   hipLaunchKernelGGL(e4m3_quantize_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, st,
                      in, out, n);
+  return hipGetLastError();
+}
+
+int launch_e4m3_quantize_pow2(const float *in, uint8_t *out, int64_t n, int e, void *stream) {
+  if (n == 0) return hipSuccess;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int64_t groups = (n + 3) / 4;
+  const uint32_t sbits = (uint32_t)(e + 127) << 23;   // 2^e, e in [-126, 127]
+  float s;
+  __builtin_memcpy(&s, &sbits, 4);
+  hipLaunchKernelGGL(e4m3_quantize_pow2_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, st,
+                     in, out, n, s);
   return hipGetLastError();
 }
 

@@ -379,4 +379,12 @@ int fmm_e4m3_quantize(const float *dIn, uint8_t *dOut, int64_t n, void *stream) 
   return hip_status(fmm::launch_e4m3_quantize(dIn, dOut, n, stream));
 }
 
+int fmm_e4m3_quantize_pow2(const float *dIn, uint8_t *dOut, int64_t n, int32_t e, void *stream) {
+  if (n < 0 || e < -126 || e > 127) return FMM_ERR_ARG;
+  if (n == 0) return FMM_OK;
+  if (!dIn || !dOut) return FMM_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(dIn) % 16 || reinterpret_cast<uintptr_t>(dOut) % 4) return FMM_ERR_ARG;
+  return hip_status(fmm::launch_e4m3_quantize_pow2(dIn, dOut, n, e, stream));
+}
+
 }  // extern "C"

@@ -29,6 +29,8 @@ def oracle_c_lib():
     lib = ctypes.CDLL(so)
     lib.oracle_e4m3_encode.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]
     lib.oracle_e4m3_sweep.argtypes = [ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p]
+    lib.oracle_e4m3_sweep_pow2.argtypes = [ctypes.c_uint32, ctypes.c_size_t, ctypes.c_int,
+                                           ctypes.c_void_p]
     return lib
 
 
@@ -248,3 +250,46 @@ def test_blocks2d_scale_is_the_block_max_and_codes_follow(rule):
             for (i, j), v in np.ndenumerate(blk):
                 q = np.float32(v / sb[0])
                 assert codes[rows][i, 16 * kb + j] == e4m3.encode_bruteforce(float(q))
+
+
+POW2_SWEEP_EXPONENTS = (-126, -48, -20, -9, 0, 8, 60, 119, 120, 127)
+
+
+@pytest.mark.parametrize("e", POW2_SWEEP_EXPONENTS)
+def test_c_codec_pow2_matches_numpy_codec(e):
+    """The C twin's cast under a power-of-two scale 2^e (the sweep the device
+    cast is checked against) equals the numpy codec applied to the binary32
+    quotient fl32(x / 2^e): runs of consecutive bit patterns at random
+    starts, and runs around every binary32 exponent boundary whose quotient
+    lands near the e4m3 range (subnormal quotients, midpoints, 448, overflow
+    of the quotient)."""
+    lib = oracle_c_lib()
+    rng = np.random.default_rng(1000 + e)
+    starts = list(rng.integers(0, 2 ** 32 - 4096, size=300))
+    for E in range(0, 255):                      # exponent field of x
+        q = E - 127 - e                          # exponent of the quotient
+        if -12 <= q <= 9 or E in (0, 1, 254):
+            for sign in (0, 1):
+                starts.append((sign << 31) | (E << 23) | int(rng.integers(0, 2 ** 23 - 4096)))
+                starts.append((sign << 31) | (E << 23))
+    n = 4096
+    for st in starts:
+        st = int(st)
+        got = np.empty(n, dtype=np.uint8)
+        lib.oracle_e4m3_sweep_pow2(st, n, e, got.ctypes.data)
+        pat = (np.arange(n, dtype=np.uint64) + st).astype(np.uint32)
+        x = pat.view(np.float32)
+        fin = np.isfinite(x)
+        with np.errstate(over="ignore"):
+            quot = (x[fin].astype(np.float64) * 2.0 ** -e).astype(np.float32)
+        want = e4m3.encode(quot)
+        assert np.array_equal(got[fin], want), (hex(st), e)
+
+
+def test_c_codec_pow2_saturates_overflowing_quotients():
+    lib = oracle_c_lib()
+    for e, pat in ((-126, 0x3F800000), (-48, 0x7F7FFFFF), (-9, 0x7F000000), (-1, 0x7F7FFFFF)):
+        for sign in (0, 1):
+            got = np.empty(1, dtype=np.uint8)
+            lib.oracle_e4m3_sweep_pow2((sign << 31) | pat, 1, e, got.ctypes.data)
+            assert got[0] == (0xFE if sign else 0x7E), (e, hex(pat))
