@@ -87,11 +87,14 @@ enum {
    * default sub-product path feeds the e4m3 codes and E8M0 scales to the
    * fp8 matrix cores, whose dot product aligns each group of eight products
    * to the group's largest and keeps 13 bits below it (measured on gfx950);
-   * with this flag the codes are converted exactly to bf16 and multiplied on
-   * the bf16 matrix cores (23 retained bits), each block's partial sum is
-   * scaled and accumulated in fp32.  Half the peak rate of the default path.
-   * FP32_AMAX scales and block 16 always take this path; tile-aligned plans
-   * (FMM_LAYOUT_TILE256x64) on it run on 256 x 128 tiles whatever K. */
+   * with this flag the operands go to the bf16 matrix cores (23 retained
+   * bits) exactly: with E8M0 scales each code is converted to bf16 together
+   * with its block's power of two (the dequantized value itself, exact for
+   * every scale the rules produce), with fp32 scales each block's partial
+   * sum of codes is scaled and accumulated in fp32.  Half the peak rate of
+   * the default path.  FP32_AMAX scales and block 16 always take this path;
+   * tile-aligned plans (FMM_LAYOUT_TILE256x64) on it run on 256 x 128 tiles
+   * whatever K. */
   FMM_FLAG_EXACT_DOT = 1,
   /* Weight-side deployment granularity (Appendix E, weight-scale
    * granularity; the real kernel's 128 x 128 weight blocks): one B-side scale

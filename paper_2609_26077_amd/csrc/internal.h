@@ -61,8 +61,9 @@ struct Problem {
   int b_bf16;              // round encoded B combinations to bfloat16 first (FMM_FLAG_B_BF16)
 };
 
-// Large-tile plans whose sub-products take the exact-dot kernel: fp32
-// scales, block 16, or the exact-dot flag.
+// Large-tile plans whose sub-products take an exact-dot kernel (fp32 scales,
+// block 16, or the exact-dot flag): the promote kernel for fp32 scales, the
+// folded-scale kernel for E8M0 scales.
 inline bool exact_split(const Problem &pb) { return pb.exact_dot || pb.scale_bytes == 4 || pb.block == 16; }
 
 // Bytes of one (batch, term) plane of scales for `rows` rows.

@@ -381,14 +381,44 @@ __device__ __forceinline__ void item_of(int tiles_m, int tiles_n, int &tm, int &
 }
 
 // Operands of one K step for one wave: fragments [substep s][tile i] and,
-// for each of its A and B row tiles, the two E8M0 scale bytes of the lane's
-// blocks (byte s: substep s).
+// for each of its A and B row tiles, the E8M0 scale bytes: on the fp8 path
+// the two of the lane's blocks (byte s: substep s), on the exact-dot path
+// the row's whole record of the step.
 struct MxFrags {
   v8i a[2][2], b[2][2];
   int sa[2], sb[2];
 };
 
-template <int BS>
+// codes in dwords d, d + 1 of a fragment, times the power of two whose
+// exponent field `s` carries, as eight bf16 (exact: the dequantized values)
+__device__ __forceinline__ v8bf dequant8(const v8i &f, int d, float s) {
+  const v2bf a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(f[d], s, false);
+  const v2bf b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(f[d], s, true);
+  const v2bf c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(f[d + 1], s, false);
+  const v2bf e = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(f[d + 1], s, true);
+  v8bf r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
+  r[4] = c[0]; r[5] = c[1]; r[6] = e[0]; r[7] = e[1];
+  return r;
+}
+
+// 2^(byte - 127) of byte i of a scale record (byte >= 1 for every rule's scale)
+__device__ __forceinline__ float e8m0_at(int w, int i) {
+  return __uint_as_float((((uint32_t)w >> (8 * i)) & 0xffu) << 23);
+}
+
+// DQ = false: the fp8 matrix cores with the E8M0 scales applied by the
+// scaled MFMA.  DQ = true (exact-dot plans with E8M0 scales): the same
+// transfers, fragments and fused W-combine, but every 64-byte substep runs as
+// four v_mfma_f32_32x32x16_bf16 per tile pair on the dequantized operands,
+// each code converted to bf16 together with its block's power of two
+// (v_cvt_scalef32_pk_bf16_fp8; exact for every scale the rules produce), so
+// the products of the dequantized operands are summed across the whole
+// contracted axis at fp32 grade.  Instruction t of substep s takes, in lane
+// half h, bytes 64 s + 32 (t >> 1) + 16 h + 8 (t & 1) .. + 7 of the row on both
+// operands, which lie in block 2 s + (t >> 1) at block 32 (record byte
+// 2 (t >> 1) + s, the record holding blocks 0, 2, 1, 3).
+template <int BS, bool DQ>
 __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, int tiles_m) {
   __shared__ uint4 lds_raw[kSlots * kSlot / 16];
   __shared__ float lds_w[4 * kMaxRank];
@@ -448,8 +478,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     const uint8_t *lsb = lsa + BM * 4;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      f.sa[i] = *reinterpret_cast<const uint16_t *>(lsa + 4 * (wrow_a + 32 * i + r32) + 2 * h);
-      f.sb[i] = *reinterpret_cast<const uint16_t *>(lsb + 4 * (wrow_b + 32 * i + r32) + 2 * h);
+      if (DQ) {
+        f.sa[i] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + 32 * i + r32));
+        f.sb[i] = *reinterpret_cast<const int *>(lsb + 4 * (wrow_b + 32 * i + r32));
+      } else {
+        f.sa[i] = *reinterpret_cast<const uint16_t *>(lsa + 4 * (wrow_a + 32 * i + r32) + 2 * h);
+        f.sb[i] = *reinterpret_cast<const uint16_t *>(lsb + 4 * (wrow_b + 32 * i + r32) + 2 * h);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -485,21 +520,41 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     if (step + 3 < total) issue(step + 3);
     const int ks = step % nk;
     load(step + 1, nxt);
+    if constexpr (DQ) {
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss)
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+          const int c = tt >> 1, d = 4 * c + 2 * (tt & 1);
+          const int sbyte = BS == 32 ? 2 * c + ss : 0;
+          v8bf fa[2], fb[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) fa[i] = dequant8(cur.a[ss][i], d, e8m0_at(cur.sa[i], sbyte));
+#pragma unroll
+          for (int j = 0; j < 2; ++j) fb[j] = dequant8(cur.b[ss][j], d, e8m0_at(cur.sb[j], sbyte));
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+    } else {
 #define FMM_MFMA_SIJ(S, I, J)                                                                      \
   acc[I][J] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[S][I], cur.b[S][J], acc[I][J], 0, 0, \
                                                               S, cur.sa[I], S, cur.sb[J])
-    FMM_MFMA_SIJ(0, 0, 0); FMM_MFMA_SIJ(0, 0, 1); FMM_MFMA_SIJ(0, 1, 0); FMM_MFMA_SIJ(0, 1, 1);
-    FMM_MFMA_SIJ(1, 0, 0); FMM_MFMA_SIJ(1, 0, 1); FMM_MFMA_SIJ(1, 1, 0); FMM_MFMA_SIJ(1, 1, 1);
+      FMM_MFMA_SIJ(0, 0, 0); FMM_MFMA_SIJ(0, 0, 1); FMM_MFMA_SIJ(0, 1, 0); FMM_MFMA_SIJ(0, 1, 1);
+      FMM_MFMA_SIJ(1, 0, 0); FMM_MFMA_SIJ(1, 0, 1); FMM_MFMA_SIJ(1, 1, 0); FMM_MFMA_SIJ(1, 1, 1);
 #undef FMM_MFMA_SIJ
-    // MFMA and LDS reads alternate: 1 MFMA, then 3 reads (20 reads over 7 gaps)
+      // MFMA and LDS reads alternate: 1 MFMA, then 3 reads (20 reads over 7 gaps)
 #pragma unroll
-    for (int k = 0; k < 6; ++k) {
+      for (int k = 0; k < 6; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+      }
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     if (ks + 1 == nk) {
       const int ri = step / nk;
       // end of term ri: quadrant q += w[ri][q] * P
@@ -800,11 +855,17 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
   g.w = tab.w_inner;
   const dim3 grid((unsigned)(tiles_m * tiles_n), (unsigned)pb.To, (unsigned)pb.batch);
   const bool mx = !pb.exact_dot && pb.rule != dev::RULE_FP32_AMAX && (pb.block == 32 || pb.block == 128);
+  // the 128 x 128 tile layout: E8M0 scales at blocks 32 and 128 (fp8 path, or
+  // the exact-dot path with each block's power of two folded into the codes)
   const bool aligned = pb.layout == FMM_LAYOUT_TILE128x128;
-  if (mx && aligned && pb.block == 32)
-    hipLaunchKernelGGL(gemm_mx_fast_kernel<32>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
-  else if (mx && aligned && pb.block == 128)
-    hipLaunchKernelGGL(gemm_mx_fast_kernel<128>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  if (aligned && pb.exact_dot && pb.block == 32)
+    hipLaunchKernelGGL((gemm_mx_fast_kernel<32, true>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  else if (aligned && pb.exact_dot)
+    hipLaunchKernelGGL((gemm_mx_fast_kernel<128, true>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  else if (aligned && pb.block == 32)
+    hipLaunchKernelGGL((gemm_mx_fast_kernel<32, false>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  else if (aligned)
+    hipLaunchKernelGGL((gemm_mx_fast_kernel<128, false>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
   else if (mx)
     hipLaunchKernelGGL(gemm_mx_kernel, grid, dim3(kThreads), 0, st, g);
   else

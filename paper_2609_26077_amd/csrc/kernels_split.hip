@@ -13,6 +13,10 @@
 //      keep the SIMDs busy.  64-byte K steps run through a three-slot LDS ring
 //      filled by global_load_lds two steps ahead, one barrier per step; P_r is
 //      stored in fp32 with nontemporal stores.
+//      Exact-dot plans take gemm_dq256x128_kernel (E8M0 scales: each block's
+//      power of two folded into the codes' conversion to bf16) or
+//      gemm_exact256x128_kernel (fp32 scales: per-block partial sums promoted
+//      in fp32) instead, on the same tiles and layouts.
 //   2. combine1_kernel: C block (i, k) = sum_r w[r][2k + i] P_r, ascending r,
 //      one fused multiply-add per nonzero weight (the order of the fused
 //      W-combine of the 128 x 128 path); combine2_kernel the same over the
@@ -225,15 +229,188 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 }
 
 // ---------------------------------------------------------------------------
-// Exact-dot large-tile sub-products (fp32 amax/448 scales, block 16, or the
-// exact-dot flag; blocks 16, 32 and 128; fp32 or E8M0 scales).
+// Exact-dot large-tile sub-products with power-of-two (E8M0) scales, blocks
+// 16, 32 and 128: the dequantized operands themselves on the bf16 matrix
+// cores.
 //
-// fp32 scales are arbitrary numbers, which the scaled fp8 MFMA cannot apply,
-// blocks of 16 are finer than its scale granularity, and the fp8 matrix
-// cores' dot product is narrower than fp32; so each block's partial sum of
-// code products is formed exactly on the bf16 matrix cores (e4m3 -> bf16 is
-// exact, products of two codes are exact in fp32) and promoted into the fp32
-// accumulator as acc += (sA sB) partial.  Per block and output that is two
+// v_cvt_scalef32_pk_bf16_fp8 multiplies a code by the power of two its scale
+// operand holds while converting it: code 2^e has at most four significant
+// bits and, for every scale the rules produce (e in [-48, 120]) and every
+// code below 256 2^e at e = 120, lies in the normal bf16 range, so the
+// converted value is the dequantized operand exactly.  The product of two
+// such values is exact in fp32, and v_mfma_f32_32x32x16_bf16 sums them
+// across the whole contracted axis at fp32 grade: the fp32 accumulation of
+// the dequantized products, with no per-block promote (each block's scale
+// rides in its codes' conversion).
+//
+// Same tiles, LDS ring, transfers and work order as gemm_tile256x128_kernel
+// (four waves of 128 x 64, two workgroups per CU); the 64-byte K step is four
+// bf16 instructions per 32 x 32 tile.  Instruction t of a step takes, in
+// lane half h, bytes 32 (t >> 1) + 16 h + 8 (t & 1) .. + 7 of the lane's row
+// on both operands (so the four instructions cover the step's 64 positions
+// once each); those 8 bytes always lie in one block.  Scales per step: the
+// step's K blocks (4 at block 16, 2 at block 32, the one block of two steps
+// at block 128) for the 256 A rows and the 128 B rows.
+namespace dq {
+constexpr int kMaxBlocks = 4;                              // K blocks per step (block 16)
+constexpr int kScaleA = kMaxBlocks * TM;                   // 1 KB of A scale bytes
+constexpr int kScaleB = kMaxBlocks * TN;                   // 512 B of B scale bytes
+constexpr int kSlot = kCodeA + kCodeB + kScaleA + kScaleB;  // 26112 B
+static_assert(2 * kSlots * kSlot <= 160 * 1024, "two workgroups per CU");
+}  // namespace dq
+
+typedef __bf16 v8bfq __attribute__((ext_vector_type(8)));
+typedef __bf16 v2bfq __attribute__((ext_vector_type(2)));
+
+// eight codes (two little-endian words) -> their values times the power of
+// two whose exponent field `s` carries, as bf16 (exact)
+__device__ __forceinline__ v8bfq dequant8(uint32_t lo, uint32_t hi, float s) {
+  const v2bfq a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, s, false);
+  const v2bfq b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)lo, s, true);
+  const v2bfq c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, s, false);
+  const v2bfq d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)hi, s, true);
+  v8bfq r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
+  r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
+  return r;
+}
+
+// 2^(byte - 127) for E8M0 byte i of word w (byte >= 1 for every rule's scale)
+__device__ __forceinline__ float e8m0_byte(uint32_t w, int i) {
+  return __uint_as_float(((w >> (8 * i)) & 0xffu) << 23);
+}
+
+template <int BS>
+__global__ __launch_bounds__(kThreads, 2) void gemm_dq256x128_kernel(SplitArgs g) {
+  constexpr int NB = BS >= 64 ? 1 : 64 / BS;   // K blocks per step
+  __shared__ uint4 lds_raw[kSlots * dq::kSlot / 16];
+  const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
+  const uint32_t lds_base = dma::lds_addr(lds_raw);
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = wave >> 1, wn = wave & 1;       // A rows 128 wm.., B rows 64 wn.. of the tile
+  const int r32 = lane & 31, h = lane >> 5;
+  const int64_t nitems = (int64_t)gridDim.x;
+  int64_t bt, r;
+  int tm, tn;
+  work_of(blockIdx.x, nitems, g.T, g.tiles_m, g.tiles_n, bt, r, tm, tn);
+  const int64_t pm0 = (int64_t)tm * TM, pn0 = (int64_t)tn * TN;
+  const int hb = tn & 1;
+  const int nk = (int)(g.kp / SK);
+  const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kImage;
+  const uint8_t *xb = g.xb + ((bt * g.T + r) * (g.tiles_n / 2) + (tn >> 1)) * (int64_t)nk * kImage + hb * kCodeB;
+  const uint32_t code_off = 16u * (uint32_t)lane;
+  const uint8_t *csrc[6];
+  uint32_t cdst[6];
+#pragma unroll
+  for (int j = 0; j < 6; ++j) {
+    const int region = wave * 6 + j;
+    csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
+    cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
+  }
+  // Two scale transfers per wave and step (4 bytes a lane):
+  //   A: wave w moves the 256 bytes of the step's K block w mod NB into
+  //      A slot block w mod NB (the extra waves repeat a transfer);
+  //   B: lanes 32 k + r32 move the 128 bytes of K block 2 q + k into B slot
+  //      block 2 q + k, q = wave mod (NB / 2) (block 128: both lane halves
+  //      take the step's one block; block 32: q = 0).
+  const int ablk = wave % NB;
+  const int bq = NB >= 2 ? wave % (NB / 2) : 0;
+  const int bblk = NB >= 2 ? 2 * bq + h : 0;
+  const uint8_t *sa_src = g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0;
+  const uint8_t *sb_src = g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0;   // bytes 128 hb .. of the 256-row tile
+  const uint32_t sa_off = 4u * (uint32_t)lane + (uint32_t)(ablk * g.mp);
+  const uint32_t sb_off = 4u * (uint32_t)r32 + (uint32_t)(bblk * g.np);
+  const uint32_t sa_dst = (uint32_t)(kCodeA + kCodeB + ablk * TM);
+  const uint32_t sb_dst = (uint32_t)(kCodeA + kCodeB + dq::kScaleA + 2 * bq * TN);
+
+  auto issue = [&](int step) {
+    const uint32_t m0 = lds_base + (uint32_t)(step % kSlots) * dq::kSlot;
+    const int64_t src = (int64_t)step * kImage;
+#pragma unroll
+    for (int j = 0; j < 6; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
+    const int64_t kb0 = BS >= 64 ? step / 2 : (int64_t)NB * step;   // first K block of the step
+    dma::copy4(sa_off, sa_src + kb0 * g.mp, m0 + sa_dst);
+    dma::copy4(sb_off, sb_src + kb0 * g.np, m0 + sb_dst);
+  };
+
+  v16f acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = (v16f){};
+
+  // one step: raw 16-byte chunks c = 0, 1 (bytes 32 c + 16 h ..) of the
+  // lane's rows, the scales of the blocks they lie in, four instructions
+  auto step_mfma = [&](int step) {
+    const uint8_t *la = lds + (step % kSlots) * dq::kSlot;
+    const uint8_t *lb = la + kCodeA;
+    const uint8_t *ls = lb + kCodeB;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      // K block of chunk c within the slot: block 16: 2 c + h; 32: c; 128: 0
+      const int bi = BS == 16 ? 2 * c + h : (BS == 32 ? c : 0);
+      const uint32_t wa = *reinterpret_cast<const uint32_t *>(ls + bi * TM + 4 * (wm * 32 + r32));
+      const uint32_t wb = *reinterpret_cast<const uint32_t *>(ls + dq::kScaleA + bi * TN + 4 * r32) >> (16 * wn);
+      uint4 ra[4], rb[2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        ra[i] = *reinterpret_cast<const uint4 *>(la + swz64(wm * 128 + 32 * i + r32, 2 * c + h));
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        rb[j] = *reinterpret_cast<const uint4 *>(lb + swz64(wn * 64 + 32 * j + r32, 2 * c + h));
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        v8bfq fa[4], fb[2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          fa[i] = u == 0 ? dequant8(ra[i].x, ra[i].y, e8m0_byte(wa, i)) : dequant8(ra[i].z, ra[i].w, e8m0_byte(wa, i));
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          fb[j] = u == 0 ? dequant8(rb[j].x, rb[j].y, e8m0_byte(wb, j)) : dequant8(rb[j].z, rb[j].w, e8m0_byte(wb, j));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  };
+
+  // Step s: wait for this wave's own transfers of step s (eight a step;
+  // those of step s + 1 may stay in flight), barrier, start step s + 2 into
+  // the slot of step s - 1, multiply step s.
+  issue(0);
+  if (nk > 1) issue(1);
+  for (int step = 0; step < nk; ++step) {
+    if (step + 1 < nk) dma::wait_vmcnt<8>(); else dma::wait_vmcnt<0>();
+    __syncthreads();
+    if (step + 2 < nk) issue(step + 2);
+    step_mfma(step);
+  }
+
+  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 128) * g.np + pn0 + wn * 64 + r32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
+      }
+}
+
+// ---------------------------------------------------------------------------
+// Exact-dot large-tile sub-products with fp32 amax/448 scales (blocks 16, 32
+// and 128).
+//
+// fp32 scales are arbitrary numbers, which neither the scaled fp8 MFMA nor
+// the scaled conversions can apply, and the fp8 matrix cores' dot product is
+// narrower than fp32; so each block's partial sum of code products is formed
+// exactly on the bf16 matrix cores (e4m3 -> bf16 is exact, products of two
+// codes are exact in fp32) and promoted into the fp32 accumulator as
+// acc += (sA sB) partial.  Per block and output that is two
 // VALU operations against `block` multiply-adds on the matrix cores, so at
 // blocks 16 and 32 the promotes, not the matrix cores, bound the kernel.
 //
@@ -242,9 +419,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 // workgroup per CU.  The codes arrive through a 64-byte-step LDS ring like the
 // fp8 kernel's (four slots here, two steps ahead); each slot also holds the
 // step's scales: NB = max(1, 64 / block) K blocks of the 256 A rows and
-// max(2, NB) of the 128 B rows (block 128: the step's one block, repeated).
-// Scales are stored as the layout defines them: fp32 in row order, E8M0 bytes
-// with the rows of each 256-row tile permuted.
+// max(2, NB) of the 128 B rows (block 128: the step's one block, repeated),
+// fp32 in row order.
 //
 // Each instruction's 16 contracted positions lie in one block, the same
 // positions on both operands, so every partial sum is over exactly one block.
@@ -256,8 +432,9 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 namespace ex {
 constexpr int kThreadsX = 512;
 constexpr int kSlotsX = 4;                       // two in flight, the current one, the previous one
-template <int BS, int SB>
+template <int BS>
 struct Geo {
+  static constexpr int SB = 4;                            // fp32 scale bytes
   static constexpr int NB = BS >= 64 ? 1 : 64 / BS;       // K blocks per step
   static constexpr int NBB = NB < 2 ? 2 : NB;             // B scale blocks held per slot
   static constexpr int kScaleA = NB * TM * SB;
@@ -281,12 +458,10 @@ __device__ __forceinline__ v8bfx codes8_to_bf16(uint32_t lo, uint32_t hi) {
   return r;
 }
 
-// the value of a stored E8M0 byte (e + 127; e >= -126 for every scale the rules produce)
-__device__ __forceinline__ float e8m0_value(uint32_t byte) { return __uint_as_float(byte << 23); }
-
-template <int BS, int SB>
+template <int BS>
 __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(SplitArgs g) {
-  using G = ex::Geo<BS, SB>;
+  using G = ex::Geo<BS>;
+  constexpr int SB = G::SB;
   constexpr int NB = G::NB;
   __shared__ uint4 lds_raw[ex::kSlotsX * G::kSlot / 16];
   const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
@@ -314,7 +489,7 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
     csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
     cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
   }
-  // one scale transfer per wave and step (fp32: 16 bytes a lane, E8M0: 4):
+  // one scale transfer per wave and step (16 bytes a lane):
   //   waves 0..3: the 256 A rows of K block NB step + (wave mod NB) (block
   //               128: of block step / 2; the extra waves repeat a transfer)
   //   waves 4..7: the 128 B rows of K blocks NB step + 2 p + h into lane half
@@ -326,7 +501,7 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
   const uint8_t *sbase = (s_is_a ? g.sat + (bt * g.T + r) * g.kblocks * g.mp * SB + pm0 * SB
                                  : g.sbt + (bt * g.T + r) * g.kblocks * g.np * SB + pn0 * SB);
   const int64_t splane = srows * SB;                   // bytes per K block
-  const uint32_t s_off = (uint32_t)(SB == 4 ? 16 : 4) * (uint32_t)(s_is_a ? lane : r32);
+  const uint32_t s_off = 16u * (uint32_t)(s_is_a ? lane : r32);
   const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_a ? sblk * TM * SB : G::kScaleA + sblk * TN * SB));
 
   auto issue = [&](int step) {
@@ -337,10 +512,7 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
     const int64_t kb = BS >= 64 ? step / 2 : (int64_t)NB * step + sblk;
     // B lanes of half h read the next block (blocks 16, 32)
     const uint32_t hoff = (!s_is_a && BS < 64) ? (uint32_t)(h * splane) : 0u;
-    if (SB == 4)
-      dma::copy16(s_off + hoff, sbase + kb * splane, m0 + sdst);
-    else
-      dma::copy4(s_off + hoff, sbase + kb * splane, m0 + sdst);
+    dma::copy16(s_off + hoff, sbase + kb * splane, m0 + sdst);
   };
 
   v16f acc[2][2], part[2][2];
@@ -362,29 +534,14 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
     // sB of the lane's column in column tile j
     float sbv[2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (SB == 4)
-        sbv[j] = reinterpret_cast<const float *>(sb)[wn * 64 + 32 * j + r32];
-      else   // tile-half row 64 wn + 32 j + r32 at byte 4 r32 + 2 wn + j
-        sbv[j] = e8m0_value(sb[4 * r32 + 2 * wn + j]);
-    }
+    for (int j = 0; j < 2; ++j) sbv[j] = reinterpret_cast<const float *>(sb)[wn * 64 + 32 * j + r32];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         // rows 64 wm + 32 i + 8 q + 4 h + u, u = 0..3: registers 4 q + u
-        float sav[4];
-        if (SB == 4) {
-          const float4 sa4 = *reinterpret_cast<const float4 *>(sa + 4 * (wm * 64 + 32 * i + 8 * q + 4 * h));
-          sav[0] = sa4.x; sav[1] = sa4.y; sav[2] = sa4.z; sav[3] = sa4.w;
-        } else {
-          // tile row 128 H + 32 I + J at byte 4 (32 H + J) + I: here H = wm / 2,
-          // I = (2 wm + i) mod 4, J = 8 q + 4 h + u: byte I of four consecutive words
-          const uint4 w4 = *reinterpret_cast<const uint4 *>(sa + 128 * (wm >> 1) + 32 * q + 16 * h);
-          const int sh = 8 * ((2 * wm + i) & 3);
-          sav[0] = e8m0_value((w4.x >> sh) & 0xffu); sav[1] = e8m0_value((w4.y >> sh) & 0xffu);
-          sav[2] = e8m0_value((w4.z >> sh) & 0xffu); sav[3] = e8m0_value((w4.w >> sh) & 0xffu);
-        }
+        const float4 sa4 = *reinterpret_cast<const float4 *>(sa + 4 * (wm * 64 + 32 * i + 8 * q + 4 * h));
+        const float sav[4] = {sa4.x, sa4.y, sa4.z, sa4.w};
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -622,15 +779,16 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
   g.tiles_n = (int)(pb.np / TN);
   const int64_t items = pb.batch * pb.T * g.tiles_m * g.tiles_n;
   if (exact_split(pb)) {
-    const dim3 grid((unsigned)items), block(ex::kThreadsX);
     if (pb.scale_bytes == 4) {
-      if (pb.block == 16) hipLaunchKernelGGL((gemm_exact256x128_kernel<16, 4>), grid, block, 0, st, g);
-      else if (pb.block == 32) hipLaunchKernelGGL((gemm_exact256x128_kernel<32, 4>), grid, block, 0, st, g);
-      else hipLaunchKernelGGL((gemm_exact256x128_kernel<128, 4>), grid, block, 0, st, g);
+      const dim3 grid((unsigned)items), block(ex::kThreadsX);
+      if (pb.block == 16) hipLaunchKernelGGL(gemm_exact256x128_kernel<16>, grid, block, 0, st, g);
+      else if (pb.block == 32) hipLaunchKernelGGL(gemm_exact256x128_kernel<32>, grid, block, 0, st, g);
+      else hipLaunchKernelGGL(gemm_exact256x128_kernel<128>, grid, block, 0, st, g);
     } else {
-      if (pb.block == 16) hipLaunchKernelGGL((gemm_exact256x128_kernel<16, 1>), grid, block, 0, st, g);
-      else if (pb.block == 32) hipLaunchKernelGGL((gemm_exact256x128_kernel<32, 1>), grid, block, 0, st, g);
-      else hipLaunchKernelGGL((gemm_exact256x128_kernel<128, 1>), grid, block, 0, st, g);
+      const dim3 grid((unsigned)items), block(kThreads);
+      if (pb.block == 16) hipLaunchKernelGGL(gemm_dq256x128_kernel<16>, grid, block, 0, st, g);
+      else if (pb.block == 32) hipLaunchKernelGGL(gemm_dq256x128_kernel<32>, grid, block, 0, st, g);
+      else hipLaunchKernelGGL(gemm_dq256x128_kernel<128>, grid, block, 0, st, g);
     }
     return hipGetLastError();
   }

@@ -98,25 +98,30 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
   pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
   pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
-  const bool mx = !pb.exact_dot && pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
   // large-tile path: one or two levels, 256-row tiles, whole 64-byte (blocks
   // 16, 32) or 128-byte (block 128) K steps; E8M0 scales at blocks 32 and 128
-  // on the fp8 matrix cores, the exact-dot plans (fp32 scales, block 16, the
-  // flag) on the exact kernel.  It writes every P_r (4 bytes per output of
-  // each term) and reads it back, 8 / k' bytes per flop against the fused
-  // path's none: the fp8 plans take it by default where that round trip
-  // costs less than the fused path's smaller tiles, k' >= 1024 (measured:
-  // the large tiles win at 1024, lose at 512 and below); the exact-dot plans
-  // whenever the shape allows (the fused exact-dot kernel is slower at every
-  // measured k').
+  // on the fp8 matrix cores or (exact-dot flag) the folded-scale bf16 kernel,
+  // fp32 scales and block 16 on the promote kernel.  It writes every P_r (4
+  // bytes per output of each term) and reads it back, 8 / k' bytes per flop
+  // against the fused path's none: plans with a fused kernel take it by
+  // default where that round trip costs less than the fused path's smaller
+  // tiles, k' >= 1024 (measured on both forms: the large tiles win at 1024
+  // and above, lose at 512 and below); fp32 scales and block 16 whenever the
+  // shape allows (their fused promote kernel is slower at every measured k').
   const bool split_shape = q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
              pb.kp > 0 && pb.kp % (q.block == 128 ? 128 : 64) == 0 && pb.kp < (int64_t(1) << 26) &&
              q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);
+  // E8M0 scales at blocks 32 and 128 have a fused 128 x 128 kernel on either
+  // path (the fp8 matrix cores, or the exact-dot flag's folded-scale form);
+  // fp32 scales and block 16 only the large-tile exact-dot kernels
+  const bool fused_exists = pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
   pb.split = split_shape &&
-             (fmm::exact_split(pb) || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
-  // fused 128 x 128 path: E8M0 scales, whole 128-row tiles and 128-byte K steps
-  const bool tile128 = mx && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 && pb.kp % 128 == 0 &&
-                       pb.kp < (int64_t(1) << 26);
+             (!fused_exists || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
+  // fused 128 x 128 path: E8M0 scales at blocks 32 and 128 (the fp8 matrix
+  // cores, or the exact-dot flag's folded-scale bf16 form), whole 128-row
+  // tiles and 128-byte K steps
+  const bool tile128 = fused_exists && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 &&
+                       pb.kp % 128 == 0 && pb.kp < (int64_t(1) << 26);
   pb.layout = pb.split ? FMM_LAYOUT_TILE256x64 : tile128 ? FMM_LAYOUT_TILE128x128 : FMM_LAYOUT_ROWS;
 
   // workspace layout

@@ -15,11 +15,12 @@ Bars (element by element):
   A wrong or missing term moves an element by about |P_r| ~ S / sqrt(k'), far
   outside either bound at every tested size;
 * C, the stated tolerance: max |C_gpu - C_oracle| / |C_oracle|_F <= 1e-5.  The
-  exact-dot path meets it everywhere.  The fp8 path meets it on the Gaussian
-  and uniform families; where heavy tails, row scales over four decades,
-  general basis changes or a 2 x 2 output make the group truncation above
-  exceed it (by at most 2x), the case passes ns=False and has an exact-dot
-  twin that asserts it;
+  exact-dot path meets it everywhere and every exact-dot case asserts it.  The
+  fp8 path meets it on the Gaussian and uniform families; on heavy tails, row
+  scales over four decades, general basis changes or a 2 x 2 output the group
+  truncation above exceeds it (measured up to 2.9e-4 |C|_F, on random GL(2)^3
+  basis changes of Strassen: 29x the bar).  Such fp8 cases pass ns=False and
+  always run beside an exact-dot twin on the same inputs that asserts it;
 * relative MSE against the fp64 product: within 1% of the oracle's (ratio of
   sums over the batch), with the GPU's own reference product and reduction;
 * the GPU fp64 reference product against numpy's binary64 A B: 1e-12 relative.
@@ -171,3 +172,74 @@ def oracle_rows(M, table, depth, bs, rule, side, rows):
         c, st, _, dq = e4m3.quantize_rows(x, bs, rule)
         codes.append(c); scales.append(st); deqs.append(dq)
     return np.stack(codes), np.stack(scales), np.stack(deqs)
+
+
+def sampled_parity(spec, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nrows, rng,
+                   exact=False, b_rows=1, b_bf16=False):
+    """The oracle on sampled rows of a full-size GPU run (quantization runs
+    along the contracted axis, so a row's codes depend on that row alone):
+    for each batch element in ``bsel``, ``nrows`` random rows of A's and of
+    B's sub-block grids give, through the oracle's own split / combine /
+    quantize, the codes, scales and dequantized rows of every term, hence
+    every element of C at the sampled (row, column) positions of every output
+    block.  Returns a dict of what was found (no assertion):
+    codes_scales_identical, within_dot_bound, ref_ok, max_rel_fro (over the
+    sampled entries, against |C_oracle|_F estimated by the fp64 reference's
+    norm), rel_mse_gpu / rel_mse_oracle over the sampled entries, and
+    per-element details of the first failure."""
+    D = oracle_realization(spec)
+    U, V, W = R.tables_f32(D, depth)
+    T = U.shape[0]
+    n = 2 ** depth
+    batch, M, K = A.shape
+    N = B.shape[2]
+    mp, kp, np_ = M // n, K // n, N // n
+    mx = uses_mx(bs, rule, exact)
+    g_dot = 2.0 ** -10 if mx else 2.0 ** -19
+    ac, asc, bc, bsc = f.operands()
+    res = {"codes_scales_identical": True, "within_dot_bound": True, "ref_ok": True,
+           "max_rel_fro": 0.0, "elements": 0, "batch_elements": [int(b) for b in bsel], "rows": nrows}
+    kept = {"gpu": [], "orc": [], "ref": []}
+    w64 = W.astype(np.float64)
+    for b in bsel:
+        prow = np.sort(rng.choice(mp, size=min(nrows, mp), replace=False))
+        qrow = np.sort(rng.choice(np_, size=min(nrows, np_), replace=False))
+        xc, xs, xd = oracle_rows(A[b], U, depth, bs, rule, "A", prow)
+        yc, ys, yd = oracle_rows(B[b], V, depth, bs, rule, "B", qrow)
+        gs_a = asc[b][:, prow, :].cpu().numpy()
+        gs_b = bsc[b][:, qrow, :].cpu().numpy()
+        if rule == e4m3.RULE_FP32_AMAX:
+            gs_a, gs_b, xs, ys = (v.view(np.uint32) for v in (gs_a, gs_b, xs, ys))
+        same = (np.array_equal(ac[b][:, prow, :].cpu().numpy(), xc)
+                and np.array_equal(bc[b][:, qrow, :].cpu().numpy(), yc)
+                and np.array_equal(gs_a, xs) and np.array_equal(gs_b, ys))
+        res["codes_scales_identical"] &= bool(same)
+        P = np.einsum("rpl,rql->rpq", xd, yd)
+        S = np.einsum("rpl,rql->rpq", np.abs(xd), np.abs(yd))
+        Cb = C[b].cpu().numpy().astype(np.float64)
+        Rb = Cref[b].cpu().numpy()
+        fro = float(np.sqrt(ref2[b]))
+        for I in range(n):
+            for Kb in range(n):
+                col = w64[:, Kb * n + I]
+                Co = np.tensordot(col, P, axes=(0, 0))
+                Sb = np.tensordot(np.abs(col), S, axes=(0, 0))
+                rows_g, cols_g = I * mp + prow, Kb * np_ + qrow
+                Cg = Cb[np.ix_(rows_g, cols_g)]
+                diff = np.abs(Cg - Co)
+                bound = (g_dot + (kp + T + 8) * 2.0 ** -24) * Sb
+                res["within_dot_bound"] &= bool(np.all(diff <= bound))
+                if fro > 0:
+                    res["max_rel_fro"] = max(res["max_rel_fro"], float(diff.max() / fro))
+                ref = A[b][rows_g, :].astype(np.float64) @ B[b][:, cols_g].astype(np.float64)
+                res["ref_ok"] &= bool(np.allclose(Rb[np.ix_(rows_g, cols_g)], ref, rtol=1e-12,
+                                                  atol=1e-12 * np.abs(ref).max()))
+                kept["gpu"].append(Cg.ravel()); kept["orc"].append(Co.ravel()); kept["ref"].append(ref.ravel())
+                res["elements"] += Cg.size
+    g_, o_, r_ = (np.concatenate(kept[k]) for k in ("gpu", "orc", "ref"))
+    res["rel_mse_gpu_sampled"] = float(np.sum((g_ - r_) ** 2) / np.sum(r_ ** 2))
+    res["rel_mse_oracle_sampled"] = float(np.sum((o_ - r_) ** 2) / np.sum(r_ ** 2))
+    res["rel_mse_agree"] = bool(abs(res["rel_mse_gpu_sampled"] / res["rel_mse_oracle_sampled"] - 1) <= MSE_REL_TOL)
+    res["meets_1e-5"] = res["max_rel_fro"] <= REL_FRO_TOL
+    res["path"] = "fp8" if mx else "exact"
+    return res

@@ -28,7 +28,7 @@ import pytest
 import fmm_inputs as gen
 from oracle import e4m3, fmm
 from oracle import realizations as R
-from tests.gpu_helpers import REL_FRO_TOL, check_case, oracle_rows
+from tests.gpu_helpers import check_case, sampled_parity
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
@@ -48,17 +48,10 @@ def check_sampled(name, family, batch, M, K, N, depth, bs, rule_name, seed, cfg,
     import torch
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
     rule = RULES[rule_name]
-    D = R.builtin_f64(name)
-    U, V, W = R.tables_f32(D, depth)
-    T = U.shape[0]
-    n = 2 ** depth
-    mp, kp, np_ = M // n, K // n, N // n
     log(f"{name} b={batch} {M}x{K}x{N} depth {depth} block {bs} {rule_name}: generating")
     A, B = gen.operands(family, batch, M, K, N, seed=seed, cfg=cfg, trial=trial)
     dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
     f = FMM(name, batch, M, K, N, depth, bs, rule_name, exact_dot=exact)
-    mx = (not exact) and rule != e4m3.RULE_FP32_AMAX and bs in (32, 128)
-    g_dot = 2.0 ** -10 if mx else 2.0 ** -19
     C = f.matmul(dA, dB)
     Cref = reference_f64(dA, dB)
     err2, ref2 = error_stats(C, Cref)
@@ -69,55 +62,17 @@ def check_sampled(name, family, batch, M, K, N, depth, bs, rule_name, seed, cfg,
     assert np.allclose(err2, (d * d).sum(dim=(1, 2)).cpu().numpy(), rtol=1e-10)
     assert np.allclose(ref2, (Cref * Cref).sum(dim=(1, 2)).cpu().numpy(), rtol=1e-10)
     del d
-    ac, asc, bc, bsc = f.operands()
-    rng = np.random.default_rng(1234 + seed)
-    out = {}
-    for b in bsel:
-        prow = np.sort(rng.choice(mp, size=nrows, replace=False))
-        qrow = np.sort(rng.choice(np_, size=nrows, replace=False))
-        xc, xs, xd = oracle_rows(A[b], U, depth, bs, rule, "A", prow)
-        yc, ys, yd = oracle_rows(B[b], V, depth, bs, rule, "B", qrow)
-        assert np.array_equal(ac[b][:, prow, :].cpu().numpy(), xc), "A codes differ"
-        assert np.array_equal(bc[b][:, qrow, :].cpu().numpy(), yc), "B codes differ"
-        gs_a = asc[b][:, prow, :].cpu().numpy()
-        gs_b = bsc[b][:, qrow, :].cpu().numpy()
-        if rule == e4m3.RULE_FP32_AMAX:
-            gs_a, gs_b, xs, ys = (v.view(np.uint32) for v in (gs_a, gs_b, xs, ys))
-        assert np.array_equal(gs_a, xs), "A scales differ"
-        assert np.array_equal(gs_b, ys), "B scales differ"
-        # C at every (I p, K q) of the sampled rows and columns
-        P = np.einsum("rpl,rql->rpq", xd, yd)                    # binary64, T x s x s
-        S = np.einsum("rpl,rql->rpq", np.abs(xd), np.abs(yd))
-        w64 = W.astype(np.float64)
-        Cb = C[b].cpu().numpy().astype(np.float64)
-        Rb = Cref[b].cpu().numpy()
-        fro = float(np.sqrt(ref2[b]))
-        kept = {"gpu": [], "orc": [], "ref": []}
-        worst = 0.0
-        for I in range(n):
-            for Kb in range(n):
-                col = w64[:, Kb * n + I]
-                Co = np.tensordot(col, P, axes=(0, 0))
-                Sb = np.tensordot(np.abs(col), S, axes=(0, 0))
-                rows_g, cols_g = I * mp + prow, Kb * np_ + qrow
-                Cg = Cb[np.ix_(rows_g, cols_g)]
-                diff = np.abs(Cg - Co)
-                bound = (g_dot + (kp + T + 8) * 2.0 ** -24) * Sb
-                assert np.all(diff <= bound), f"{int((diff > bound).sum())} beyond the bound"
-                worst = max(worst, diff.max() / fro)
-                ref = A[b][rows_g, :].astype(np.float64) @ B[b][:, cols_g].astype(np.float64)
-                assert np.allclose(Rb[np.ix_(rows_g, cols_g)], ref, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
-                kept["gpu"].append(Cg); kept["orc"].append(Co); kept["ref"].append(ref)
-        if ns or not mx:
-            assert worst <= REL_FRO_TOL, worst
-        g_, o_, r_ = (np.concatenate([v.ravel() for v in kept[k]]) for k in ("gpu", "orc", "ref"))
-        rel_g = np.sum((g_ - r_) ** 2) / np.sum(r_ ** 2)
-        rel_o = np.sum((o_ - r_) ** 2) / np.sum(r_ ** 2)
-        assert abs(rel_g / rel_o - 1) <= 0.01, (rel_g, rel_o)
-        out[b] = {"max_rel_fro": worst, "sampled_rel_mse_gpu": rel_g, "sampled_rel_mse_oracle": rel_o}
-        log(f"batch element {b}: {out[b]}")
-    out["rel_mse_gpu"] = float(err2.sum() / ref2.sum())
-    return out
+    r = sampled_parity(name, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nrows,
+                       np.random.default_rng(1234 + seed), exact=exact)
+    log(f"sampled: {r}")
+    assert r["codes_scales_identical"], "codes or scales differ"
+    assert r["within_dot_bound"], "elements beyond the dot-product bound"
+    assert r["ref_ok"], "fp64 reference differs from numpy's"
+    assert r["rel_mse_agree"], (r["rel_mse_gpu_sampled"], r["rel_mse_oracle_sampled"])
+    if ns or r["path"] == "exact":
+        assert r["meets_1e-5"], r["max_rel_fro"]
+    r["rel_mse_gpu"] = float(err2.sum() / ref2.sum())
+    return r
 
 
 def test_headline_8192_depth1_tstar_full():
@@ -152,3 +107,13 @@ def test_batch1024_512_cube_sampled(bs, exact):
 def test_16384x8192x16384_rowscaled_sampled(depth, exact):
     check_sampled("tstar", "rowscaled", 1, 16384, 8192, 16384, depth, 32, "pow2_ceil", seed=0, cfg=5,
                   bsel=[0], nrows=8, exact=exact, ns=False)
+
+
+@pytest.mark.parametrize("exact", [False, True])
+def test_headline_heavy_tailed_sampled(exact):
+    """The headline workload on the heavy-tailed repeat (Student-t, 3 degrees
+    of freedom, unit variance): the fp8 path (1e-5 bar not asserted: its
+    group truncation) and the exact-dot twin (bar asserted)."""
+    r = check_sampled("tstar", "student_t3", 1, 8192, 8192, 8192, 1, 32, "pow2_ceil", seed=0, cfg=0,
+                      bsel=[0], nrows=12, exact=exact, ns=False)
+    log(f"8192^3 student_t3 exact={exact}: max_rel_fro {r['max_rel_fro']:.3e}")

@@ -130,6 +130,11 @@ def test_weight_deployment_granularity(case):
     r = check_case("tstar", "student_t3", b, M, K, N, 1, bs, rule, seed=3, cfg=9,
                    b_rows=b_rows, b_bf16=bf16, ns=False, flags=FMM_FLAG_LARGE_TILE)
     print(case, r, flush=True)
+    if r["path"] == "fp8":
+        # the exact-dot twin asserts the 1e-5 |C|_F bar on the same case
+        r = check_case("tstar", "student_t3", b, M, K, N, 1, bs, rule, seed=3, cfg=9,
+                       b_rows=b_rows, b_bf16=bf16, exact=True, flags=FMM_FLAG_LARGE_TILE)
+        print(case, "exact", r, flush=True)
 
 
 @pytest.mark.parametrize("depth,flags", [(1, 0), (1, 8), (2, 0), (2, 8), (3, 0)])
@@ -141,9 +146,10 @@ def test_term_without_coefficients(depth, flags):
     U[4, :] = 0.0
     n = 2 ** depth
     M = K = N = 256 * n if flags else 32 * n
-    r = check_case(("unchecked", (U, V, W)), "gaussian", 1, M, K, N, depth, 32, 1, seed=21, cfg=7,
-                   flags=flags, ns=False)
-    print(depth, flags, r, flush=True)
+    for exact in (False, True):
+        r = check_case(("unchecked", (U, V, W)), "gaussian", 1, M, K, N, depth, 32, 1, seed=21, cfg=7,
+                       flags=flags, exact=exact, ns=exact)
+        print(depth, flags, r, flush=True)
 
 
 def test_rowscaled_family():
@@ -298,15 +304,20 @@ def test_large_tile_split_path(case):
     ("tstar", 1, 512, 640, 1536, 1, 32, 1, True),       # five k-steps, 1 x 3 tiles
     ("strassen", 1, 1024, 1024, 1024, 2, 128, 1, True), # depth 2, the flag, block 128
     ("winograd", 2, 1024, 256, 1024, 2, 32, 0, False),  # depth 2, fp32 scales, batch of two, one k-step
+    ("cubic8", 2, 1024, 512, 1024, 1, 32, 1, True),     # E8M0, eight terms, 2 x 2 tiles, eight k-steps, batch
+    ("tstar", 1, 1024, 512, 1024, 2, 32, 2, True),      # E8M0 depth 2, OCP, the flag
+    ("strassen", 1, 512, 1536, 512, 1, 16, 2, False),   # block 16 E8M0, twelve k-steps
 ])
 def test_exact_large_tile_path(case):
-    """The exact-dot large-tile kernel (bf16 matrix cores on exactly
-    converted codes, one promote per block and output) at every block size,
-    with fp32 and E8M0 scales, at its default choice (exact-dot plans take the
-    large tiles whenever the shape allows)."""
+    """The exact-dot large-tile kernels at every block size (fp32 scales and
+    block 16 take them whenever the shape allows; E8M0 scales at blocks 32
+    and 128 from k' = 1024 on or with FMM_FLAG_LARGE_TILE, as here):
+    fp32 scales on the promote kernel (bf16 matrix cores on exactly converted
+    codes, one promote per block and output), E8M0 scales on the kernel that
+    folds each block's power of two into the codes' conversion."""
     name, b, M, K, N, depth, bs, rule, exact = case
     r = check_case(name, "student_t3", b, M, K, N, depth, bs, rule, seed=18, cfg=10, exact=exact,
-                   layout=FMM_LAYOUT_TILE256x64)
+                   flags=FMM_FLAG_LARGE_TILE, layout=FMM_LAYOUT_TILE256x64)
     print(case, r, flush=True)
 
 
@@ -320,8 +331,7 @@ def test_default_path_choice(case):
     """Without FMM_FLAG_LARGE_TILE the large-tile path is taken from
     k' = 1024 on; both choices meet the parity bars."""
     name, b, M, K, N, depth, layout = case
-    r = check_case(name, "gaussian", b, M, K, N, depth, 32, 1, seed=17, cfg=10, layout=layout,
-                   ns=False)
+    r = check_case(name, "gaussian", b, M, K, N, depth, 32, 1, seed=17, cfg=10, layout=layout)
     print(case, r, flush=True)
 
 
@@ -386,3 +396,54 @@ def test_fused_and_large_tile_paths_agree_on_a_large_batch():
     torch.cuda.synchronize()
     assert not torch.isnan(C1).any()
     assert torch.equal(C1, C2)
+
+
+@pytest.mark.parametrize("case", [
+    # (spec, family, batch, M, K, N, depth, block, rule): the input families on
+    # which the fp8 matrix cores' group truncation exceeds 1e-5 |C|_F, on the
+    # large tiles the benchmark configurations take
+    ("tstar", "rowscaled", 1, 1024, 1024, 1024, 1, 32, 1),
+    ("tstar", "rowscaled", 1, 1024, 1024, 1024, 2, 32, 1),
+    ("strassen", "student_t3", 4, 512, 512, 512, 1, 16, 1),
+    ("strassen", "student_t3", 4, 512, 512, 512, 1, 128, 1),
+    ("tstar", "student_t3", 2, 1024, 512, 1024, 1, 32, 2),
+])
+def test_dq_large_tile_heavy_inputs(case):
+    """The folded-scale exact kernel on heavy-tailed and row-scaled operands:
+    codes and scales bit-exact, C within 1e-5 |C|_F, relMSE within 1%."""
+    spec, fam, b, M, K, N, depth, bs, rule = case
+    r = check_case(spec, fam, b, M, K, N, depth, bs, rule, seed=31, cfg=11, exact=True,
+                   flags=FMM_FLAG_LARGE_TILE, layout=FMM_LAYOUT_TILE256x64)
+    print(case, r, flush=True)
+
+
+def test_dq_basis_changes():
+    """Random GL(2)^3 basis changes of Strassen (the batched sweep's arms) on
+    the folded-scale exact kernels, large tiles and fused 128 x 128, where the
+    fp8 path's C is furthest from the oracle's: every element within
+    1e-5 |C|_F."""
+    for i, g in enumerate(gen.basis_changes(3, seed=5)):
+        for flags, layout in ((FMM_FLAG_LARGE_TILE, FMM_LAYOUT_TILE256x64), (0, FMM_LAYOUT_TILE128x128)):
+            r = check_case(("strassen", g), "student_t3", 4, 512, 512, 512, 1, 32, 1, seed=9, cfg=4,
+                           trial=i, exact=True, flags=flags, layout=layout)
+            print(i, layout, r, flush=True)
+
+
+@pytest.mark.parametrize("case", [
+    # (spec, family, batch, M, K, N, depth, block, rule): tile-aligned shapes
+    # off the large tiles, exact-dot plans with E8M0 scales
+    ("tstar", "gaussian", 1, 256, 256, 256, 1, 32, 1),         # one tile, two k-steps
+    ("strassen", "student_t3", 2, 768, 1024, 512, 1, 128, 2),  # block 128, OCP, batch, 3 x 2 tiles
+    ("tstar", "rowscaled", 1, 1024, 1024, 512, 2, 32, 1),      # depth 2, outer combine
+    ("cubic8", "gaussian", 1, 1536, 2048, 1536, 2, 128, 1),    # depth 2, 64 terms, block 128
+    ("tstar", "rowscaled", 1, 1024, 2048, 1024, 3, 32, 1),     # depth 3, 343 terms
+    ("winograd", "student_t3", 16, 256, 256, 256, 1, 32, 1),   # a batch of small products
+])
+def test_dq_fused_path(case):
+    """The fused 128 x 128 kernel in its exact-dot form (each block's power
+    of two folded into the codes' conversion to bf16; W-combine quadrants in
+    registers): codes and scales bit-exact, C within 1e-5 |C|_F, relMSE."""
+    spec, fam, b, M, K, N, depth, bs, rule = case
+    r = check_case(spec, fam, b, M, K, N, depth, bs, rule, seed=41, cfg=12, exact=True,
+                   layout=FMM_LAYOUT_TILE128x128)
+    print(case, r, flush=True)
