@@ -14,8 +14,26 @@ from . import (FMM_LAYOUT_TILE128x128, FMM_LAYOUT_TILE256x64, Realization, fmm_c
                fmm_plan_workspace_size, fmm_realization_builtin, fmm_reference_f64, make_desc)
 
 
+def _require(x, name, shape, dtype, device):
+    """Raise ValueError unless x is a contiguous torch tensor of exactly this
+    shape and dtype on this device: the kernels index with the plan's sizes,
+    so any other buffer would be read or written out of bounds."""
+    if not isinstance(x, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(x).__name__}")
+    if x.dtype != dtype:
+        raise ValueError(f"{name}: dtype {x.dtype}, expected {dtype}")
+    if tuple(x.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(x.shape)}, expected {tuple(shape)}")
+    if not x.is_contiguous():
+        raise ValueError(f"{name}: not contiguous")
+    if x.device != device:
+        raise ValueError(f"{name}: on {x.device}, expected {device}")
+
+
 class FMM:
-    """One planned product shape on one device, with its own workspace."""
+    """One planned product shape on one device, with its own workspace.
+    Every call checks its tensors (float32, contiguous, on the plan's device,
+    exactly the plan's shapes) before anything reaches the library."""
 
     def __init__(self, realization, batch, M, K, N, depth=1, block=32, rule="pow2_ceil",
                  device="cuda:0", exact_dot=False, flags=0):
@@ -23,6 +41,8 @@ class FMM:
             realization = fmm_realization_builtin(realization)
         self.real = realization
         self.device = torch.device(device)
+        if self.device.type == "cuda" and self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
         self.shape = (int(batch), int(M), int(K), int(N))
         self.depth, self.block = int(depth), int(block)
         with torch.cuda.device(self.device):
@@ -33,33 +53,42 @@ class FMM:
             self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         self.scale_bytes = 4 if (rule in ("fp32_amax", 0)) else 1
 
-    def matmul(self, A, B, C=None, stream=None):
+    def _inputs(self, A, B):
+        b, M, K, N = self.shape
+        _require(A, "A", (b, M, K), torch.float32, self.device)
+        _require(B, "B", (b, K, N), torch.float32, self.device)
+
+    def _output(self, C):
         b, M, K, N = self.shape
         if C is None:
-            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+            return torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        _require(C, "C", (b, M, N), torch.float32, self.device)
+        return C
+
+    def matmul(self, A, B, C=None, stream=None):
+        self._inputs(A, B)
+        C = self._output(C)
         fmm_matmul(self.plan, A, B, C, self.ws, stream)
         return C
 
     def encode(self, A, B, stream=None):
+        self._inputs(A, B)
         fmm_encode(self.plan, A, B, self.ws, stream)
 
     def multiply(self, C=None, stream=None):
-        b, M, K, N = self.shape
-        if C is None:
-            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        C = self._output(C)
         fmm_multiply(self.plan, self.ws, C, stream)
         return C
 
     def products(self, C=None, stream=None):
         """First half of multiply (the sub-products); returns C, which it may or may not have written."""
-        b, M, K, N = self.shape
-        if C is None:
-            C = torch.empty((b, M, N), dtype=torch.float32, device=self.device)
+        C = self._output(C)
         fmm_products(self.plan, self.ws, C, stream)
         return C
 
     def combine(self, C, stream=None):
         """Second half of multiply (the rest of the W-combine); writes C."""
+        C = self._output(C)
         fmm_combine(self.plan, self.ws, C, stream)
         return C
 
@@ -67,6 +96,7 @@ class FMM:
         """Operand-side rounding energy of the encoding in the workspace (call
         after encode with the same A, B): numpy [batch][2 sides][T][2] of
         (sum (xhat - x)^2, sum x^2) per batch element, side and term."""
+        self._inputs(A, B)
         batch, T = self.shape[0], None
         from . import fmm_realization_terms
         _, T = fmm_realization_terms(self.real, self.depth)
@@ -152,6 +182,8 @@ def _unpermute_scales256(raw, batch, terms, rows, kblocks):
 def reference_f64(A, B, stream=None):
     b, M, K = A.shape
     N = B.shape[2]
+    _require(A, "A", (b, M, K), torch.float32, A.device)
+    _require(B, "B", (b, K, N), torch.float32, A.device)
     Cref = torch.empty((b, M, N), dtype=torch.float64, device=A.device)
     fmm_reference_f64(b, M, K, N, A, B, Cref, stream)
     return Cref
@@ -160,6 +192,8 @@ def reference_f64(A, B, stream=None):
 def error_stats(C, Cref, stream=None):
     """(err2, ref2) per product as numpy float64 arrays (one host sync)."""
     b, M, N = C.shape
+    _require(C, "C", (b, M, N), torch.float32, C.device)
+    _require(Cref, "Cref", (b, M, N), torch.float64, C.device)
     nbytes = fmm_error_stats_scratch_size(b, M, N)
     scratch = torch.empty(max(nbytes, 8), dtype=torch.uint8, device=C.device)
     out = torch.empty((b, 2), dtype=torch.float64, device=C.device)
