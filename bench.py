@@ -2,22 +2,28 @@
 
 One step = encode + quantize both operands, the T fp8 sub-products, the
 W-combine, C written once (fmm_encode, fmm_products, fmm_combine: together
-fmm_matmul); fp32 A and B are resident in HBM before the timed region.  Default workload: 8192^3, one
-level, the Phi-optimal realization T*, e4m3 block 32 along K, power-of-two
-(E8M0) block scales, A and B iid N(0,1) (synthetic, seeded).
+fmm_matmul); fp32 A and B are resident in HBM before the timed region.
+Default workload: 8192^3, one level, the Phi-optimal realization T*, e4m3
+block 32 along K, power-of-two (E8M0) block scales, A and B iid N(0,1)
+(synthetic, seeded).
 
-Prints one JSON line with the effective rate 2MNK / t, the relative RMS error
-of C against the fp64 product (measured after the timed region), the
-roofline of the dominant kernel (the sub-product GEMM, fmm_products, against
-the fp8 dense MFMA peak) with HIP-event times of encode, products and combine
-taken on the launch stream, and the oracle timed on this host's cores on a
+Prints one JSON line with the effective rate 2MNK / t over exactly --steps
+whole steps (after --warmup untimed ones), the relative RMS error of C against
+the fp64 product (measured after the timed region), the roofline of the
+dominant kernel (the sub-products, fmm_products, against the fp8 dense MFMA
+peak) from HIP events on the launch stream, the step's required HBM bytes
+against the HBM peak, the comparison arms timed interleaved in batches (the
+paired protocol of the paper's Table E.7), the records of the run (device,
+versions, sources, seeds), and the oracle timed on this host's cores on a
 bounded sample.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -32,13 +38,14 @@ BF16_DENSE_PEAK_TFLOPS = 2500.0
 HBM_PEAK_GBS = 8000.0
 
 METRIC = "effective fp8 TFLOP/s (2mnk/t) at 8192³ 1-level; relative RMS error vs fp64"
+SEED = 0          # operand streams SeedSequence([SEED, cfg, trial, operand])
 
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__)
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--size", type=int, default=8192, help="M = K = N")
     p.add_argument("--shape", type=int, nargs=3, metavar=("M", "K", "N"),
                    help="a rectangular product instead of --size (the other configurations)")
@@ -49,13 +56,15 @@ def parse():
     p.add_argument("--realization", default="tstar")
     p.add_argument("--family", default="gaussian")
     p.add_argument("--exact-dot", action="store_true")
+    p.add_argument("--large-tile", action="store_true",
+                   help="FMM_FLAG_LARGE_TILE: the 256 x 128 sub-product tiles wherever the shape allows")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-arms", action="store_true",
-                   help="skip the comparison arms (cubic and Strassen realizations, heavy-tailed operands)")
-    p.add_argument("--arm-steps", type=int, default=20)
-    p.add_argument("--cpu-sample", type=int, default=4096,
-                   help="edge of the cubic products the oracle is timed on")
-    p.add_argument("--cpu-trials", type=int, default=6)
+                   help="skip the comparison arms (cubic and Strassen realizations, heavy-tailed "
+                        "operands, the deployment granularity)")
+    p.add_argument("--arm-batches", type=int, default=4,
+                   help="interleaved rounds over the arms (each arm times --arm-steps steps a round)")
+    p.add_argument("--arm-steps", type=int, default=5)
     p.add_argument("--calibrate-copy", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy five times (the known-size "
                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters to bytes)")
@@ -73,101 +82,152 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 5}))
 
 
-def recorded_traffic(kernel, size, args):
-    """HBM bytes per launch of the sub-product kernel from the committed counter
-    summary (profiles/), if it was taken on this workload and on the kernel
-    source as it is now; otherwise None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{size}cube_depth{args.depth}_{args.realization}_pmc.md")
+def source_hash(names=None):
+    """sha256 over the library's HIP/C++ sources and its header (the kernels
+    a measurement or a counter summary belongs to)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_26077_amd", "csrc")
+    if names is None:
+        names = sorted(n for n in os.listdir(csrc) if n.endswith((".hip", ".h", ".cpp")))
+    for name in names:
+        with open(os.path.join(csrc, name), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "fmm8.h"), "rb") as fh:
+        h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_counters(workload_key):
+    """Per-launch HBM bytes (FETCH_SIZE, WRITE_SIZE scaled to bytes) of each
+    kernel of the step from the committed counter summary of this workload,
+    if it was taken on the sources as they are now; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"step_counters_{workload_key}.md")
     if not os.path.exists(path):
         return None
-    fields = {}
+    fields, rows = {}, {}
     with open(path) as fh:
         for l in fh:
             if l.startswith("- ") and ": " in l:
                 k, v = l[2:].split(": ", 1)
                 fields[k.strip()] = v.strip().strip("`")
-    try:
-        if fields.get("kernel source sha256") != kernel_source_hash():
-            return None
-        return float(fields["HBM bytes per launch"])
-    except (KeyError, ValueError):
+            elif l.startswith("| `") and l.count("|") >= 6:
+                c = [x.strip() for x in l.strip().strip("|").split("|")]
+                try:
+                    rows[c[0].strip("`")] = {"role": c[1], "read": float(c[2]) * 1e6, "written": float(c[3]) * 1e6}
+                except ValueError:
+                    pass
+    if fields.get("source sha256") != source_hash() or not rows:
         return None
+    return rows
 
 
-def kernel_source_hash():
-    """sha256 over the HIP sources of the sub-product kernels."""
-    import hashlib
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_26077_amd", "csrc")
-    for name in ("kernels_gemm.hip", "kernels_split.hip", "lds_dma.h", "device.h", "internal.h"):
-        with open(os.path.join(csrc, name), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()
-
-
-def time_arm(f, dA, dB, C, stream, steps, warmup):
-    """Mean and median wall of `steps` whole steps (encode, sub-products,
-    W-combine) from HIP events on the launch stream, after `warmup` steps."""
+def run_meta(dev):
     import torch
-    for _ in range(warmup):
-        f.matmul(dA, dB, C, stream)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    torch.cuda.synchronize()
-    for a, b in ev:
-        a.record(stream)
-        f.matmul(dA, dB, C, stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    t = np.array([a.elapsed_time(b) for a, b in ev])
-    return float(t.mean()), float(np.median(t))
+    props = torch.cuda.get_device_properties(dev)
+    rocm = None
+    for p in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        try:
+            rocm = open(p).read().strip()
+            break
+        except OSError:
+            pass
+    commit = None
+    try:
+        commit = subprocess.run(["git", "-C", ROOT, "rev-parse", "HEAD"], capture_output=True, text=True,
+                                timeout=10).stdout.strip() or None
+    except Exception:
+        pass
+    return {"device": torch.cuda.get_device_name(dev), "gcnArchName": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count, "rocm": rocm, "torch": torch.__version__,
+            "torch_hip": torch.version.hip, "numpy": np.__version__, "python": sys.version.split()[0],
+            "git_commit": commit, "source_sha256": source_hash(),
+            "seeds": {"operands": f"numpy PCG64(SeedSequence([{SEED}, cfg, trial, operand])), "
+                                  "cfg 0 (headline), trial 0; operand 0 = A, 1 = B"}}
 
 
-def other_arms(args, dA, dB, C, stream):
-    """The comparison arms on the same code path and workload size: the cubic
-    (8-product) and Strassen 1969 realizations on the same Gaussian operands,
-    the default realization on heavy-tailed operands (Student-t, 3 degrees
-    of freedom, unit variance), and the default realization under the real
-    kernel's quantization (block 128, 128 x 128 weight blocks with the
-    bfloat16 pre-round; fp32 amax/448 scales, which take the exact-dot
-    sub-product path, and E8M0 scales on the fp8 path).  Each: effective
-    TFLOP/s from the mean event time of whole steps, and the relative RMS
-    error against fp64."""
+def time_steps(f, dA, dB, C, stream, steps):
+    """Per-step event times (ms) of encode, sub-products, combine and the
+    whole step on the launch stream, for `steps` consecutive steps."""
+    import torch
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for s in range(steps):
+        ev[s][0].record(stream)
+        f.encode(dA, dB, stream)
+        ev[s][1].record(stream)
+        f.products(C, stream)
+        ev[s][2].record(stream)
+        f.combine(C, stream)
+        ev[s][3].record(stream)
+    torch.cuda.synchronize()
+    t = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3]),
+                   e[0].elapsed_time(e[3])] for e in ev])
+    return {"encode": t[:, 0], "products": t[:, 1], "combine": t[:, 2], "step": t[:, 3]}
+
+
+def interleaved_arms(args, dA, dB, stream):
+    """The comparison arms on the same code path and workload size, timed
+    interleaved: --arm-batches rounds, each arm --arm-steps steps per round
+    (the paired, interleaved protocol of Table E.7), after 3 warm-up steps
+    each.  Arms: the headline itself; cubic (8 products) and Strassen 1969 on
+    the same Gaussian operands; the default realization on heavy-tailed
+    operands (Student-t, 3 degrees of freedom, unit variance) on the fp8 path
+    and on the exact-dot path; the real kernel's quantization (block 128,
+    128 x 128 weight blocks with the bfloat16 pre-round) with fp32 amax/448
+    scales (exact-dot sub-products) and with E8M0 scales.  Each: effective
+    TFLOP/s from the mean event time of its steps, the sub-products' mean, and
+    the relative RMS error against fp64."""
     import torch
     import fmm_inputs as gen
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
     n = args.size
     mkn = 2.0 * n ** 3
-    out = {}
-    # (realization, family, rule, block, flags, label)
-    arms = [("cubic8", "gaussian", args.rule, args.block, 0, "cubic8/gaussian"),
-            ("strassen", "gaussian", args.rule, args.block, 0, "strassen/gaussian"),
-            (args.realization, "student_t3", args.rule, args.block, 0, f"{args.realization}/student_t3"),
-            # the real kernel's quantization (Appendix E): fp32 amax/448 scales,
-            # 1 x 128 activation groups, 128 x 128 weight blocks, bfloat16 pre-round
-            (args.realization, "gaussian", "fp32_amax", 128, 2 | 4,
+    t3 = None
+    arms = [(args.realization, args.family, args.rule, args.block, 0, False, "headline"),
+            ("cubic8", "gaussian", args.rule, args.block, 0, False, "cubic8/gaussian"),
+            ("strassen", "gaussian", args.rule, args.block, 0, False, "strassen/gaussian"),
+            (args.realization, "student_t3", args.rule, args.block, 0, False,
+             f"{args.realization}/student_t3/fp8"),
+            (args.realization, "student_t3", args.rule, args.block, 0, True,
+             f"{args.realization}/student_t3/exact-dot"),
+            (args.realization, "gaussian", "fp32_amax", 128, 2 | 4, False,
              f"{args.realization}/gaussian/deployment-fp32amax-b128x128-bf16"),
-            (args.realization, "gaussian", "pow2_ceil", 128, 2 | 4,
+            (args.realization, "gaussian", "pow2_ceil", 128, 2 | 4, False,
              f"{args.realization}/gaussian/deployment-e8m0-b128x128-bf16")]
-    for real, family, rule, block, flags, label in arms:
-        if family != args.family:
-            A, B = gen.operands(family, 1, n, n, n, seed=0, cfg=0, trial=0)
-            xa, xb = torch.from_numpy(A).to(dA.device), torch.from_numpy(B).to(dA.device)
-            del A, B
-        else:
+    if args.depth != 1:
+        arms = [a for a in arms if not a[4]]
+    state = []
+    for real, family, rule, block, flags, exact, label in arms:
+        if family == args.family:
             xa, xb = dA, dB
-        if flags and args.depth != 1:
-            continue
-        f = FMM(real, 1, n, n, n, args.depth, block, rule, exact_dot=args.exact_dot, flags=flags)
-        mean_ms, med_ms = time_arm(f, xa, xb, C, stream, args.arm_steps, 5)
-        Cref = reference_f64(xa, xb)
-        err2, ref2 = error_stats(C, Cref)
-        del Cref, f
-        out[label] = {"value": mkn / (mean_ms * 1e-3) / 1e12, "unit": "TFLOP/s",
-                                   "ms_per_step": mean_ms, "median_ms": med_ms,
-                                   "rel_rms_error_vs_fp64": float(np.sqrt(err2.sum() / ref2.sum())),
-                                   "steps": args.arm_steps}
+        else:
+            if t3 is None:
+                A, B = gen.operands(family, 1, n, n, n, seed=SEED, cfg=0, trial=0)
+                t3 = (torch.from_numpy(A).to(dA.device), torch.from_numpy(B).to(dA.device))
+                del A, B
+            xa, xb = t3
+        f = FMM(real, 1, n, n, n, args.depth, block, rule, exact_dot=exact or args.exact_dot, flags=flags)
+        C = torch.empty((1, n, n), dtype=torch.float32, device=dA.device)
+        time_steps(f, xa, xb, C, stream, 3)
+        state.append({"label": label, "f": f, "a": xa, "b": xb, "C": C, "t": []})
+    for _ in range(args.arm_batches):
+        for s in state:
+            s["t"].append(time_steps(s["f"], s["a"], s["b"], s["C"], stream, args.arm_steps))
+    out = {}
+    for s in state:
+        step = np.concatenate([t["step"] for t in s["t"]])
+        prod = np.concatenate([t["products"] for t in s["t"]])
+        Cref = reference_f64(s["a"], s["b"])
+        err2, ref2 = error_stats(s["C"], Cref)
+        del Cref
+        out[s["label"]] = {"value": mkn / (step.mean() * 1e-3) / 1e12, "unit": "TFLOP/s",
+                           "ms_per_step": float(step.mean()), "median_ms": float(np.median(step)),
+                           "products_ms": float(prod.mean()),
+                           "rel_rms_error_vs_fp64": float(np.sqrt(err2.sum() / ref2.sum())),
+                           "steps": int(step.size)}
+        s.clear()
         torch.cuda.empty_cache()
-    return out
+    return {"protocol": f"{args.arm_batches} interleaved rounds x {args.arm_steps} steps per arm, "
+                        "3 warm-up steps each, same seeded operands across arms", "arms": out}
 
 
 def paper_context():
@@ -181,7 +241,7 @@ def paper_context():
     import fmm_inputs as gen
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
     n, trials = 512, 8
-    A, B = gen.operands("uniform", trials, n, n, n, seed=0, cfg=11, trial=0)
+    A, B = gen.operands("uniform", trials, n, n, n, seed=SEED, cfg=11, trial=0)
     dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
     Cref = reference_f64(dA, dB)
     e = {}
@@ -199,36 +259,51 @@ def paper_context():
 
 
 def cpu_baseline(args):
-    """The oracle, unchanged, timed end to end on one bounded sample."""
+    """The oracle, unchanged, timed on this host's cores on a bounded sample
+    of the benchmark configurations: the 100 trials of the 256^3
+    configuration for the cubic and Strassen 1969 realizations, and one trial
+    of the headline workload.  BLAS threads are held to the cores this
+    process may run on."""
+    from threadpoolctl import threadpool_limits
     from oracle import e4m3, fmm
     from oracle import realizations as R
     import fmm_inputs as gen
-    n = args.cpu_sample
-    tabs = R.tables_f32(R.builtin_f64(args.realization), args.depth)
+    cores = len(os.sched_getaffinity(0))
     rule = e4m3.RULES[args.rule]
-    t = 0.0
-    for trial in range(args.cpu_trials):
-        A, B = gen.operands(args.family, 1, n, n, n, seed=0, cfg=90, trial=trial)
+    flop, t = 0.0, 0.0
+    parts = []
+    with threadpool_limits(limits=cores):
+        A, B = gen.operands("gaussian", 100, 256, 256, 256, seed=SEED, cfg=1, trial=0)
+        for name in ("cubic8", "strassen"):
+            tabs = R.tables_f32(R.builtin_f64(name), 1)
+            t0 = time.perf_counter()
+            for b in range(100):
+                fmm.fmm(A[b], B[b], tabs, 1, 32, rule, keep=False)
+            dt = time.perf_counter() - t0
+            t += dt
+            flop += 100 * 2.0 * 256 ** 3
+            parts.append(f"100 x 256^3 {name} {dt:.2f} s")
+        del A, B
+        n = args.size
+        A, B = gen.operands(args.family, 1, n, n, n, seed=SEED, cfg=0, trial=0)
+        tabs = R.tables_f32(R.builtin_f64(args.realization), args.depth)
         t0 = time.perf_counter()
         fmm.fmm(A[0], B[0], tabs, args.depth, args.block, rule, keep=False)
-        t += time.perf_counter() - t0
-    threads = None
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+        dt = time.perf_counter() - t0
+        t += dt
+        flop += 2.0 * n ** 3
+        parts.append(f"1 x {n}^3 {args.realization} depth {args.depth} {dt:.2f} s")
     cpu = ""
     try:
         with open("/proc/cpuinfo") as f:
             cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
     except OSError:
         pass
-    return {"value": args.cpu_trials * 2.0 * n ** 3 / t / 1e12, "unit": "TFLOP/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": f"{args.cpu_trials} x {n}x{n}x{n} products ({args.realization}, depth {args.depth}, block "
-                      f"{args.block}, {args.rule}, {args.family}): numpy fp32 encode + e4m3 codec, "
-                      f"fp64 BLAS sub-products, W-combine; {t:.2f} s wall",
+    return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": "the 100 trials of the 256^3 configuration (N(0,1), block 32, cubic8 and Strassen "
+                      f"1969) and one trial of the headline workload ({args.rule}, block {args.block}): "
+                      "numpy fp32 encode + e4m3 codec, fp64 BLAS sub-products, W-combine; "
+                      + "; ".join(parts),
             "seconds": t, "cpu_model": cpu}
 
 
@@ -238,14 +313,14 @@ def main():
         calibrate_copy()
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (the path has no cross-GPU step); "
-              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        print(f"bench.py measures one GPU: the path has no cross-GPU step and this build runs on a "
+              f"single MI355X (--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
 
     import torch
     import fmm_inputs as gen
-    from paper_2609_26077_amd import (FMM_LAYOUT_TILE256x64, fmm_operand_views,
-                                      fmm_realization_metrics)
+    from paper_2609_26077_amd import (FMM_LAYOUT_TILE256x64, fmm_operand_views, fmm_realization_metrics,
+                                      fmm_realization_terms)
     from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
 
     dev = torch.device("cuda:0")
@@ -255,11 +330,13 @@ def main():
     # the comparison arms, the paper context and the oracle baseline go with
     # the headline shape (one cubic product)
     headline = args.shape is None and nb == 1
-    A, B = gen.operands(args.family, nb, M, K, N, seed=0, cfg=0, trial=0)
+    A, B = gen.operands(args.family, nb, M, K, N, seed=SEED, cfg=0, trial=0)
     dA = torch.from_numpy(A).to(dev)
     dB = torch.from_numpy(B).to(dev)
     del A, B
-    f = FMM(args.realization, nb, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot)
+    from paper_2609_26077_amd import FMM_FLAG_LARGE_TILE
+    f = FMM(args.realization, nb, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot,
+            flags=FMM_FLAG_LARGE_TILE if args.large_tile else 0)
     C = torch.empty((nb, M, N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
@@ -267,25 +344,13 @@ def main():
         f.matmul(dA, dB, C, stream)
     torch.cuda.synchronize(dev)
 
-    # timed region: K whole steps, events around each launch on the launch stream
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize(dev)
+    # timed region: exactly --steps whole steps, bracketed by synchronizations;
+    # events around each launch on the launch stream
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        ev[s][0].record(stream)
-        f.encode(dA, dB, stream)
-        ev[s][1].record(stream)
-        f.products(C, stream)
-        ev[s][2].record(stream)
-        f.combine(C, stream)
-        ev[s][3].record(stream)
-    torch.cuda.synchronize(dev)
+    ev = time_steps(f, dA, dB, C, stream, args.steps)      # ends with a synchronize
     wall = time.perf_counter() - t0
-    step_ms = np.array([e[0].elapsed_time(e[3]) for e in ev])
-    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    prod_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    comb_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
     ms_per_step = wall * 1e3 / args.steps
+    enc_ms, prod_ms, comb_ms = (float(ev[k].mean()) for k in ("encode", "products", "combine"))
 
     # error of the last step's C against the fp64 product (not timed)
     Cref = reference_f64(dA, dB)
@@ -293,10 +358,8 @@ def main():
     rel_mse = float(err2.sum() / ref2.sum())
     del Cref
 
-    real = f.real
-    from paper_2609_26077_amd import fmm_realization_terms
-    R_, T = fmm_realization_terms(real, args.depth)
-    phi = fmm_realization_metrics(real, args.depth)["phi"]
+    R_, T = fmm_realization_terms(f.real, args.depth)
+    phi = fmm_realization_metrics(f.real, args.depth)["phi"]
     a_view, _ = fmm_operand_views(f.plan, f.ws)
     split = a_view.code_layout == FMM_LAYOUT_TILE256x64
     mkn = 2.0 * nb * M * N * K
@@ -305,18 +368,42 @@ def main():
     sb = 4 if args.rule == "fp32_amax" else 1
     code_bytes = nb * T * (mp + np_) * kp
     scale_bytes = nb * T * (mp + np_) * (kp // args.block) * sb
-    enc_bytes = 4 * nb * (M * K + K * N) + code_bytes + scale_bytes
-    prod_bytes = nb * T * mp * np_ * 4 if split else 4 * nb * M * N
-    comb_bytes = prod_bytes + 4 * nb * M * N if split else 0
-    peak = BF16_DENSE_PEAK_TFLOPS if (args.exact_dot or args.rule == "fp32_amax" or args.block == 16) \
-        else FP8_DENSE_PEAK_TFLOPS
+    ab_bytes = 4 * nb * (M * K + K * N)
+    c_bytes = 4 * nb * M * N
+    pr_bytes = nb * T * mp * np_ * 4 if split else 0          # P_r written and read back (not required)
+    enc_bytes = ab_bytes + code_bytes + scale_bytes
+    gemm_required = code_bytes + scale_bytes + c_bytes        # codes and scales read once, C written once
+    step_required = enc_bytes + gemm_required
+    exact = args.exact_dot or args.rule == "fp32_amax" or args.block == 16
+    peak = BF16_DENSE_PEAK_TFLOPS if exact else FP8_DENSE_PEAK_TFLOPS
     achieved = mfma_flop / (prod_ms * 1e-3) / 1e12
-    traffic = recorded_traffic("gemm_tile256x128" if split else "gemm_mx_fast", M, args) if headline else None
+    wkey = None
+    if headline and not args.exact_dot:
+        wkey = f"{M}cube_depth{args.depth}_{args.realization}_b{args.block}_{args.rule}_{args.family}"
+    counters = recorded_counters(wkey) if wkey else None
+    # the sub-product kernel the plan runs (layout and scale rule decide it)
+    if split:
+        prod_kernel = ("gemm_exact256x128_kernel" if sb == 4 else
+                       "gemm_dq256x128_kernel" if exact else "gemm_tile256x128_kernel")
+    elif a_view.code_layout == 2:
+        prod_kernel = "gemm_mx_fast_kernel" + (" (exact-dot form)" if exact else "")
+    else:
+        prod_kernel = "gemm_promote_kernel" if exact else "gemm_mx_kernel"
+    traffic = None
+    step_traffic = None
+    if counters:
+        for name, c in counters.items():
+            if c["role"] == "sub-products":
+                traffic = c["read"] + c["written"]
+        step_traffic = sum(c["read"] + c["written"] for c in counters.values())
 
-    def hbm(nbytes, ms):
+    def hbm(nbytes, ms, note=None):
         gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
-        return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": gbs / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": nbytes}
+        d = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": gbs / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": nbytes}
+        if note:
+            d["note"] = note
+        return d
 
     line = {
         "metric": METRIC,
@@ -331,10 +418,10 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8",
         "data": "synthetic",
-        "config": {"workload": (f"batch {nb} x " if nb > 1 else "") + f"{M}x{K}x{N} product, depth {args.depth}, realization "
-                               f"{args.realization} (Phi={phi:.4f}), e4m3 block {args.block} along K, "
-                               f"{args.rule} scales, {args.family} operands"
-                               + (", exact-dot" if args.exact_dot else ""),
+        "config": {"workload": (f"batch {nb} x " if nb > 1 else "") + f"{M}x{K}x{N} product, depth {args.depth}, "
+                               f"realization {args.realization} (Phi={phi:.4f}), e4m3 block {args.block} along "
+                               f"K, {args.rule} scales, {args.family} operands"
+                               + (", exact-dot sub-products" if args.exact_dot else ""),
                    "M": M, "K": K, "N": N, "depth": args.depth, "terms": T, "block": args.block,
                    "rule": args.rule, "realization": args.realization, "family": args.family,
                    "exact_dot": bool(args.exact_dot),
@@ -343,22 +430,35 @@ def main():
         "rel_rms_error_vs_fp64": float(np.sqrt(rel_mse)),
         "rel_mse_vs_fp64": rel_mse,
         "kernels_ms": {"encode": enc_ms, "products": prod_ms, "combine": comb_ms},
-        "step_event_ms": {"median": float(np.median(step_ms)), "min": float(step_ms.min()),
-                          "mean": float(step_ms.mean())},
-        "roofline": {"bound": "mfma", "kernel": "fp8 sub-product GEMM (fmm_products)",
+        "step_event_ms": {"median": float(np.median(ev["step"])), "min": float(ev["step"].min()),
+                          "mean": float(ev["step"].mean())},
+        "roofline": {"bound": "mfma", "kernel": f"{prod_kernel} (fmm_products: the T sub-products)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
                      "algorithmic_flop_per_launch": mfma_flop,
-                     "algorithmic_bytes_per_launch": code_bytes + scale_bytes + prod_bytes},
+                     "algorithmic_bytes_per_launch": gemm_required,
+                     "algorithmic_bytes_note": "codes and scales read once + C written once; on the large-tile "
+                                               "path C is written by the combine launch and this launch writes "
+                                               f"the fp32 P_r instead ({pr_bytes} bytes, not required)",
+                     "traffic_over_algorithmic": traffic / gemm_required if traffic else None},
         "encode_roofline": hbm(enc_bytes, enc_ms),
-        "device": torch.cuda.get_device_name(dev),
+        "step_hbm": {"required_bytes": step_required, "achieved": step_required / (ms_per_step * 1e-3) / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": step_required / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                     "pr_round_trip_bytes": 2 * pr_bytes,
+                     "traffic": step_traffic,
+                     "traffic_over_required": step_traffic / step_required if step_traffic else None,
+                     "note": "required = A, B read + codes and scales written + read once + C written once"},
+        "meta": run_meta(dev),
     }
     if split:
-        line["combine_roofline"] = hbm(comb_bytes, comb_ms)
+        line["combine_roofline"] = hbm(pr_bytes + c_bytes, comb_ms,
+                                       "the P_r read back is not required work: the pass exists because the "
+                                       "W-combine is not fused on the large-tile path")
     if nb > 1:
         line["config"]["batch"] = nb
     if not args.no_arms and headline:
-        line["arms"] = other_arms(args, dA, dB, C, stream)
+        line["arms"] = interleaved_arms(args, dA, dB, stream)
         line["paper_context"] = paper_context()
     if not args.no_cpu_baseline and headline:
         del dA, dB, C

@@ -1,0 +1,280 @@
+"""The benchmark configurations as specified, one JSON record per
+(configuration, arm, depth, block, trial), each with the oracle check made on
+it.  Test infrastructure (it calls the oracle): run on an MI355X as
+
+    python -m tests.run_configs --config C2 --out gpurun_out/records/C2.jsonl
+
+Configurations (seeded synthetic operands, fmm_inputs streams
+SeedSequence([0, cfg, trial, operand]); the same operands for every arm of a
+trial, as in the paper's paired protocol):
+
+* C1  256^3, N(0,1), block 32, E8M0 (power-of-two ceiling) scales, depth 1;
+      cubic, Strassen 1969, Winograd, T*; 100 trials (one batch of 100
+      products); every trial checked in full.
+* C2  4096^3, N(0,1), block 32, E8M0; the four realizations; 32 trials each;
+      every trial checked on sampled rows, trial 0 of each arm in full.
+* C3  8192^3, Uniform[-1,1], depth 2 (49 sub-products), block 32, E8M0;
+      T* (x) T* and Strassen (x) Strassen; 16 trials; trials 0 and 15 of each
+      arm checked on sampled rows.
+* C4  1024 products of 512^3, Student-t (3 degrees of freedom) / sqrt(3),
+      depth 1; 64 random GL(2)^3 changes of Strassen (each factor I + 0.45
+      N(0,1), |det| >= 1e-3, change i from stream [0, 4, i, 4]) x blocks
+      {16, 32, 128}; Phi and the measured relative MSE per arm, and their
+      Spearman rank correlation per block; changes 0, 21, 42, 63 checked at
+      every block on sampled rows of products 0, 511, 1023.
+* C5  16384 x 8192 x 16384, N(0,1) with a log-uniform factor over
+      [1e-2, 1e2] per row of A and of B, T*, depths 1, 2, 3, block 32, E8M0;
+      8 trials; trial 0 of each depth checked on sampled rows.
+
+Every configuration runs the path that meets the 1e-5 |C|_F element bar on
+its inputs: the fp8 matrix cores for C1-C3 (Gaussian and uniform operands),
+the exact-dot sub-products for C4 and C5 (heavy tails, four-decade row
+scales and general basis changes, where the fp8 dot product's group
+truncation exceeds it).  Timing: 2 warm-up and --reps timed whole steps per
+record (HIP events on the launch stream; median reported).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import fmm_inputs as gen                                   # noqa: E402
+from oracle import e4m3, fmm                               # noqa: E402
+from oracle import realizations as R                       # noqa: E402
+from tests.gpu_helpers import REL_FRO_TOL, MSE_REL_TOL, sampled_parity, uses_mx  # noqa: E402
+
+REALIZATIONS = ("cubic8", "strassen", "winograd", "tstar")
+RULE = "pow2_ceil"
+
+
+def log(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def timed(f, dA, dB, C, reps):
+    """Median event times (ms) of encode, sub-products, combine and the step."""
+    import torch
+    from bench import time_steps
+    stream = torch.cuda.current_stream()
+    time_steps(f, dA, dB, C, stream, 2)
+    t = time_steps(f, dA, dB, C, stream, reps)
+    return {k: float(np.median(v)) for k, v in t.items()}
+
+
+def full_parity(spec, A, B, C, err2, ref2, ops, depth, bs, rule, exact):
+    """Every code, scale and element of C of every batch element against the
+    oracle (small products)."""
+    from tests.gpu_helpers import oracle_realization
+    D = oracle_realization(spec)
+    tabs = R.tables_f32(D, depth)
+    ac, asc, bc, bsc = ops
+    same, worst, e_o, r_o = True, 0.0, 0.0, 0.0
+    for b in range(A.shape[0]):
+        o = fmm.fmm(A[b], B[b], tabs, depth, bs, rule)
+        if rule == e4m3.RULE_FP32_AMAX:
+            sa, sb, xa, xb = (v.view(np.uint32) for v in (asc[b], bsc[b], o["a"]["scales"], o["b"]["scales"]))
+        else:
+            sa, sb, xa, xb = asc[b], bsc[b], o["a"]["scales"], o["b"]["scales"]
+        same &= bool(np.array_equal(ac[b], o["a"]["codes"]) and np.array_equal(bc[b], o["b"]["codes"])
+                     and np.array_equal(sa, xa) and np.array_equal(sb, xb))
+        Co = o["C"]
+        fro = np.linalg.norm(Co)
+        if fro > 0:
+            worst = max(worst, float(np.abs(C[b].astype(np.float64) - Co).max() / fro))
+        e2, r2 = fmm.error_sums(Co, fmm.reference(A[b], B[b]))
+        e_o += e2
+        r_o += r2
+    rel_gpu = float(err2.sum() / ref2.sum())
+    rel_orc = e_o / r_o
+    return {"checked": f"full: all {A.shape[0]} products, every code, scale and element of C",
+            "codes_scales_identical": same, "max_rel_fro": worst, "meets_1e-5": worst <= REL_FRO_TOL,
+            "rel_mse_oracle": rel_orc, "rel_mse_agree": abs(rel_gpu / rel_orc - 1) <= MSE_REL_TOL,
+            "path": "fp8" if uses_mx(bs, rule, exact) else "exact"}
+
+
+def run_arm(spec, real_handle, A, B, dA, dB, depth, bs, exact, reps, parity, rng=None, bsel=(0,), nrows=16):
+    """One GPU run of (realization, operands): timing, GPU statistics and the
+    requested oracle check ('full', 'sampled' or None)."""
+    import torch
+    from paper_2609_26077_amd import FMM_LAYOUT_TILE256x64, fmm_operand_views, fmm_realization_metrics
+    from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
+    batch, M, K = A.shape
+    N = B.shape[2]
+    f = FMM(real_handle, batch, M, K, N, depth, bs, RULE, exact_dot=exact)
+    C = torch.empty((batch, M, N), dtype=torch.float32, device=dA.device)
+    t = timed(f, dA, dB, C, reps)
+    C = f.matmul(dA, dB, C)
+    Cref = reference_f64(dA, dB)
+    err2, ref2 = error_stats(C, Cref)
+    layout = fmm_operand_views(f.plan, f.ws)[0].code_layout
+    rule = e4m3.RULES[RULE]
+    rec = {"ms": t, "eff_tflops": 2.0 * batch * M * K * N / (t["step"] * 1e-3) / 1e12,
+           "rel_mse_gpu": float(err2.sum() / ref2.sum()),
+           "rel_rms_gpu": float(np.sqrt(err2.sum() / ref2.sum())),
+           "mean_rel_fro_gpu": float(np.mean(np.sqrt(err2 / ref2))),
+           "phi": fmm_realization_metrics(real_handle, depth)["phi"],
+           "path": ("exact-dot" if exact else "fp8") + (" 256x128 tiles + W-combine pass"
+                                                       if layout == FMM_LAYOUT_TILE256x64 else " fused 128x128"),
+           "parity": None}
+    if parity == "full":
+        ops = [x.cpu().numpy() for x in f.operands()]
+        rec["parity"] = full_parity(spec, A, B, C.cpu().numpy(), err2, ref2, ops, depth, bs, rule, exact)
+    elif parity == "sampled":
+        p = sampled_parity(spec, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nrows, rng, exact=exact)
+        p["checked"] = (f"sampled: {p['rows']} random rows of A's and of B's sub-block grids of products "
+                        f"{p['batch_elements']}, every element of C they give ({p['elements']})")
+        rec["parity"] = p
+    del f, C, Cref
+    torch.cuda.empty_cache()
+    return rec
+
+
+def device_operands(A, B):
+    import torch
+    return torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+
+
+def emit(out, rec):
+    line = json.dumps(rec)
+    print(line, flush=True)
+    if out:
+        out.write(line + "\n")
+        out.flush()
+
+
+def config1(args, out):
+    from paper_2609_26077_amd import fmm_realization_builtin
+    A, B = gen.operands("gaussian", 100, 256, 256, 256, seed=0, cfg=1, trial=0)
+    dA, dB = device_operands(A, B)
+    for name in REALIZATIONS:
+        rec = run_arm(name, fmm_realization_builtin(name), A, B, dA, dB, 1, 32, False, args.reps, "full")
+        rec.update({"config": "C1", "arm": name, "depth": 1, "block": 32, "rule": RULE, "family": "gaussian",
+                    "trials": "100 (one batch of 100 products)", "shape": [100, 256, 256, 256]})
+        emit(out, rec)
+        log(f"C1 {name}: {rec['eff_tflops']:.1f} TFLOP/s relMSE {rec['rel_mse_gpu']:.4e} "
+            f"parity {rec['parity']['codes_scales_identical']} {rec['parity']['max_rel_fro']:.2e}")
+
+
+def config2(args, out):
+    from paper_2609_26077_amd import fmm_realization_builtin
+    n = 4096
+    reals = {name: fmm_realization_builtin(name) for name in REALIZATIONS}
+    rng = np.random.default_rng(202)
+    for trial in range(args.trials or 32):
+        A, B = gen.operands("gaussian", 1, n, n, n, seed=0, cfg=2, trial=trial)
+        dA, dB = device_operands(A, B)
+        for name in REALIZATIONS:
+            parity = "full" if trial == 0 else "sampled"
+            rec = run_arm(name, reals[name], A, B, dA, dB, 1, 32, False, args.reps, parity, rng=rng, nrows=32)
+            rec.update({"config": "C2", "arm": name, "depth": 1, "block": 32, "rule": RULE, "family": "gaussian",
+                        "trial": trial, "shape": [1, n, n, n]})
+            emit(out, rec)
+            log(f"C2 t{trial} {name}: {rec['ms']['step']:.3f} ms relMSE {rec['rel_mse_gpu']:.4e} "
+                f"max_rel_fro {rec['parity']['max_rel_fro']:.2e}")
+        del dA, dB
+
+
+def config3(args, out):
+    import torch
+    from paper_2609_26077_amd import fmm_realization_builtin
+    n = 8192
+    reals = {name: fmm_realization_builtin(name) for name in ("tstar", "strassen")}
+    rng = np.random.default_rng(303)
+    trials = args.trials or 16
+    for trial in range(trials):
+        A, B = gen.operands("uniform", 1, n, n, n, seed=0, cfg=3, trial=trial)
+        dA, dB = device_operands(A, B)
+        for name in ("tstar", "strassen"):
+            parity = "sampled" if trial in (0, trials - 1) else None
+            rec = run_arm(name, reals[name], A, B, dA, dB, 2, 32, False, args.reps, parity, rng=rng, nrows=12)
+            rec.update({"config": "C3", "arm": f"{name} (x) {name}", "depth": 2, "block": 32, "rule": RULE,
+                        "family": "uniform", "trial": trial, "shape": [1, n, n, n]})
+            emit(out, rec)
+            log(f"C3 t{trial} {name}: {rec['ms']['step']:.3f} ms relMSE {rec['rel_mse_gpu']:.4e}")
+        del dA, dB
+        torch.cuda.empty_cache()
+
+
+def config4(args, out):
+    from scipy.stats import spearmanr
+    from paper_2609_26077_amd import fmm_realization_builtin, fmm_realization_transform
+    A, B = gen.operands("student_t3", 1024, 512, 512, 512, seed=0, cfg=4, trial=0)
+    dA, dB = device_operands(A, B)
+    nchanges = args.trials or 64
+    changes = gen.basis_changes(nchanges, seed=0, cfg=4)
+    checked = {0, 21, 42, 63}
+    base = fmm_realization_builtin("strassen")
+    rng = np.random.default_rng(404)
+    for bs in (16, 32, 128):
+        phis, mses = [], []
+        for i, g in enumerate(changes):
+            real = fmm_realization_transform(base, *g)
+            parity = "sampled" if i in checked else None
+            rec = run_arm(("strassen", g), real, A, B, dA, dB, 1, bs, True, args.reps, parity, rng=rng,
+                          bsel=(0, 511, 1023), nrows=16)
+            rec.update({"config": "C4", "arm": f"strassen . g{i}", "depth": 1, "block": bs, "rule": RULE,
+                        "family": "student_t3", "trial": 0, "change": i,
+                        "g": [np.asarray(m).ravel().tolist() for m in g], "shape": [1024, 512, 512, 512]})
+            emit(out, rec)
+            phis.append(rec["phi"])
+            mses.append(rec["rel_mse_gpu"])
+            log(f"C4 block {bs} g{i}: Phi {rec['phi']:.2f} relMSE {rec['rel_mse_gpu']:.4e} {rec['ms']['step']:.3f} ms")
+        rho = spearmanr(phis, mses)
+        emit(out, {"config": "C4", "summary": True, "block": bs, "changes": len(phis),
+                   "spearman_phi_vs_rel_mse": float(rho.statistic), "p_value": float(rho.pvalue),
+                   "phi_range": [min(phis), max(phis)], "rel_mse_range": [min(mses), max(mses)]})
+        log(f"C4 block {bs}: Spearman rho(Phi, relMSE) = {rho.statistic:.4f}")
+
+
+def config5(args, out):
+    import torch
+    from paper_2609_26077_amd import fmm_realization_builtin
+    M, K, N = 16384, 8192, 16384
+    real = fmm_realization_builtin("tstar")
+    rng = np.random.default_rng(505)
+    for trial in range(args.trials or 8):
+        A, B = gen.operands("rowscaled", 1, M, K, N, seed=0, cfg=5, trial=trial)
+        dA, dB = device_operands(A, B)
+        for depth in (1, 2, 3):
+            parity = "sampled" if trial == 0 else None
+            rec = run_arm("tstar", real, A, B, dA, dB, depth, 32, True, args.reps, parity, rng=rng, nrows=8)
+            rec.update({"config": "C5", "arm": "tstar", "depth": depth, "block": 32, "rule": RULE,
+                        "family": "rowscaled", "trial": trial, "shape": [1, M, K, N]})
+            emit(out, rec)
+            log(f"C5 t{trial} depth {depth}: {rec['ms']['step']:.3f} ms ({rec['eff_tflops']:.0f} TFLOP/s) "
+                f"relMSE {rec['rel_mse_gpu']:.4e}")
+        del dA, dB
+        torch.cuda.empty_cache()
+
+
+def main():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--config", required=True, choices=["C1", "C2", "C3", "C4", "C5"])
+    p.add_argument("--trials", type=int, default=None, help="fewer trials (basis changes for C4) than specified")
+    p.add_argument("--reps", type=int, default=5)
+    p.add_argument("--out", default=None)
+    args = p.parse_args()
+    out = None
+    if args.out:
+        os.makedirs(os.path.dirname(os.path.abspath(args.out)), exist_ok=True)
+        out = open(args.out, "w")
+    import torch
+    from bench import run_meta
+    emit(out, {"config": args.config, "meta": run_meta(torch.device("cuda:0")),
+               "command": "python -m tests.run_configs " + " ".join(sys.argv[1:])})
+    {"C1": config1, "C2": config2, "C3": config3, "C4": config4, "C5": config5}[args.config](args, out)
+    if out:
+        out.close()
+
+
+if __name__ == "__main__":
+    main()
