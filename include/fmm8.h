@@ -344,6 +344,25 @@ int fmm_encode_noise_scratch_size(const fmm_plan *p, size_t *bytes);
 int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const void *dWs, double *dOut,
                      void *dScratch, size_t scratch_bytes, void *stream);
 
+/* The cross-term diagnostic of the error model (Appendix D: the share of
+ * the error's linear part that the diagonal sum defining Phi leaves out).
+ * Call after fmm_encode with the same dA, dB and workspace; depth-1 plans
+ * only (FMM_ERR_UNSUPPORTED otherwise), any layout, rule and block.  With
+ * X_r, Y_r the fp32 combinations (the encoder's arithmetic), dX_r, dY_r their
+ * rounding residuals against the stored codes times their scales, t_r =
+ * dX_r Y_r + X_r dY_r (m' x n', binary64) and L_q = sum_r w[r, q] t_r, dOut
+ * (device, [batch][2] binary64) receives for every batch element
+ * |L|^2 = sum_q |L_q|^2 and diag = sum_{r, q} w[r, q]^2 |t_r|^2, each by a
+ * fixed summation order (repeated calls agree bit for bit); the residual
+ * fraction is (|L|^2 - diag) / |L|^2.  dScratch: device, 256-byte aligned, at
+ * least fmm_cross_terms_scratch_size bytes (16 (M + N) K / 2 + 8 M N / 4
+ * bytes per term and product, FMM_ERR_WORKSPACE otherwise).  With
+ * FMM_FLAG_B_BF16, Y_r is the combination before the bfloat16 rounding.
+ * Asynchronous on stream; measurement, not on the timed path. */
+int fmm_cross_terms_scratch_size(const fmm_plan *p, size_t *bytes);
+int fmm_cross_terms(const fmm_plan *p, const float *dA, const float *dB, const void *dWs, double *dOut,
+                    void *dScratch, size_t scratch_bytes, void *stream);
+
 /* dOut[i] = e4m3 code of dIn[i] at unit scale: round to nearest, ties to the
  * even mantissa field, saturate to +-448, keep the sign (the cast the
  * quantizer applies after dividing by the block scale).  n >= 0; dIn must be

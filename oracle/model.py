@@ -38,14 +38,21 @@ def predicted_rel_mse(s_a2: float, s_b2: float, phi: float, depth: int,
 
 def cross_r_residual(ea, eb, w_table) -> float:
     """The share of the error's linear part that the diagonal sum defining
-    Phi leaves out (Appendix D, the cross-r covariance measurement).
+    Phi leaves out (Appendix D, the cross-r covariance measurement):
+    (|L|^2 - diag) / |L|^2 from cross_r_sums."""
+    L2, diag = cross_r_sums(ea, eb, w_table)
+    return (L2 - diag) / L2
+
+
+def cross_r_sums(ea, eb, w_table):
+    """(|L|^2, diag) of the cross-r covariance measurement (Appendix D).
 
     With X_r, Y_r the fp32 combinations and dX_r, dY_r their rounding
     residuals (encode_side outputs, B side transposed back), the part of the
     sub-product error linear in the residuals is t_r = dX_r Y_r + X_r dY_r,
-    and that of output block q is L_q = sum_r w[r, q] t_r.  Returns
-    (|L|^2 - diag) / |L|^2 with diag = sum_{r,q} w[r, q]^2 |t_r|^2
-    (binary64 throughout)."""
+    and that of output block q is L_q = sum_r w[r, q] t_r.  |L|^2 =
+    sum_q |L_q|^2 and diag = sum_{r,q} w[r, q]^2 |t_r|^2 (binary64
+    throughout)."""
     w = np.asarray(w_table, dtype=np.float64)
     T, nq = w.shape
     t = []
@@ -63,4 +70,4 @@ def cross_r_residual(ea, eb, w_table) -> float:
             continue
         L2 += float(np.sum(Lq * Lq))
         diag += sum(float(w[r, q] ** 2 * np.sum(t[r] * t[r])) for r in range(T))
-    return (L2 - diag) / L2
+    return L2, diag

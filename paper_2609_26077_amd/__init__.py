@@ -117,6 +117,8 @@ _SIGS = {
     "fmm_error_stats": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                        _vp]),
     "fmm_error_stats_noalloc": (ctypes.c_int, [_i64, _i64, _i64, _vp, _vp, _vp, _vp]),
+    "fmm_cross_terms_scratch_size": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_size_t)]),
+    "fmm_cross_terms": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]),
     "fmm_e4m3_quantize": (ctypes.c_int, [_vp, _vp, _i64, _vp]),
     "fmm_e4m3_quantize_pow2": (ctypes.c_int, [_vp, _vp, _i64, ctypes.c_int32, _vp]),
     "fmm_encode_noise_scratch_size": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_size_t)]),
@@ -340,6 +342,17 @@ def fmm_encode_noise_scratch_size(p: Plan) -> int:
 def fmm_encode_noise(p: Plan, A, B, ws, out, scratch, scratch_bytes: int, stream=None):
     _check(_lib.fmm_encode_noise(p.handle, _ptr(A), _ptr(B), _ptr(ws), _ptr(out), _ptr(scratch),
                                  int(scratch_bytes), _stream(stream)), "fmm_encode_noise")
+
+
+def fmm_cross_terms_scratch_size(p: Plan) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib.fmm_cross_terms_scratch_size(p.handle, ctypes.byref(n)), "fmm_cross_terms_scratch_size")
+    return n.value
+
+
+def fmm_cross_terms(p: Plan, A, B, ws, out, scratch, scratch_bytes: int, stream=None):
+    _check(_lib.fmm_cross_terms(p.handle, _ptr(A), _ptr(B), _ptr(ws), _ptr(out), _ptr(scratch),
+                                int(scratch_bytes), _stream(stream)), "fmm_cross_terms")
 
 
 def fmm_plan_create(d: Realization, desc: fmm_plan_desc) -> Plan:

@@ -14,7 +14,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 
 SOURCES = ["realization.cpp", "optimize.cpp", "plan.cpp", "kernels_encode.hip", "kernels_gemm.hip",
-           "kernels_split.hip", "kernels_measure.hip"]
+           "kernels_split.hip", "kernels_measure.hip", "kernels_cross.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
           "-Wno-unused-function", "-Wno-unused-variable"]

@@ -14,7 +14,13 @@ simple statistics of what they return:
   g in GL(2)^3), one shape, signed-uniform operands; its coefficient of
   variation;
 * designed Rademacher cells: +-1 operands at unit scale and at scale 10 on
-  three shapes; whether classic Strassen's measured error is below T*'s.
+  three shapes; whether classic Strassen's measured error is below T*'s;
+* cross-r covariance residual: the share of the error's linear part that the
+  diagonal sum defining Phi leaves out, (|L|^2 - diag) / |L|^2 from the
+  library's cross-term kernels, on six arms (cubic, Strassen, Winograd raw
+  and rebalanced, T*, a random orbit member of Strassen) at n = 512, Gaussian
+  operands, four seeds, 1 x 128 blocks with fp32 amax/448 scales; the
+  armwise means (the paper reports -0.085% to 0.201%).
 
 Usage: python -m paper_2609_26077_amd.controls [--quick]  (prints one JSON object)
 """
@@ -27,7 +33,8 @@ import math
 import numpy as np
 import torch
 
-from . import fmm_realization_builtin, fmm_realization_metrics, fmm_realization_transform
+from . import (fmm_realization_builtin, fmm_realization_metrics, fmm_realization_rebalance,
+               fmm_realization_transform)
 from .runner import FMM, error_stats, reference_f64
 
 FAMILIES = ("gaussian", "uniform", "student_t3", "laplace", "rowscaled")
@@ -104,6 +111,29 @@ def rademacher_cells(shapes, batch=2, seed=0):
     return {"cells": cells, "strassen_wins": sum(c["strassen_wins"] for c in cells), "of": len(cells)}
 
 
+def cross_r_residual(n=512, seeds=4):
+    import fmm_inputs as gen
+    s = fmm_realization_builtin("strassen")
+    arms = {"cubic8": fmm_realization_builtin("cubic8"), "strassen": s,
+            "winograd": fmm_realization_builtin("winograd"),
+            "winograd/rebalanced": fmm_realization_rebalance(fmm_realization_builtin("winograd")),
+            "tstar": fmm_realization_builtin("tstar"),
+            "strassen.g": fmm_realization_transform(s, *gen.basis_changes(1, seed=0, cfg=14)[0])}
+    out = {}
+    for label, real in arms.items():
+        vals = []
+        for seed in range(seeds):
+            A, B = device_operands("gaussian", 1, n, n, n, seed, 14)
+            f = FMM(real, 1, n, n, n, 1, 128, "fp32_amax")
+            f.encode(A, B)
+            L2, diag = f.cross_terms(A, B)[0]
+            vals.append(float((L2 - diag) / L2))
+        out[label] = {"mean_pct": 100.0 * float(np.mean(vals)), "per_seed_pct": [100.0 * v for v in vals]}
+    means = [v["mean_pct"] for v in out.values()]
+    return {"arms": out, "armwise_mean_range_pct": [min(means), max(means)],
+            "paper_range_pct": [-0.085, 0.201]}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--quick", action="store_true", help="small shapes (a smoke run)")
@@ -116,7 +146,8 @@ def main():
         orbit = dict(n_members=15, shape=(1024, 1024, 1024))
     out = {"calibration_transport": calibration_transport(shapes),
            "orbit_stability": orbit_stability(**orbit),
-           "rademacher": rademacher_cells(shapes)}
+           "rademacher": rademacher_cells(shapes),
+           "cross_r_residual": cross_r_residual(seeds=1 if args.quick else 4)}
     print(json.dumps(out), flush=True)
 
 

@@ -110,6 +110,10 @@ int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8
 size_t encode_noise_scratch_bytes(const Problem &pb);
 int launch_encode_noise(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
                         const uint8_t *ws, const Workspace &wl, double *out, void *scratch, void *stream);
+// the cross-term diagnostic (depth 1): out [batch][2] binary64 = (|L|^2, diag)
+size_t cross_terms_scratch_bytes(const Problem &pb);
+int launch_cross_terms(const Problem &pb, const DeviceTables &tab, const float *A, const float *B,
+                       const uint8_t *ws, const Workspace &wl, double *out, void *scratch, void *stream);
 int launch_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *A,
                          const float *B, double *Cref, void *stream);
 size_t error_stats_scratch_bytes(int64_t batch, int64_t M, int64_t N);

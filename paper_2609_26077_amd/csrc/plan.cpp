@@ -376,6 +376,27 @@ int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const 
                                              dOut, dScratch, stream));
 }
 
+int fmm_cross_terms_scratch_size(const fmm_plan *p, size_t *bytes) {
+  if (!p || !bytes) return FMM_ERR_ARG;
+  if (p->pb.depth != 1) return FMM_ERR_UNSUPPORTED;
+  *bytes = fmm::cross_terms_scratch_bytes(p->pb);
+  return FMM_OK;
+}
+
+int fmm_cross_terms(const fmm_plan *p, const float *dA, const float *dB, const void *dWs, double *dOut,
+                    void *dScratch, size_t scratch_bytes, void *stream) {
+  if (!p) return FMM_ERR_ARG;
+  const fmm::Problem &pb = p->pb;
+  if (pb.depth != 1) return FMM_ERR_UNSUPPORTED;
+  if (pb.batch == 0) return FMM_OK;
+  if (!dOut || !dWs || (pb.M * pb.K > 0 && !dA) || (pb.K * pb.N > 0 && !dB)) return FMM_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(dWs) % 256) return FMM_ERR_WORKSPACE;
+  if (!dScratch || scratch_bytes < fmm::cross_terms_scratch_bytes(pb) || reinterpret_cast<uintptr_t>(dScratch) % 256)
+    return FMM_ERR_WORKSPACE;
+  return hip_status(fmm::launch_cross_terms(pb, p->tab, dA, dB, reinterpret_cast<const uint8_t *>(dWs), p->wl,
+                                            dOut, dScratch, stream));
+}
+
 int fmm_e4m3_quantize(const float *dIn, uint8_t *dOut, int64_t n, void *stream) {
   if (n < 0) return FMM_ERR_ARG;
   if (n == 0) return FMM_OK;

@@ -106,6 +106,18 @@ class FMM:
         fmm_encode_noise(self.plan, A, B, self.ws, out, scratch, nbytes, stream)
         return out.cpu().numpy()
 
+    def cross_terms(self, A, B, stream=None):
+        """The cross-term diagnostic of the encoding in the workspace (call
+        after encode with the same A, B; depth 1): numpy [batch][2] of
+        (|L|^2, diag) per batch element (include/fmm8.h, fmm_cross_terms)."""
+        self._inputs(A, B)
+        from . import fmm_cross_terms, fmm_cross_terms_scratch_size
+        out = torch.empty((self.shape[0], 2), dtype=torch.float64, device=self.device)
+        nbytes = fmm_cross_terms_scratch_size(self.plan)
+        scratch = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        fmm_cross_terms(self.plan, A, B, self.ws, out, scratch, nbytes, stream)
+        return out.cpu().numpy()
+
     def operands(self):
         """(a_codes, a_scales, b_codes, b_scales) as [batch][terms][rows][kdim]
         and [batch][terms][rows][kblocks] tensors: views of the workspace, or

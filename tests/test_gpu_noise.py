@@ -101,3 +101,64 @@ def test_controls_quick_run():
     cal = controls.calibration_transport(shapes, families=("gaussian", "uniform"))
     assert 0 < cal["max_within_family_across_shape_spread_pct"] < 20
     print(rad, orb, cal, flush=True)
+
+
+@pytest.mark.parametrize("case", [
+    # (name, family, batch, M, K, N, block, rule, flags): every layout and rule
+    ("tstar", "gaussian", 1, 512, 512, 512, 128, 0, 0),            # fp32 amax/448, large tiles (the paper's setting)
+    ("strassen", "gaussian", 1, 512, 512, 512, 32, 1, 0),          # E8M0, fused 128 x 128 tile layout
+    ("winograd", "student_t3", 2, 512, 256, 512, 32, 1, 8),        # E8M0, large tiles, batch of two
+    ("cubic8", "gaussian", 1, 130, 256, 66, 32, 2, 0),             # ragged: row layout, OCP rule
+    ("tstar", "student_t3", 1, 384, 512, 320, 128, 0, 2 | 4),      # deployment granularity (bf16 pre-round)
+])
+def test_cross_terms_match_oracle(case):
+    """The cross-term diagnostic (fmm_cross_terms; Appendix D) against the
+    oracle's cross_r_sums on the same encoding: |L|^2 and diag to 1e-10
+    relative (binary64 on both sides, different summation orders), the
+    residual fraction to 1e-6 absolute, and repeat calls bit for bit."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    name, family, b, M, K, N, bs, rule, flags = case
+    A, B = gen.operands(family, b, M, K, N, seed=3, cfg=13, trial=0)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM(name, b, M, K, N, 1, bs, rule, flags=flags)
+    f.encode(dA, dB)
+    g = f.cross_terms(dA, dB)
+    assert np.array_equal(g, f.cross_terms(dA, dB))
+    U, V, W = R.tables_f32(R.builtin_f64(name), 1)
+    for i in range(b):
+        ea = fmm.encode_side(A[i], U, 1, bs, rule, "A")
+        eb = fmm.encode_side(B[i], V, 1, bs, rule, "B", row_block=128 if flags & 2 else 1, bf16=bool(flags & 4))
+        L2, diag = model.cross_r_sums(ea, eb, W)
+        assert g[i, 0] == pytest.approx(L2, rel=1e-10) and g[i, 1] == pytest.approx(diag, rel=1e-10), (g[i], L2, diag)
+        assert abs((g[i, 0] - g[i, 1]) / g[i, 0] - (L2 - diag) / L2) < 1e-6
+
+
+def test_cross_terms_six_arm_diagnostic():
+    """Appendix D's diagnostic on the GPU path: six arms (cubic, Strassen,
+    Winograd raw and rebalanced, T*, a random orbit member of Strassen) at
+    n = 512, Gaussian operands, four seeds, 1 x 128 blocks with fp32 amax/448
+    scales; the armwise mean residual fractions lie in the paper's range
+    (-0.085% to 0.201%), widened to +-0.3% for this population."""
+    import torch
+    import paper_2609_26077_amd as fm
+    from paper_2609_26077_amd.runner import FMM
+    s = fm.fmm_realization_builtin("strassen")
+    arms = {"cubic8": fm.fmm_realization_builtin("cubic8"), "strassen": s,
+            "winograd": fm.fmm_realization_builtin("winograd"),
+            "winograd/rebalanced": fm.fmm_realization_rebalance(fm.fmm_realization_builtin("winograd")),
+            "tstar": fm.fmm_realization_builtin("tstar"),
+            "strassen.g": fm.fmm_realization_transform(s, *gen.basis_changes(1, seed=0, cfg=14)[0])}
+    means = {}
+    for label, real in arms.items():
+        vals = []
+        for seed in range(4):
+            A, B = gen.operands("gaussian", 1, 512, 512, 512, seed=seed, cfg=14, trial=0)
+            dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+            f = FMM(real, 1, 512, 512, 512, 1, 128, "fp32_amax")
+            f.encode(dA, dB)
+            L2, diag = f.cross_terms(dA, dB)[0]
+            vals.append((L2 - diag) / L2)
+        means[label] = float(np.mean(vals))
+    print("armwise mean residual fractions", means, flush=True)
+    assert all(abs(v) < 0.003 for v in means.values()), means
