@@ -1,18 +1,19 @@
 // Large-tile sub-products for tile-aligned block-scaled problems at depths 1 and 2.
 //
 // The sub-products are the dominant cost; each is a plain block-scaled fp8
-// GEMM P_r = A_r B_r^T with fp32 accumulation.  Large tiles halve the operand
+// GEMM P_r = A_r B_r^T with fp32 accumulation.  Large tiles cut the operand
 // bytes per MFMA flop of a 128 x 128 tile, which is what bounds the feed from
 // L2 into LDS; the price is that P_r leaves the workgroup, so the W-combine
 // becomes its own bandwidth-bound pass:
 //
-//   1. gemm_tile256x128_kernel: one workgroup per (batch, term r, 256 x 128
-//      tile), four waves of 128 x 64 (4 x 2 MFMA tiles of 32 x 32, 128
-//      accumulation registers each), one per SIMD, and two workgroups per CU:
-//      while one waits (LDS reads, a barrier, its epilogue) the other's MFMAs
-//      keep the SIMDs busy.  64-byte K steps run through a three-slot LDS ring
-//      filled by global_load_lds two steps ahead, one barrier per step; P_r is
-//      stored in fp32 with nontemporal stores.
+//   1. gemm_tile256x256_kernel: one workgroup per (batch, term r, 256 x 256
+//      tile), eight waves of 128 x 64 (4 x 2 MFMA tiles of 32 x 32, 128
+//      accumulation registers each), two per SIMD, one workgroup per CU.
+//      64-byte K steps run through a four-slot LDS ring filled by
+//      global_load_lds two steps ahead, one barrier per step; P_r is stored
+//      in fp32 with nontemporal stores.  Against 256 x 128 tiles (two
+//      four-wave workgroups per CU) the L2 -> LDS bytes per flop drop by a
+//      third: 8192^3 sub-products 0.47 -> 0.40 ms.
 //      Exact-dot plans take gemm_dq256x128_kernel (E8M0 scales: each block's
 //      power of two folded into the codes' conversion to bf16) or
 //      gemm_exact256x128_kernel (fp32 scales: per-block partial sums promoted
@@ -49,15 +50,24 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 constexpr int TM = kSplitTile;        // tile rows of A_r (and rows of one code image)
 constexpr int TN = kSplitTileN;       // tile rows of B_r: half an image
 constexpr int SK = 64;                // contracted bytes per step
+constexpr int kCodeA = TM * SK;       // 16 KB of A codes per step
+constexpr int kImage = TM * SK;       // one (256-row tile, k-step) code image
+
+// the fp8 kernel: 256 A rows x 256 B rows (a whole B code image) per tile
+namespace big {
+constexpr int TNB = 2 * TN;
+constexpr int kThreadsB = 512;
+constexpr int kSlotsB = 4;
+constexpr int kCodeB = TNB * SK;                     // 16 KB of B codes per step
+constexpr int kScaleA = 2 * TM, kScaleB = 2 * TNB;   // two K blocks x 256 rows each side
+constexpr int kSlot = kCodeA + kCodeB + kScaleA + kScaleB;   // 33792 B
+static_assert(kSlotsB * kSlot <= 160 * 1024, "one workgroup per CU");
+}  // namespace big
+
+// the exact-dot kernels: 256 A rows x 128 B rows (half an image) per tile
 constexpr int kThreads = 256;
 constexpr int kSlots = 3;
-constexpr int kCodeA = TM * SK;       // 16 KB of A codes per step
 constexpr int kCodeB = TN * SK;       // 8 KB of B codes per step
-constexpr int kImage = TM * SK;       // one (256-row tile, k-step) code image
-constexpr int kScaleA = 2 * TM;       // two K blocks x 256 rows of scale bytes
-constexpr int kScaleB = 2 * TN;       // two K blocks x 128 rows
-constexpr int kSlot = kCodeA + kCodeB + kScaleA + kScaleB;   // 25344 B; two workgroups fit in LDS
-static_assert(2 * kSlots * kSlot <= 160 * 1024, "two workgroups per CU");
 
 struct SplitArgs {
   const uint8_t *xa, *xb;      // codes [batch][T][rows / 256][kp / 64][256 x 64 tile image]
@@ -94,8 +104,9 @@ struct Frags {
 
 // Work order: workgroups are dispatched round-robin over the eight XCDs, so
 // the ids of one XCD (bid, bid + 8, ...) are given a contiguous range of work
-// items; items run term-major, and the tiles of a term in groups of eight
+// items; items run term-major, and the tiles of a term in groups of GM
 // tile-rows, so the workgroups resident on an XCD share A and B rows in L2.
+template <int GM = 8>
 __device__ __forceinline__ void work_of(int bid, int64_t nitems, int64_t T, int tiles_m, int tiles_n,
                                         int64_t &bt, int64_t &r, int &tm, int &tn) {
   int64_t id = bid;
@@ -105,7 +116,6 @@ __device__ __forceinline__ void work_of(int bid, int64_t nitems, int64_t T, int 
   const int64_t rem = id - bt * T * ntiles;
   r = rem / ntiles;
   const int tile = (int)(rem - r * ntiles);
-  constexpr int GM = 8;
   const int per_group = GM * tiles_n;
   const int group = tile / per_group;
   const int first_m = group * GM;
@@ -116,67 +126,65 @@ __device__ __forceinline__ void work_of(int bid, int64_t nitems, int64_t T, int 
 }
 
 template <int BS>
-__global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs g) {
-  __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+__global__ __launch_bounds__(big::kThreadsB, 1) void gemm_tile256x256_kernel(SplitArgs g) {
+  __shared__ uint4 lds_raw[big::kSlotsB * big::kSlot / 16];
   const uint8_t *lds = reinterpret_cast<const uint8_t *>(lds_raw);
   const uint32_t lds_base = dma::lds_addr(lds_raw);
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wm = wave >> 1, wn = wave & 1;       // A rows 128 wm.., B rows 64 wn.. of the tile
+  const int wm = wave >> 2, wn = wave & 3;       // A rows 128 wm.., B rows 64 wn.. of the tile
   const int r32 = lane & 31, h = lane >> 5;
   const int64_t nitems = (int64_t)gridDim.x;
+  const int tiles_nb = g.tiles_n / 2;            // 256-row B tiles
   int64_t bt, r;
   int tm, tn;
-  work_of(blockIdx.x, nitems, g.T, g.tiles_m, g.tiles_n, bt, r, tm, tn);
-  const int64_t pm0 = (int64_t)tm * TM, pn0 = (int64_t)tn * TN;
-  const int hb = tn & 1;                          // half of the 256-row B tile
+  work_of<4>(blockIdx.x, nitems, g.T, g.tiles_m, tiles_nb, bt, r, tm, tn);
+  const int64_t pm0 = (int64_t)tm * TM, pn0 = (int64_t)tn * big::TNB;
   const int nk = (int)(g.kp / SK);
   // codes arrive tiled: the image of (256-row tile, k-step) is contiguous, so a
   // transfer is a straight 1 KB copy (lane l moves bytes 16 l .. 16 l + 15)
   const uint8_t *xa = g.xa + ((bt * g.T + r) * g.tiles_m + tm) * (int64_t)nk * kImage;
-  const uint8_t *xb = g.xb + ((bt * g.T + r) * (g.tiles_n / 2) + (tn >> 1)) * (int64_t)nk * kImage + hb * kCodeB;
+  const uint8_t *xb = g.xb + ((bt * g.T + r) * tiles_nb + tn) * (int64_t)nk * kImage;
   const uint32_t code_off = 16u * (uint32_t)lane;
-  // the six 1 KB regions wave w moves each step: regions 6 w .. 6 w + 5 of
-  // the slot's codes, 0..15 from A's image, 16..23 from B's half image
-  const uint8_t *csrc[6];
-  uint32_t cdst[6];
+  // the four 1 KB regions wave w moves each step: 4 w .. 4 w + 3 of the
+  // slot's codes, 0..15 from A's image, 16..31 from B's
+  const uint8_t *csrc[4];
+  uint32_t cdst[4];
 #pragma unroll
-  for (int j = 0; j < 6; ++j) {
-    const int region = wave * 6 + j;
+  for (int j = 0; j < 4; ++j) {
+    const int region = wave * 4 + j;
     csrc[j] = region < 16 ? xa + region * 1024 : xb + (region - 16) * 1024;
     cdst[j] = (uint32_t)(region < 16 ? region * 1024 : kCodeA + (region - 16) * 1024);
   }
-  // scale transfer of this wave (256 bytes, lane l moves 4):
-  //   wave 0 / 1: A scale bytes of K block 2 step + wave (block 32) or step / 2
-  //   wave 2 / 3: B scale bytes of the tile's half, lanes 32 k' .. of K block
-  //               2 step + k' (block 32), or of block step / 2 in both halves
-  //               of the lanes (block 128); waves 2 and 3 move the same bytes
-  const bool s_is_b = wave >= 2;
-  const int64_t srows = s_is_b ? g.np : g.mp;
-  const uint8_t *ssrc = s_is_b ? g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0   // bytes 128 hb .. of the 256-row tile
-                               : g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0 + (BS == 32 ? wave * g.mp : 0);
-  const uint32_t s_off = s_is_b ? 4u * (uint32_t)r32 + (BS == 32 ? (uint32_t)(h * g.np) : 0u) : 4u * (uint32_t)lane;
-  const uint32_t sdst = (uint32_t)(kCodeA + kCodeB + (s_is_b ? kScaleA : (BS == 32 ? wave * TM : 0)));
+  // one scale transfer per wave and step (256 bytes, lane l moves 4): wave w
+  // moves side (w >> 1) & 1 (A, B), K block 2 step + (w & 1) (block 32) or
+  // step / 2 (block 128), all 256 rows of the tile; waves 4..7 repeat 0..3
+  const int sside = (wave >> 1) & 1, sblk = wave & 1;
+  const int64_t srows = sside ? g.np : g.mp;
+  const uint8_t *ssrc = sside ? g.sbt + (bt * g.T + r) * g.kblocks * g.np + pn0
+                              : g.sat + (bt * g.T + r) * g.kblocks * g.mp + pm0;
+  const uint32_t s_off = 4u * (uint32_t)lane + (BS == 32 ? (uint32_t)(sblk * srows) : 0u);
+  const uint32_t sdst = (uint32_t)(kCodeA + big::kCodeB + (sside ? big::kScaleA : 0) + (BS == 32 ? sblk * TM : 0));
 
   auto issue = [&](int step) {
-    const uint32_t m0 = lds_base + (uint32_t)(step % kSlots) * kSlot;
+    const uint32_t m0 = lds_base + (uint32_t)(step % big::kSlotsB) * big::kSlot;
     const int64_t src = (int64_t)step * kImage;
 #pragma unroll
-    for (int j = 0; j < 6; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
+    for (int j = 0; j < 4; ++j) dma::copy16(code_off, csrc[j] + src, m0 + cdst[j]);
     const int64_t kb = BS == 32 ? 2 * (int64_t)step : step / 2;
     dma::copy4(s_off, ssrc + kb * srows, m0 + sdst);
   };
 
   // LDS -> registers for one step (any step index reads in bounds)
   auto load = [&](int step, Frags &f) {
-    const uint8_t *la = lds + (step % kSlots) * kSlot;
+    const uint8_t *la = lds + (step % big::kSlotsB) * big::kSlot;
     const uint8_t *lb = la + kCodeA;
-    const uint8_t *ls = lb + kCodeB;
-    // A: block 2 step + h (block 32) or step / 2 at bytes h TM .. (block 32) / 0 ..;
-    // B: the 128 bytes of K block 2 step + h at 128 h (block 32) / 0 (block 128)
+    const uint8_t *ls = lb + big::kCodeB;
+    // block 2 step + h (block 32) or step / 2: tile row 128 H + 32 I + J at byte 4 (32 H + J) + I;
+    // A: H = wm, I = i; B row 64 wn + 32 j + r32: H = wn >> 1, I = 2 (wn & 1) + j
     f.sa = *reinterpret_cast<const uint32_t *>(ls + (BS == 32 ? h * TM : 0) + 4 * (wm * 32 + r32));
-    // B row 64 wn + 32 j + r of the half is row 128 hb + 32 (2 wn + j) + r of the 256-row tile
-    f.sb = *reinterpret_cast<const uint32_t *>(ls + kScaleA + (BS == 32 ? h * TN : 0) + 4 * r32) >> (16 * wn);
+    f.sb = *reinterpret_cast<const uint32_t *>(ls + big::kScaleA + (BS == 32 ? h * big::TNB : 0) + 4 * (32 * (wn >> 1) + r32))
+           >> (16 * (wn & 1));
 #pragma unroll
     for (int i = 0; i < 4; ++i) f.a[i] = frag64(la, wm * 128 + 32 * i + r32, h);
 #pragma unroll
@@ -198,14 +206,14 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 #undef FMM_MFMA_IJ
   };
 
-  // Step s: wait for this wave's own transfers of step s (seven a step; those
+  // Step s: wait for this wave's own transfers of step s (five a step; those
   // of step s + 1 may stay in flight), barrier (every wave's transfers of s
   // have landed, and every wave has read step s - 1), start step s + 2 into
-  // the slot of step s - 1, read step s, multiply.
+  // the slot of step s - 2, read step s, multiply.
   issue(0);
   if (nk > 1) issue(1);
   for (int step = 0; step < nk; ++step) {
-    if (step + 1 < nk) dma::wait_vmcnt<7>(); else dma::wait_vmcnt<0>();
+    if (step + 1 < nk) dma::wait_vmcnt<5>(); else dma::wait_vmcnt<0>();
     __syncthreads();
     if (step + 2 < nk) issue(step + 2);
     Frags f;
@@ -243,9 +251,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_tile256x128_kernel(SplitArgs
 // the dequantized products, with no per-block promote (each block's scale
 // rides in its codes' conversion).
 //
-// Same tiles, LDS ring, transfers and work order as gemm_tile256x128_kernel
-// (four waves of 128 x 64, two workgroups per CU); the 64-byte K step is four
-// bf16 instructions per 32 x 32 tile.  Instruction t of a step takes, in
+// Tiles of 256 x 128 (four waves of 128 x 64, two workgroups per CU: twice
+// the matrix-core time per byte of the fp8 kernel, so the half-size B tile
+// feeds it); a three-slot LDS ring two steps ahead, one barrier per step; the
+// 64-byte K step is four bf16 instructions per 32 x 32 tile.  Instruction t of a step takes, in
 // lane half h, bytes 32 (t >> 1) + 16 h + 8 (t & 1) .. + 7 of the lane's row
 // on both operands (so the four instructions cover the step's 64 positions
 // once each); those 8 bytes always lie in one block.  Scales per step: the
@@ -792,10 +801,11 @@ int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace 
     }
     return hipGetLastError();
   }
+  const int64_t items_big = pb.batch * pb.T * g.tiles_m * (g.tiles_n / 2);
   if (pb.block == 32)
-    hipLaunchKernelGGL(gemm_tile256x128_kernel<32>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+    hipLaunchKernelGGL(gemm_tile256x256_kernel<32>, dim3((unsigned)items_big), dim3(big::kThreadsB), 0, st, g);
   else
-    hipLaunchKernelGGL(gemm_tile256x128_kernel<128>, dim3((unsigned)items), dim3(kThreads), 0, st, g);
+    hipLaunchKernelGGL(gemm_tile256x256_kernel<128>, dim3((unsigned)items_big), dim3(big::kThreadsB), 0, st, g);
   return hipGetLastError();
 }
 

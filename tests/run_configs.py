@@ -30,8 +30,9 @@ Every configuration runs the path that meets the 1e-5 |C|_F element bar on
 its inputs: the fp8 matrix cores for C1-C3 (Gaussian and uniform operands),
 the exact-dot sub-products for C4 and C5 (heavy tails, four-decade row
 scales and general basis changes, where the fp8 dot product's group
-truncation exceeds it).  Timing: 2 warm-up and --reps timed whole steps per
-record (HIP events on the launch stream; median reported).
+truncation exceeds it).  Timing: at least 2 warm-up steps and 30 ms of GPU
+time, then --reps timed whole steps per record (HIP events on the launch
+stream; median reported).
 """
 from __future__ import annotations
 
@@ -63,9 +64,9 @@ def log(msg):
 def timed(f, dA, dB, C, reps):
     """Median event times (ms) of encode, sub-products, combine and the step."""
     import torch
-    from bench import time_steps
+    from bench import time_steps, warm_up
     stream = torch.cuda.current_stream()
-    time_steps(f, dA, dB, C, stream, 2)
+    warm_up(f, dA, dB, C, stream, 2, 30.0)
     t = time_steps(f, dA, dB, C, stream, reps)
     return {k: float(np.median(v)) for k, v in t.items()}
 
@@ -122,7 +123,7 @@ def run_arm(spec, real_handle, A, B, dA, dB, depth, bs, exact, reps, parity, rng
            "rel_rms_gpu": float(np.sqrt(err2.sum() / ref2.sum())),
            "mean_rel_fro_gpu": float(np.mean(np.sqrt(err2 / ref2))),
            "phi": fmm_realization_metrics(real_handle, depth)["phi"],
-           "path": ("exact-dot" if exact else "fp8") + (" 256x128 tiles + W-combine pass"
+           "path": ("exact-dot" if exact else "fp8") + (" large tiles + W-combine pass"
                                                        if layout == FMM_LAYOUT_TILE256x64 else " fused 128x128"),
            "parity": None}
     if parity == "full":
