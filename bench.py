@@ -408,7 +408,7 @@ def main():
     # the sub-product kernel the plan runs (layout and scale rule decide it)
     if split:
         prod_kernel = ("gemm_exact256x128_kernel" if sb == 4 else
-                       "gemm_dq256x128_kernel" if exact else "gemm_tile256x128_kernel")
+                       "gemm_dq256x128_kernel" if exact else "gemm_tile256x256_kernel")
     elif a_view.code_layout == 2:
         prod_kernel = "gemm_mx_fast_kernel" + (" (exact-dot form)" if exact else "")
     else:
