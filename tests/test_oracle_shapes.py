@@ -1,0 +1,124 @@
+"""The oracle for realizations of other shapes <m,k,n;R> (oracle/shapes.py),
+pinned to what the mathematics fixes: the Brent equations in exact
+arithmetic (and a perturbed coefficient fails them), the exact product on
+integer matrices with and without the quantizer (any index mistake in the
+grids or the cyclic third factor breaks it), Phi of a direct sum as the sum
+of the parts' Phi and of the cubic algorithm as mkn, agreement bit for bit
+with the <2,2,2> oracle, and the second-moment model of Appendix D
+(E|dC|^2 / E|C|^2 ~ 2 s_q^2 Phi / (m k n))."""
+import numpy as np
+import pytest
+
+import fmm_inputs as gen
+from oracle import e4m3, fmm, model, shapes
+from oracle import realizations as R
+
+
+def strassen():
+    return shapes.from_222(R.builtin_f64("strassen"))
+
+
+def shaped(name):
+    """The shapes the tests and the GPU path run (name -> realization)."""
+    if name == "222_strassen":
+        return strassen()
+    if name == "223_11":
+        return shapes.direct_sum(strassen(), shapes.cubic(2, 2, 1), "n")
+    if name == "322_11":
+        return shapes.direct_sum(strassen(), shapes.cubic(1, 2, 2), "m")
+    if name == "232_11":
+        return shapes.direct_sum(strassen(), shapes.cubic(2, 1, 2), "k")
+    if name == "223_tstar":
+        return shapes.direct_sum(shapes.from_222(R.builtin_f64("tstar")), shapes.cubic(2, 2, 1), "n")
+    if name == "333_27":
+        return shapes.cubic(3, 3, 3)
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("mkn", [(2, 2, 3), (3, 2, 2), (2, 3, 2), (3, 3, 3), (1, 2, 3), (2, 1, 1)])
+def test_cubic_is_exact_with_phi_mkn(mkn):
+    D = shapes.cubic(*mkn)
+    assert len(D[1]) == mkn[0] * mkn[1] * mkn[2]
+    assert shapes.brent_exact(D)
+    assert shapes.phi(D) == mkn[0] * mkn[1] * mkn[2]
+
+
+@pytest.mark.parametrize("name,shape,R_,phi", [("223_11", (2, 2, 3), 11, 36.0), ("322_11", (3, 2, 2), 11, 36.0),
+                                                ("232_11", (2, 3, 2), 11, 36.0),
+                                                ("223_tstar", (2, 2, 3), 11, 200 / 9 + 4)])
+def test_direct_sums_are_exact(name, shape, R_, phi):
+    D = shaped(name)
+    assert D[0] == shape and len(D[1]) == R_
+    if name != "223_tstar":          # T*'s entries are irrational in binary64; exactness there is to rounding
+        assert shapes.brent_exact(D)
+    assert shapes.phi(D) == pytest.approx(phi, rel=1e-13)
+
+
+def test_perturbed_direct_sum_fails_brent():
+    for part in (1, 2, 3):
+        D = shaped("223_11")
+        M = [list(r) for r in D[part]]
+        M[8][0] = 1 - M[8][0]                # flip one coefficient of a cubic term
+        D2 = list(D)
+        D2[part] = M
+        assert not shapes.brent_exact(tuple(D2))
+
+
+@pytest.mark.parametrize("name", ["223_11", "322_11", "232_11", "333_27"])
+def test_bilinear_map_is_the_product_on_integers(name):
+    D = shaped(name)
+    m, k, n = D[0]
+    rng = np.random.default_rng(7)
+    A = rng.integers(-9, 10, size=(m * 6, k * 5)).astype(np.float64)
+    B = rng.integers(-9, 10, size=(k * 5, n * 4)).astype(np.float64)
+    assert np.array_equal(shapes.exact_product(A, B, D), A @ B)
+
+
+@pytest.mark.parametrize("name", ["223_11", "322_11", "232_11"])
+@pytest.mark.parametrize("rule", [e4m3.RULE_POW2_CEIL, e4m3.RULE_POW2_OCP])
+def test_quantized_evaluation_exact_on_sign_operands(name, rule):
+    """With +-1 and 0 operands and +-1 coefficients every combination is a
+    small integer, exactly representable after either power-of-two scale, so
+    the whole fused evaluation (split, combine, quantize, products,
+    W-combine) must return A B exactly; a wrong block index anywhere breaks
+    it."""
+    D = shaped(name)
+    m, k, n = D[0]
+    rng = np.random.default_rng(11)
+    A = rng.integers(-1, 2, size=(m * 8, k * 64)).astype(np.float32)
+    B = rng.integers(-1, 2, size=(k * 64, n * 8)).astype(np.float32)
+    o = shapes.fmm_shape(A, B, D, 32, rule)
+    assert np.array_equal(o["C"], A.astype(np.float64) @ B.astype(np.float64))
+
+
+def test_agrees_with_the_222_oracle_bit_for_bit():
+    D = R.builtin_f64("strassen")
+    A, B = gen.operands("gaussian", 1, 128, 256, 192, seed=0, cfg=16, trial=0)
+    want = fmm.fmm(A[0], B[0], R.tables_f32(D, 1), 1, 32, e4m3.RULE_POW2_CEIL)
+    got = shapes.fmm_shape(A[0], B[0], shapes.from_222(D), 32, e4m3.RULE_POW2_CEIL)
+    assert np.array_equal(got["a"]["codes"], want["a"]["codes"])
+    assert np.array_equal(got["b"]["codes"], want["b"]["codes"])
+    assert np.array_equal(got["a"]["scales"], want["a"]["scales"])
+    assert np.array_equal(got["b"]["scales"], want["b"]["scales"])
+    assert np.array_equal(got["C"], want["C"])
+
+
+@pytest.mark.parametrize("name", ["223_11", "223_tstar", "333_27"])
+def test_model_predicts_measured(name):
+    """Appendix D's model with the measured noise coefficients predicts the
+    measured relative MSE within a few percent at shape <m,k,n> (mkn in place
+    of 8), and T* in the n-direct sum beats Strassen there as Phi says."""
+    D = shaped(name)
+    m, k, n = D[0]
+    errs, refs, sa, sb = [], [], [], []
+    for t in range(3):
+        A, B = gen.operands("gaussian", 1, 64 * m, 64 * k, 64 * n, seed=0, cfg=17, trial=t)
+        o = shapes.fmm_shape(A[0], B[0], D, 32, e4m3.RULE_POW2_CEIL)
+        e2, r2 = fmm.error_sums(o["C"], fmm.reference(A[0], B[0]))
+        errs.append(e2); refs.append(r2)
+        sa.append(model.noise_coefficient(o["a"]["x"], o["a"]["deq"]))
+        sb.append(model.noise_coefficient(o["b"]["x"], o["b"]["deq"]))
+    rel = np.sum(errs) / np.sum(refs)
+    s_a2, s_b2 = np.mean(sa), np.mean(sb)
+    pred = (s_a2 + s_b2 + s_a2 * s_b2) * shapes.phi(D) / (m * k * n)
+    assert pred / rel == pytest.approx(1.0, abs=0.06), (pred, rel)
