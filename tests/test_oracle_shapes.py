@@ -107,7 +107,7 @@ def test_agrees_with_the_222_oracle_bit_for_bit():
 def test_model_predicts_measured(name):
     """Appendix D's model with the measured noise coefficients predicts the
     measured relative MSE within a few percent at shape <m,k,n> (mkn in place
-    of 8), and T* in the n-direct sum beats Strassen there as Phi says."""
+    of 8)."""
     D = shaped(name)
     m, k, n = D[0]
     errs, refs, sa, sb = [], [], [], []
