@@ -118,12 +118,13 @@ enum {
   FMM_FLAG_LARGE_TILE = 8
 };
 
-typedef struct fmm_real fmm_real;   /* a base realization (U, V, w), R x 4 each, binary64 */
+typedef struct fmm_real fmm_real;   /* a base realization (U, V, w) of <m,k,n;R>, binary64 */
 typedef struct fmm_plan fmm_plan;   /* one problem shape bound to a realization */
 
 typedef struct {
   int64_t batch;   /* number of independent products, >= 0 */
-  int64_t M, K, N; /* each >= 0 and divisible by 2^depth; K / 2^depth divisible by block */
+  int64_t M, K, N; /* each >= 0 and divisible by 2^depth (by m, k, n for a realization of
+                    * another shape <m,k,n;R>); K / 2^depth (K / k) divisible by block */
   int32_t depth;   /* recursion (Kronecker) depth l: 1, 2 or 3 */
   int32_t block;   /* e4m3 block length along the contracted axis: 16, 32 or 128 */
   int32_t rule;    /* FMM_RULE_* */
@@ -145,8 +146,9 @@ enum {
    * M / 2^l and N / 2^l multiples of 256, K / 2^l a multiple of 64 (of 128
    * at block 128), and either the exact-dot path (fp32 scales, block 16, or
    * FMM_FLAG_EXACT_DOT) or E8M0 scales at block 32 or 128 on the fp8 matrix
-   * cores with K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE.  The B side is read as
-   * 128-row halves of these tiles. */
+   * cores with K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE; and every plan of a
+   * realization of another shape (rows M / m and N / n, kdim K / k).  The B
+   * side is read as 128-row halves of these tiles. */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
@@ -180,11 +182,19 @@ int fmm_realization_builtin(int which, fmm_real **out);
 
 /* A realization of <m,k,n;R> (Section 2.1: R rank-one terms of the matrix
  * multiplication tensor of an m x k by k x n product) from caller arrays U, V,
- * w, each R x (m k), R x (k n), R x (n m) row-major binary64 in the
- * conventions above.  The library runs <2,2,2;R>, 1 <= R <= 8: any other
- * m, k, n >= 1 returns FMM_ERR_UNSUPPORTED (m, k or n < 1: FMM_ERR_ARG).  If
- * the Brent residual max|sum_r U_r (x) V_r (x) w_r - <2,2,2>| exceeds tol the
- * call fails with FMM_ERR_NOT_EXACT (tol < 0 is FMM_ERR_ARG). */
+ * w, each R x (m k), R x (k n), R x (n m) row-major binary64: A is split into
+ * an m x k grid of sub-blocks, block (i, j) at index i k + j; B into a k x n
+ * grid, block (j, l) at j n + l; C block (i, l) takes w's index l m + i (the
+ * cyclic third factor of Appendix A; at <2,2,2> the conventions above).
+ * Exact means sum_r U_r[i k + j] V_r[j' n + l] w_r[l' m + i'] =
+ * [j = j'][l = l'][i = i'] (the Brent equations); if the largest deviation
+ * exceeds tol the call fails with FMM_ERR_NOT_EXACT (tol < 0 is FMM_ERR_ARG).
+ * <2,2,2;R> takes 1 <= R <= 8 and runs at depths 1 to 3.  Other shapes (the
+ * rows of Table E.1 beyond <2,2,2>) take m k, k n, n m <= 64 and
+ * 1 <= R <= 4096 (FMM_ERR_UNSUPPORTED for larger grids; m, k or n < 1 or R
+ * out of range: FMM_ERR_ARG) and run at depth 1 only, on the large-tile plans
+ * (FMM_LAYOUT_TILE256x64); the change of basis, the re-basing optimizer and
+ * its gradient are <2,2,2>'s (FMM_ERR_UNSUPPORTED for other shapes). */
 int fmm_realization_create(int m, int k, int n, int R, const double *U, const double *V,
                            const double *w, double tol, fmm_real **out);
 
@@ -199,7 +209,8 @@ int fmm_realization_transform(const fmm_real *d, const double X[4], const double
                               const double Z[4], fmm_real **out);
 
 /* The canonical rebalanced gauge (Appendix E.2):
- * (U_r, V_r, W_r) -> (U_r / s_r, s_r V_r, W_r), s_r = sqrt(|U_r| / |V_r|). */
+ * (U_r, V_r, W_r) -> (U_r / s_r, s_r V_r, W_r), s_r = sqrt(|U_r| / |V_r|)
+ * (terms with a zero U_r or V_r unchanged); any shape. */
 int fmm_realization_rebalance(const fmm_real *d, fmm_real **out);
 
 /* Re-basing (Section 3.1; the protocol of Appendix E.2): minimize Phi over
@@ -231,17 +242,23 @@ int fmm_realization_phi_gradient(const fmm_real *d, const double g[12], double *
 
 /* Phi = sum_r |U_r|^2 |V_r|^2 |W_r|^2 and Gamma = sum_r |U_r||V_r||W_r|
  * (Section 2.1) of the depth-l flattening (Phi^l, Gamma^l), and the Brent
- * residual of the base realization.  Any output pointer may be NULL. */
+ * residual of the base realization.  Any output pointer may be NULL.  Other
+ * shapes than <2,2,2>: depth 1 only (FMM_ERR_UNSUPPORTED otherwise). */
 int fmm_realization_metrics(const fmm_real *d, int depth, double *phi, double *gamma,
                             double *brent_resid);
 
-/* R (base rank) and T = R^depth. */
+/* R (base rank) and T = R^depth (other shapes: depth 1 only, as above). */
 int fmm_realization_terms(const fmm_real *d, int depth, int64_t *rank, int64_t *terms);
 
-/* The base coefficients, R x 4 binary64 each (any pointer may be NULL). */
+/* The shape <m,k,n> and rank R of a realization (any pointer may be NULL). */
+int fmm_realization_shape(const fmm_real *d, int *m, int *k, int *n, int *R);
+
+/* The base coefficients, R x (m k), R x (k n), R x (n m) binary64 (R x 4 each
+ * at <2,2,2>; any pointer may be NULL). */
 int fmm_realization_coefficients(const fmm_real *d, double *U, double *V, double *w);
 
-/* The exact fp32 depth-l tables the kernels use, T x 4^l each. */
+/* The exact fp32 depth-l tables the kernels use, T x 4^l each (other shapes:
+ * depth 1, R x (m k), R x (k n), R x (n m), each entry rounded once). */
 int fmm_realization_tables(const fmm_real *d, int depth, float *U, float *V, float *w);
 
 void fmm_realization_destroy(fmm_real *d);
@@ -250,7 +267,14 @@ void fmm_realization_destroy(fmm_real *d);
 
 /* Validates desc (FMM_ERR_ARG / FMM_ERR_SHAPE / FMM_ERR_UNSUPPORTED are
  * returned before any device call), then uploads the coefficient tables to
- * the current device (FMM_ERR_DEVICE if it is not gfx950). */
+ * the current device (FMM_ERR_DEVICE if it is not gfx950).
+ * A realization of another shape <m,k,n;R> splits A into m x k sub-blocks of
+ * M / m x K / k, B into k x n of K / k x N / n, and runs at depth 1 on the
+ * large-tile path only: M / m and N / n multiples of 256 and K / k a multiple
+ * of 64 (of 128 at block 128), with no flags but FMM_FLAG_EXACT_DOT and
+ * FMM_FLAG_LARGE_TILE; anything else is FMM_ERR_UNSUPPORTED (dimensions not
+ * divisible by m, k, n or K / k by block: FMM_ERR_SHAPE).  Such plans have
+ * no operand-noise or cross-term pass (FMM_ERR_UNSUPPORTED). */
 int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out);
 
 /* Bytes of device workspace fmm_encode/fmm_multiply/fmm_matmul need: the

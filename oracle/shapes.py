@@ -15,10 +15,11 @@ Then C block (i, l) = sum_r W_r[l m + i] P_r with P_r = (sum_b U_r[b] A_b)
 oracle/realizations.py (2i + j, 2j + k, 2k + i).
 
 The paper tabulates errors for decompositions of other shapes (Table E.1)
-whose coefficients are not printed.  The shapes here are built from exact
-pieces: the cubic algorithm of any shape, and direct sums along one
-dimension (C = A [B1 B2] = [A B1, A B2] along n, and the like along m and
-k), e.g. <2,2,3;11> = Strassen (x) cubic <2,2,1;4> along n.
+whose coefficients are not printed.  The realizations run here are inputs
+(fmm_inputs/shapes.py builds them from the cubic algorithm and direct sums,
+e.g. <2,2,3;11> = Strassen (+) cubic <2,2,1;4> along n); this module checks
+them (the Brent equations in exact arithmetic) and evaluates them.
+A realization is ((m, k, n), U, V, W) with U, V, W arrays of R rows.
 
 The evaluation follows oracle/fmm.py step by step (fp32 combination in
 ascending block index, no fused multiply-add; quantization along the
@@ -32,73 +33,6 @@ from fractions import Fraction
 import numpy as np
 
 from . import e4m3, fmm
-
-
-def cubic(m: int, k: int, n: int):
-    """The cubic <m,k,n; mkn> algorithm: term (i, j, l) in lexicographic order
-    multiplies A block (i, j) by B block (j, l) into C block (i, l)."""
-    U, V, W = [], [], []
-    for i in range(m):
-        for j in range(k):
-            for l in range(n):
-                u = [0] * (m * k); u[i * k + j] = 1
-                v = [0] * (k * n); v[j * n + l] = 1
-                w = [0] * (n * m); w[l * m + i] = 1
-                U.append(u); V.append(v); W.append(w)
-    return (m, k, n), U, V, W
-
-
-def from_222(D):
-    """A <2,2,2> realization (U, V, w lists of rows) in this module's form."""
-    U, V, W = D
-    return (2, 2, 2), [list(r) for r in U], [list(r) for r in V], [list(r) for r in W]
-
-
-def direct_sum(D1, D2, axis: str):
-    """<m,k,n1+n2> from <m,k,n1> and <m,k,n2> (axis 'n': C = A [B1 B2]),
-    <m1+m2,k,n> (axis 'm': C = [A1; A2] B) or <m,k1+k2,n> (axis 'k':
-    C = A1 B1 + A2 B2): the terms of D1 followed by those of D2, each
-    re-indexed into the larger grids."""
-    (m1, k1, n1), U1, V1, W1 = D1
-    (m2, k2, n2), U2, V2, W2 = D2
-    if axis == "n":
-        assert (m1, k1) == (m2, k2)
-        m, k, n = m1, k1, n1 + n2
-        a_map = lambda part, i, j: (i, j)
-        b_map = lambda part, j, l: (j, l + (0 if part == 0 else n1))
-        c_map = lambda part, i, l: (i, l + (0 if part == 0 else n1))
-    elif axis == "m":
-        assert (k1, n1) == (k2, n2)
-        m, k, n = m1 + m2, k1, n1
-        a_map = lambda part, i, j: (i + (0 if part == 0 else m1), j)
-        b_map = lambda part, j, l: (j, l)
-        c_map = lambda part, i, l: (i + (0 if part == 0 else m1), l)
-    elif axis == "k":
-        assert (m1, n1) == (m2, n2)
-        m, k, n = m1, k1 + k2, n1
-        a_map = lambda part, i, j: (i, j + (0 if part == 0 else k1))
-        b_map = lambda part, j, l: (j + (0 if part == 0 else k1), l)
-        c_map = lambda part, i, l: (i, l)
-    else:
-        raise ValueError(axis)
-    U, V, W = [], [], []
-    for part, ((mm, kk, nn), Us, Vs, Ws) in enumerate((D1, D2)):
-        for u, v, w in zip(Us, Vs, Ws):
-            nu = [0] * (m * k); nv = [0] * (k * n); nw = [0] * (n * m)
-            for i in range(mm):
-                for j in range(kk):
-                    I, J = a_map(part, i, j)
-                    nu[I * k + J] = u[i * kk + j]
-            for j in range(kk):
-                for l in range(nn):
-                    J, L = b_map(part, j, l)
-                    nv[J * n + L] = v[j * nn + l]
-            for i in range(mm):
-                for l in range(nn):
-                    I, L = c_map(part, i, l)
-                    nw[L * m + I] = w[l * mm + i]
-            U.append(nu); V.append(nv); W.append(nw)
-    return (m, k, n), U, V, W
 
 
 def brent_exact(D) -> bool:

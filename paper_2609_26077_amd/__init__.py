@@ -98,6 +98,8 @@ _SIGS = {
     "fmm_realization_metrics": (ctypes.c_int, [_vp, ctypes.c_int, _dp, _dp, _dp]),
     "fmm_realization_terms": (ctypes.c_int, [_vp, ctypes.c_int, ctypes.POINTER(_i64),
                                              ctypes.POINTER(_i64)]),
+    "fmm_realization_shape": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int),
+                                             ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]),
     "fmm_realization_coefficients": (ctypes.c_int, [_vp, _dp, _dp, _dp]),
     "fmm_realization_tables": (ctypes.c_int, [_vp, ctypes.c_int, _fp, _fp, _fp]),
     "fmm_realization_destroy": (None, [_vp]),
@@ -208,7 +210,8 @@ def _darr(a, n):
 
 def fmm_realization_create(U, V, w, tol: float = 1e-9, shape=(2, 2, 2)) -> Realization:
     """A realization of <m,k,n;R> from R x mk, R x kn, R x nm coefficient
-    arrays; shape = (m, k, n) (the library runs (2, 2, 2) only)."""
+    arrays; shape = (m, k, n).  Shapes other than (2, 2, 2) run at depth 1
+    on the large-tile plans only."""
     import numpy as np
     m, k, n = (int(x) for x in shape)
     R = int(np.asarray(U).shape[0])
@@ -282,10 +285,18 @@ def fmm_realization_terms(d: Realization, depth: int = 1):
     return R.value, T.value
 
 
+def fmm_realization_shape(d: Realization):
+    """((m, k, n), R)."""
+    m, k, n, R = (ctypes.c_int() for _ in range(4))
+    _check(_lib.fmm_realization_shape(d.handle, ctypes.byref(m), ctypes.byref(k), ctypes.byref(n),
+                                      ctypes.byref(R)), "fmm_realization_shape")
+    return (m.value, k.value, n.value), R.value
+
+
 def fmm_realization_coefficients(d: Realization):
     import numpy as np
-    R, _ = fmm_realization_terms(d, 1)
-    U, V, W = (np.zeros((R, 4)) for _ in range(3))
+    (m, k, n), R = fmm_realization_shape(d)
+    U, V, W = np.zeros((R, m * k)), np.zeros((R, k * n)), np.zeros((R, n * m))
     _check(_lib.fmm_realization_coefficients(d.handle, U.ctypes.data_as(_dp),
                                              V.ctypes.data_as(_dp), W.ctypes.data_as(_dp)),
            "fmm_realization_coefficients")
@@ -295,8 +306,11 @@ def fmm_realization_coefficients(d: Realization):
 def fmm_realization_tables(d: Realization, depth: int = 1):
     import numpy as np
     _, T = fmm_realization_terms(d, depth)
-    nb = 4 ** depth
-    U, V, W = (np.zeros((T, nb), dtype=np.float32) for _ in range(3))
+    (m, k, n), _ = fmm_realization_shape(d)
+    if (m, k, n) == (2, 2, 2):
+        U, V, W = (np.zeros((T, 4 ** depth), dtype=np.float32) for _ in range(3))
+    else:
+        U, V, W = (np.zeros((T, c), dtype=np.float32) for c in (m * k, k * n, n * m))
     _check(_lib.fmm_realization_tables(d.handle, depth, U.ctypes.data_as(_fp),
                                        V.ctypes.data_as(_fp), W.ctypes.data_as(_fp)),
            "fmm_realization_tables")

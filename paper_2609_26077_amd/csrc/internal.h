@@ -9,6 +9,8 @@
 namespace fmm {
 
 constexpr int kMaxRank = 8;    // <2,2,2;R>, R <= 8 (cubic has 8 terms)
+constexpr int kMaxRankShape = 4096;  // other shapes <m,k,n;R>: R <= 4096
+constexpr int kMaxGridBlocks = 64;   // other shapes: mk, kn, nm <= 64 (the encoder's and combine's widest grid)
 constexpr int kMaxDepth = 3;
 constexpr int kSplitTile = 256;  // A rows per tile of the large-tile sub-product path (and code image rows)
 constexpr int kSplitTileN = 128; // B rows per tile of that path (half a code image)
@@ -35,6 +37,15 @@ int realization_optimize(const Realization &D, int nstarts, const double *starts
                          double gtol, double tol, Realization &best, double &best_phi, double *start_phi);
 void flatten(const double (*base)[4], int R, int depth, float *out);
 
+// A realization of another shape <m,k,n;R>: U R x mk (block i k + j), V R x kn
+// (block j n + l), W R x nm (block l m + i), row-major binary64.
+struct Shaped {
+  int m, k, n, R;
+  const double *U, *V, *W;
+};
+double brent_residual_shape(const Shaped &s);
+void phi_gamma_shape(const Shaped &s, double &phi, double &gamma);
+
 // ---- device-side coefficient tables -------------------------------------
 // For one operand side: the nonzero coefficients of each flattened term in
 // ascending sub-block order.  offsets[r] .. offsets[r+1] index entries.
@@ -59,7 +70,16 @@ struct Problem {
   int layout;              // FMM_LAYOUT_* of the workspace's codes and scales
   int b_rows;              // rows of y_r^T per B scale block: 1, or 128 (FMM_FLAG_B_BLOCK128)
   int b_bf16;              // round encoded B combinations to bfloat16 first (FMM_FLAG_B_BF16)
+  // the sub-block grid: A gm x gk, B gk x gn, C gm x gn (2^l each for
+  // <2,2,2> plans; m, k, n for a realization of another shape, whose plans
+  // set `shaped` and run at one level on the large-tile path)
+  int gm, gk, gn;
+  int shaped;
 };
+
+// The dense coefficient rows of a plan of another shape are padded with zeros
+// to 16 or 64 entries (the encoder's and the W-combine's grid capacities).
+inline int grid_capacity(int blocks) { return blocks <= 16 ? 16 : 64; }
 
 // Large-tile plans whose sub-products take an exact-dot kernel (fp32 scales,
 // block 16, or the exact-dot flag): the promote kernel for fp32 scales, the
@@ -87,9 +107,12 @@ struct DeviceTables {
   const CoefEntry *b_ent;
   const float *w_inner;        // R x 4 fp32 base w (the inner-level decoder), zero-padded to kMaxRank x 4
   const float *w_outer;        // To x 4^(l-1) fp32 flattened depth-(l-1) w (depth >= 2)
-  const float *w_full;         // T x 16 fp32 flattened depth-2 w (large-tile plans at depth 2)
-  const float *u_dense;        // T x 4^l fp32 flattened U, zeros included
-  const float *v_dense;        // T x 4^l fp32 flattened V, zeros included
+  const float *w_full;         // T x 16 fp32 flattened depth-2 w (large-tile plans at depth 2);
+                               // other shapes: T x grid_capacity(gm gn), w index l gm + i
+  const float *u_dense;        // T x 4^l fp32 flattened U, zeros included (other shapes:
+                               // T x grid_capacity(gm gk))
+  const float *v_dense;        // T x 4^l fp32 flattened V, zeros included (other shapes:
+                               // T x grid_capacity(gk gn))
 };
 
 // ---- launchers (kernels_*.hip); return a hipError_t as int ---------------

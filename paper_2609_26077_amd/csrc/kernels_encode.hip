@@ -107,12 +107,17 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
 // sub-product kernel reads next, from the caches), except where a tile takes
 // only part of each cache line (B tiles narrower than 32 columns).  Positions
 // outside the operand read as zero.
+// GEN: a realization of another shape, whose A grid is gm x gk and B grid
+// gk x gn (at most NB blocks; the others are neither read nor used).
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-template <int SIDE, int NB, int TR, int NT, int TL = kTL>
+template <int SIDE, int NB, int TR, int NT, int TL = kTL, bool GEN = false>
 __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__ src, const Problem &pb,
                                            int64_t bt, int64_t row0, int64_t l0, int t) {
-  constexpr int n = NB == 4 ? 2 : NB == 16 ? 4 : 8;
+  constexpr int nc = NB == 4 ? 2 : NB == 16 ? 4 : 8;
+  // blocks per grid row (A: gk columns of A's grid; B: gn) and blocks in all
+  const int n = GEN ? (SIDE == 0 ? pb.gk : pb.gn) : nc;
+  const int nbr = GEN ? (SIDE == 0 ? pb.gm * pb.gk : pb.gk * pb.gn) : NB;
   constexpr int kStr = TL + 4;
   constexpr int kPer = NB * TR * (TL / 4) / NT;       // float4s per thread
   static_assert(NB * TR * (TL / 4) % NT == 0, "the tile splits evenly over the threads");
@@ -129,7 +134,7 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
       const int rem = e % (TR * (TL / 4));
       const int64_t p = row0 + rem / (TL / 4), l = l0 + 4 * (rem % (TL / 4));
       stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (p < rows && l < kp) {
+      if ((!GEN || b < nbr) && p < rows && l < kp) {
         const int I = b / n, J = b % n;
         const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(Ab + (I * pb.mp + p) * pb.K + J * kp + l));
         stage[k] = make_float4(x.x, x.y, x.z, x.w);
@@ -153,7 +158,7 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
       const int rem = e % (TR * (TL / 4));
       const int64_t qq = row0 + rem % TR, l = l0 + 4 * (rem / TR);
       stage[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (qq < rows && l < kp) {
+      if ((!GEN || b < nbr) && qq < rows && l < kp) {
         const int J = b / n, Kb = b % n;
         const float *p = Bb + (J * kp + l) * pb.N + Kb * pb.np + qq;
         if constexpr (TR < 32) {
@@ -277,7 +282,7 @@ constexpr bool narrow_b(int side, int depth, int bs, int mode) {
   return side == 1 && depth == 2 && bs <= 32 && mode == 0;
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE>
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE, bool GEN = false>
 __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l, void *__restrict__ aux) {
@@ -302,7 +307,7 @@ __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MO
   const int64_t row0 = (qfast ? blockIdx.x % tiles_r : blockIdx.x / tiles_l) * TR;
   const int64_t l0 = (qfast ? blockIdx.x / tiles_r : blockIdx.x % tiles_l) * TL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  stage_tile<SIDE, NB, TR, NT, TL>(lds, src, pb, bt, row0, l0, t);
+  stage_tile<SIDE, NB, TR, NT, TL, GEN>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
 
   const int lane = t & 63;
@@ -529,7 +534,7 @@ __device__ __forceinline__ uint32_t quantize4(const Problem &pb, float m, float 
 
 constexpr bool narrow_b3(int side, int bs) { return side == 1 && bs <= 256 / kB3Rows; }
 
-template <int SIDE, int BS, bool F32>
+template <int SIDE, int BS, bool F32, bool GEN = false>
 __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) void encode4_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
@@ -545,7 +550,7 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) v
   const int64_t row0 = (blockIdx.x / tiles_l) * TR;
   const int64_t l0 = (blockIdx.x % tiles_l) * TL;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-  stage_tile<SIDE, TT::nblk, TR, NT, TL>(lds, src, pb, bt, row0, l0, t);
+  stage_tile<SIDE, TT::nblk, TR, NT, TL, GEN>(lds, src, pb, bt, row0, l0, t);
   __syncthreads();
 
   const int64_t T = pb.T;
@@ -611,7 +616,7 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) v
   }
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0>
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0, bool GEN = false>
 hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
                     uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
   using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>;
@@ -619,8 +624,8 @@ hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
   const int64_t tiles_l = (pb.kp + TT::TL - 1) / TT::TL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE>), grid, dim3(TT::threads), 0, st, src, pb, cf, codes,
-                     scales, tiles_l, amax);
+  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE, GEN>), grid, dim3(TT::threads), 0, st, src, pb, cf,
+                     codes, scales, tiles_l, amax);
   return hipGetLastError();
 }
 
@@ -660,55 +665,67 @@ hipError_t launch_b_deploy_any(const Problem &pb, const float *src, const SideTa
   return hipErrorInvalidValue;
 }
 
-template <int SIDE, int DEPTH>
+template <int SIDE, int DEPTH, bool GEN = false>
 hipError_t launch_wide(const Problem &pb, const float *src, const SideTab &cf,
                        uint8_t *codes, uint8_t *scales, hipStream_t st) {
   const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
   switch (pb.block) {
-    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true>(pb, src, cf, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 16, false>(pb, src, cf, codes, scales, st);
-    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true>(pb, src, cf, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 32, false>(pb, src, cf, codes, scales, st);
-    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true>(pb, src, cf, codes, scales, st)
-                         : launch16<SIDE, DEPTH, 128, false>(pb, src, cf, codes, scales, st);
+    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 0, GEN>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 16, false, 0, GEN>(pb, src, cf, codes, scales, st);
+    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 0, GEN>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 32, false, 0, GEN>(pb, src, cf, codes, scales, st);
+    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 0, GEN>(pb, src, cf, codes, scales, st)
+                         : launch16<SIDE, DEPTH, 128, false, 0, GEN>(pb, src, cf, codes, scales, st);
   }
   return hipErrorInvalidValue;
+}
+
+// 4 positions per lane over a grid of up to 64 blocks (depth 3, or GEN)
+template <int SIDE, bool GEN = false>
+hipError_t launch_narrow4(const Problem &pb, const float *src, const SideTab &cf,
+                          uint8_t *codes, uint8_t *scales, hipStream_t st) {
+  const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
+  // the B side's tile at blocks <= 256 / kB3Rows (its narrow form), else the common one
+  const bool nar = SIDE == 1 && pb.block <= 256 / kB3Rows;
+  const int TL = nar ? Tile<3, 4, 1, true>::TL : kTL, TR = nar ? Tile<3, 4, 1, true>::TR : Tile<3, 4, SIDE>::TR;
+  const int64_t tiles_l = (pb.kp + TL - 1) / TL;
+  const int64_t tiles_r = (rows + TR - 1) / TR;
+  const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
+  const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
+  const dim3 blk(Tile<3, 4, SIDE>::threads);
+  switch (pb.block) {
+    case 16:
+      if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 16, true, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      else hipLaunchKernelGGL((encode4_kernel<SIDE, 16, false, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      break;
+    case 32:
+      if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 32, true, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      else hipLaunchKernelGGL((encode4_kernel<SIDE, 32, false, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      break;
+    case 128:
+      if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 128, true, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      else hipLaunchKernelGGL((encode4_kernel<SIDE, 128, false, GEN>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int SIDE>
 hipError_t launch_side(const Problem &pb, const float *src, const SideTab &cf,
                        uint8_t *codes, uint8_t *scales, hipStream_t st) {
+  if (pb.shaped) {
+    // another shape: the depth-2 tile (16 positions per lane) over a grid of
+    // up to 16 blocks, the depth-3 one (4 per lane) over up to 64
+    const int nb = SIDE == 0 ? pb.gm * pb.gk : pb.gk * pb.gn;
+    return nb <= 16 ? launch_wide<SIDE, 2, true>(pb, src, cf, codes, scales, st)
+                    : launch_narrow4<SIDE, true>(pb, src, cf, codes, scales, st);
+  }
   switch (pb.depth) {
     case 1: return launch_wide<SIDE, 1>(pb, src, cf, codes, scales, st);
     case 2: return launch_wide<SIDE, 2>(pb, src, cf, codes, scales, st);
-    case 3: {
-      const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
-      // the B side's tile at blocks <= 256 / kB3Rows (its narrow form), else the common one
-      const bool nar = SIDE == 1 && pb.block <= 256 / kB3Rows;
-      const int TL = nar ? Tile<3, 4, 1, true>::TL : kTL, TR = nar ? Tile<3, 4, 1, true>::TR : Tile<3, 4, SIDE>::TR;
-      const int64_t tiles_l = (pb.kp + TL - 1) / TL;
-      const int64_t tiles_r = (rows + TR - 1) / TR;
-      const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-      const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
-      const dim3 blk(Tile<3, 4, SIDE>::threads);
-      switch (pb.block) {
-        case 16:
-          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 16, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          else hipLaunchKernelGGL((encode4_kernel<SIDE, 16, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          break;
-        case 32:
-          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 32, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          else hipLaunchKernelGGL((encode4_kernel<SIDE, 32, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          break;
-        case 128:
-          if (f32) hipLaunchKernelGGL((encode4_kernel<SIDE, 128, true>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          else hipLaunchKernelGGL((encode4_kernel<SIDE, 128, false>), grid, blk, 0, st, src, pb, cf, codes, scales, tiles_l);
-          break;
-        default:
-          return hipErrorInvalidValue;
-      }
-      return hipGetLastError();
-    }
+    case 3: return launch_narrow4<SIDE>(pb, src, cf, codes, scales, st);
   }
   return hipErrorInvalidValue;
 }

@@ -719,7 +719,9 @@ __global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__
 // w[r][4K + I] P_r[p][4 q4 ..], ascending r, fma per nonzero weight, with the
 // 16 blocks' accumulators in registers so that every P_r is read once.  The
 // weights are uniform over the grid (scalar loads).
-template <bool VEC>
+// GEN: a realization of another shape with gm gn <= 16 C blocks, block (I, L)
+// at w index L gm + I of a row padded to 16; K = 0 leaves C zero.
+template <bool VEC, bool GEN = false>
 __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__ P, const float *__restrict__ w,
                                                        float *__restrict__ C, Problem pb) {
   const int64_t n4 = pb.np / 4;
@@ -732,7 +734,7 @@ __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__
   float4 acc[16];
 #pragma unroll
   for (int b = 0; b < 16; ++b) acc[b] = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int T = (int)pb.T;
+  const int T = (GEN && pb.kp == 0) ? 0 : (int)pb.T;
   // eight terms' loads are issued together, ahead of the (uniformly branching)
   // multiply-adds; past the last term the index is clamped and the load unused
   for (int r0 = 0; r0 < T; r0 += 8) {
@@ -763,7 +765,8 @@ __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__
   }
 #pragma unroll
   for (int b = 0; b < 16; ++b) {
-    const int i = b & 3, k = b >> 2;
+    if (GEN && b >= pb.gm * pb.gn) continue;     // (uniform; a full unroll keeps acc in registers)
+    const int i = GEN ? b % pb.gm : b & 3, k = GEN ? b / pb.gm : b >> 2;
     float *dst = C + bt * pb.M * pb.N + (i * pb.mp + p) * pb.N + k * pb.np + 4 * q4;
     if (VEC) {
       *reinterpret_cast<float4 *>(dst) = acc[b];
@@ -773,10 +776,53 @@ __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__
   }
 }
 
+// Another shape with 16 < gm gn <= 64 C blocks: one output column per thread
+// (row p, column q of every block), the blocks' 64 accumulators in registers
+// so that every P_r is read once; otherwise as combine2_kernel's GEN form.
+__global__ __launch_bounds__(256) void combine64_kernel(const float *__restrict__ P, const float *__restrict__ w,
+                                                        float *__restrict__ C, Problem pb) {
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // p * np + q
+  const int64_t bt = blockIdx.y;
+  if (pos >= pb.mp * pb.np) return;
+  const int64_t p = pos / pb.np, q = pos - p * pb.np;
+  const int64_t plane = pb.mp * pb.np;
+  const float *src = P + bt * pb.T * plane + pos;
+  float acc[64];
+#pragma unroll
+  for (int b = 0; b < 64; ++b) acc[b] = 0.0f;
+  const int T = pb.kp == 0 ? 0 : (int)pb.T;
+  for (int r0 = 0; r0 < T; r0 += 8) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int r = min(r0 + j, T - 1);
+      x[j] = __builtin_nontemporal_load(src + r * plane);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (r0 + j < T) {
+#pragma unroll
+        for (int b = 0; b < 64; ++b) {
+          const float wb = w[64 * (r0 + j) + b];
+          if (wb != 0.0f) acc[b] = __fmaf_rn(wb, x[j], acc[b]);
+        }
+      }
+    }
+  }
+  const int nbc = pb.gm * pb.gn;
+#pragma unroll
+  for (int b = 0; b < 64; ++b) {
+    if (b >= nbc) continue;
+    const int i = b % pb.gm, l = b / pb.gm;
+    C[bt * pb.M * pb.N + (i * pb.mp + p) * pb.N + l * pb.np + q] = acc[b];
+  }
+}
+
 }  // namespace
 
 int launch_products_split(const Problem &pb, const uint8_t *ws, const Workspace &wl, void *stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (pb.kp == 0) return hipSuccess;    // plans of other shapes with K = 0: the W-combine writes C = 0
   SplitArgs g;
   g.xa = ws + wl.a_codes;
   g.xb = ws + wl.b_codes;
@@ -816,6 +862,17 @@ int launch_combine_split(const Problem &pb, const DeviceTables &tab, const uint8
   const int64_t npos = pb.mp * (pb.np / 4);
   const dim3 g2((unsigned)((npos + 255) / 256), (unsigned)pb.batch);
   const bool vec = (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+  if (pb.shaped) {
+    if (pb.gm * pb.gn > 16) {
+      const dim3 g1((unsigned)((pb.mp * pb.np + 255) / 256), (unsigned)pb.batch);
+      hipLaunchKernelGGL(combine64_kernel, g1, dim3(256), 0, st, P, tab.w_full, C, pb);
+    } else if (vec) {
+      hipLaunchKernelGGL((combine2_kernel<true, true>), g2, dim3(256), 0, st, P, tab.w_full, C, pb);
+    } else {
+      hipLaunchKernelGGL((combine2_kernel<false, true>), g2, dim3(256), 0, st, P, tab.w_full, C, pb);
+    }
+    return hipGetLastError();
+  }
   if (pb.depth == 2) {
     if (vec)
       hipLaunchKernelGGL(combine2_kernel<true>, g2, dim3(256), 0, st, P, tab.w_full, C, pb);

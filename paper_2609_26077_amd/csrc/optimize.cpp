@@ -326,8 +326,12 @@ namespace {
 
 // the base realization behind a handle, read through the C-ABI
 int realization_of(const fmm_real *d, fmm::Realization &D) {
+  int m = 0, k = 0, n = 0, Rs = 0;
+  int st = fmm_realization_shape(d, &m, &k, &n, &Rs);
+  if (st != FMM_OK) return st;
+  if (m != 2 || k != 2 || n != 2) return FMM_ERR_UNSUPPORTED;   // the orbit under GL(2)^3 is <2,2,2>'s
   int64_t R = 0, T = 0;
-  const int st = fmm_realization_terms(d, 1, &R, &T);
+  st = fmm_realization_terms(d, 1, &R, &T);
   if (st != FMM_OK) return st;
   std::memset(&D, 0, sizeof(D));
   D.R = (int)R;

@@ -73,9 +73,16 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if (q.depth < 1 || q.depth > fmm::kMaxDepth) return FMM_ERR_ARG;
   if (q.block != 16 && q.block != 32 && q.block != 128) return FMM_ERR_ARG;
   if (q.rule < FMM_RULE_FP32_AMAX || q.rule > FMM_RULE_POW2_OCP) return FMM_ERR_ARG;
+  int sm = 2, sk = 2, sn = 2, sR = 0;
+  if (fmm_realization_shape(d, &sm, &sk, &sn, &sR) != FMM_OK) return FMM_ERR_ARG;
+  const bool shaped = !(sm == 2 && sk == 2 && sn == 2);
+  if (shaped && (q.depth != 1 || (q.flags & (FMM_FLAG_B_BLOCK128 | FMM_FLAG_B_BF16))))
+    return FMM_ERR_UNSUPPORTED;
+  // the sub-block grid: 2^l x 2^l at <2,2,2>, m x k by k x n for other shapes
   const int64_t n = int64_t(1) << q.depth;
-  if (q.M % n || q.K % n || q.N % n) return FMM_ERR_SHAPE;
-  if ((q.K / n) % q.block) return FMM_ERR_SHAPE;
+  const int64_t gm = shaped ? sm : n, gk = shaped ? sk : n, gn = shaped ? sn : n;
+  if (q.M % gm || q.K % gk || q.N % gn) return FMM_ERR_SHAPE;
+  if ((q.K / gk) % q.block) return FMM_ERR_SHAPE;
   // grid limits of the launches (batch on grid z/y, terms on grid y)
   if (q.batch > 65535) return FMM_ERR_UNSUPPORTED;
   // the weight-side deployment granularity is built for one level
@@ -83,21 +90,9 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
 
   // the realization, as the C-ABI sees it
   int64_t R = 0, T = 0;
-  if (fmm_realization_terms(d, q.depth, &R, &T) != FMM_OK) return FMM_ERR_ARG;
+  const int rst = fmm_realization_terms(d, q.depth, &R, &T);
+  if (rst != FMM_OK) return rst;
 
-  fmm_plan *p = new (std::nothrow) fmm_plan;
-  if (!p) return FMM_ERR_NOMEM;
-  fmm::Problem &pb = p->pb;
-  pb.batch = q.batch; pb.M = q.M; pb.K = q.K; pb.N = q.N;
-  pb.depth = q.depth; pb.nsplit = (int)n;
-  pb.mp = q.M / n; pb.kp = q.K / n; pb.np = q.N / n;
-  pb.block = q.block; pb.rule = q.rule;
-  pb.R = (int)R; pb.T = T; pb.To = fmm::ipow(R, q.depth - 1);
-  pb.kblocks = pb.kp / q.block;
-  pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
-  pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
-  pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
-  pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
   // large-tile path: one or two levels, 256-row tiles, whole 64-byte (blocks
   // 16, 32) or 128-byte (block 128) K steps; E8M0 scales at blocks 32 and 128
   // on the fp8 matrix cores or (exact-dot flag) the folded-scale bf16 kernel,
@@ -108,15 +103,36 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   // tiles, k' >= 1024 (measured on both forms: the large tiles win at 1024
   // and above, lose at 512 and below); fp32 scales and block 16 whenever the
   // shape allows (their fused promote kernel is slower at every measured k').
-  const bool split_shape = q.depth <= 2 && pb.mp % fmm::kSplitTile == 0 && pb.np % fmm::kSplitTile == 0 &&
-             pb.kp > 0 && pb.kp % (q.block == 128 ? 128 : 64) == 0 && pb.kp < (int64_t(1) << 26) &&
-             q.batch * T * (pb.mp / fmm::kSplitTile) * (pb.np / fmm::kSplitTileN) < (int64_t(1) << 31);
+  // Plans of other shapes take it always (their W-combine fans each P_r out
+  // to up to m n blocks of C), K = 0 included (C is then zero).
+  const int64_t mp = q.M / gm, kp = q.K / gk, np = q.N / gn;
+  const bool tiles_fit = mp % fmm::kSplitTile == 0 && np % fmm::kSplitTile == 0 &&
+                         kp % (q.block == 128 ? 128 : 64) == 0 && kp < (int64_t(1) << 26) &&
+                         q.batch * T * (mp / fmm::kSplitTile) * (np / fmm::kSplitTileN) < (int64_t(1) << 31);
+  if (shaped && !tiles_fit) return FMM_ERR_UNSUPPORTED;
+  const bool split_shape = q.depth <= 2 && kp > 0 && tiles_fit;
+
+  fmm_plan *p = new (std::nothrow) fmm_plan;
+  if (!p) return FMM_ERR_NOMEM;
+  fmm::Problem &pb = p->pb;
+  pb.batch = q.batch; pb.M = q.M; pb.K = q.K; pb.N = q.N;
+  pb.depth = q.depth; pb.nsplit = (int)n;
+  pb.mp = mp; pb.kp = kp; pb.np = np;
+  pb.gm = (int)gm; pb.gk = (int)gk; pb.gn = (int)gn;
+  pb.shaped = shaped ? 1 : 0;
+  pb.block = q.block; pb.rule = q.rule;
+  pb.R = (int)R; pb.T = T; pb.To = fmm::ipow(R, q.depth - 1);
+  pb.kblocks = pb.kp / q.block;
+  pb.scale_bytes = q.rule == FMM_RULE_FP32_AMAX ? 4 : 1;
+  pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
+  pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
+  pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
   // E8M0 scales at blocks 32 and 128 have a fused 128 x 128 kernel on either
   // path (the fp8 matrix cores, or the exact-dot flag's folded-scale form);
   // fp32 scales and block 16 only the large-tile exact-dot kernels
   const bool fused_exists = pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
-  pb.split = split_shape &&
-             (!fused_exists || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE));
+  pb.split = shaped || (split_shape &&
+             (!fused_exists || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE)));
   // fused 128 x 128 path: E8M0 scales at blocks 32 and 128 (the fp8 matrix
   // cores, or the exact-dot flag's folded-scale bf16 form), whole 128-row
   // tiles and 128-byte K steps
@@ -140,25 +156,40 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if (pb.b_rows > 1) off = align256(off + B * T * ((pb.np + 127) / 128) * pb.kblocks * sizeof(uint32_t));
   wl.total = off;
 
-  // host tables: fp32 flattened U, V (nonzeros in ascending block order), base w, outer w
-  const int nb = (int)(n * n);
-  std::vector<float> U((size_t)T * nb), V((size_t)T * nb);
-  fmm_realization_tables(d, q.depth, U.data(), V.data(), nullptr);
+  // host tables: fp32 flattened U, V (dense rows; and their nonzeros in
+  // ascending block order), base w, outer w.  Other shapes: the dense rows
+  // and w padded with zeros to the kernels' grid capacities.
+  const int nba = (int)(gm * gk), nbb = (int)(gk * gn), nbc = (int)(gm * gn);
+  const int sta = shaped ? fmm::grid_capacity(nba) : nba, stb = shaped ? fmm::grid_capacity(nbb) : nbb;
+  std::vector<float> U((size_t)T * sta, 0.0f), V((size_t)T * stb, 0.0f);
+  std::vector<float> wfull;
+  if (shaped) {
+    std::vector<float> u0((size_t)T * nba), v0((size_t)T * nbb), w0((size_t)T * nbc);
+    fmm_realization_tables(d, 1, u0.data(), v0.data(), w0.data());
+    const int stc = fmm::grid_capacity(nbc);
+    wfull.assign((size_t)T * stc, 0.0f);
+    for (int64_t r = 0; r < T; ++r) {
+      for (int b = 0; b < nba; ++b) U[r * sta + b] = u0[r * nba + b];
+      for (int b = 0; b < nbb; ++b) V[r * stb + b] = v0[r * nbb + b];
+      for (int b = 0; b < nbc; ++b) wfull[r * stc + b] = w0[r * nbc + b];
+    }
+  } else {
+    fmm_realization_tables(d, q.depth, U.data(), V.data(), nullptr);
+  }
   std::vector<int32_t> aoff(T + 1), boff(T + 1);
   std::vector<fmm::CoefEntry> aent, bent;
   for (int64_t r = 0; r < T; ++r) {
     aoff[r] = (int32_t)aent.size();
     boff[r] = (int32_t)bent.size();
-    for (int b = 0; b < nb; ++b) {
-      const float u = U[r * nb + b], v = V[r * nb + b];
-      if (u != 0.0f) aent.push_back({b, u});
-      if (v != 0.0f) bent.push_back({b, v});
-    }
+    for (int b = 0; b < nba; ++b)
+      if (U[r * sta + b] != 0.0f) aent.push_back({b, U[r * sta + b]});
+    for (int b = 0; b < nbb; ++b)
+      if (V[r * stb + b] != 0.0f) bent.push_back({b, V[r * stb + b]});
   }
   aoff[T] = (int32_t)aent.size();
   boff[T] = (int32_t)bent.size();
-  std::vector<float> wbase((size_t)R * 4);
-  fmm_realization_tables(d, 1, nullptr, nullptr, wbase.data());
+  std::vector<float> wbase((size_t)fmm::kMaxRank * 4, 0.0f);
+  if (!shaped) fmm_realization_tables(d, 1, nullptr, nullptr, wbase.data());
   std::vector<float> wouter;
   if (q.depth >= 2) {
     const int no = 1 << (2 * (q.depth - 1));
@@ -166,7 +197,6 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
     fmm_realization_tables(d, q.depth - 1, nullptr, nullptr, wouter.data());
   }
   // large-tile plans at depth 2 combine all T terms in one pass: the flattened w
-  std::vector<float> wfull;
   if (pb.split && q.depth == 2) {
     wfull.resize((size_t)T * 16);
     fmm_realization_tables(d, 2, nullptr, nullptr, wfull.data());
@@ -177,12 +207,13 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   const size_t s_boff = s_aoff;
   const size_t s_aent = align256(std::max<size_t>(1, aent.size()) * sizeof(fmm::CoefEntry));
   const size_t s_bent = align256(std::max<size_t>(1, bent.size()) * sizeof(fmm::CoefEntry));
-  const size_t s_wi = align256((size_t)fmm::kMaxRank * 4 * sizeof(float));   // zero-padded to 8 x 4
+  const size_t s_wi = align256(wbase.size() * sizeof(float));   // zero-padded to 8 x 4
   const size_t s_wo = align256(std::max<size_t>(1, wouter.size()) * sizeof(float));
   const size_t s_wf = align256(std::max<size_t>(1, wfull.size()) * sizeof(float));
-  const size_t s_ud = align256(U.size() * sizeof(float));   // dense flattened rows (the encoder at depths 2, 3)
+  const size_t s_ud = align256(std::max<size_t>(1, U.size()) * sizeof(float));   // dense rows (the encoder at depths 2, 3)
+  const size_t s_vd = align256(std::max<size_t>(1, V.size()) * sizeof(float));
   const size_t o_ud = s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo + s_wf;
-  const size_t tot = o_ud + 2 * s_ud;
+  const size_t tot = o_ud + s_ud + s_vd;
   std::vector<uint8_t> host(tot, 0);
   std::memcpy(host.data(), aoff.data(), (T + 1) * sizeof(int32_t));
   std::memcpy(host.data() + s_aoff, boff.data(), (T + 1) * sizeof(int32_t));
@@ -193,8 +224,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   if (!wouter.empty())
     std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent + s_wi, wouter.data(),
                 wouter.size() * sizeof(float));
-  std::memcpy(host.data() + o_ud, U.data(), U.size() * sizeof(float));
-  std::memcpy(host.data() + o_ud + s_ud, V.data(), V.size() * sizeof(float));
+  if (!U.empty()) std::memcpy(host.data() + o_ud, U.data(), U.size() * sizeof(float));
+  if (!V.empty()) std::memcpy(host.data() + o_ud + s_ud, V.data(), V.size() * sizeof(float));
   if (!wfull.empty())
     std::memcpy(host.data() + s_aoff + s_boff + s_aent + s_bent + s_wi + s_wo, wfull.data(),
                 wfull.size() * sizeof(float));
@@ -357,7 +388,7 @@ int fmm_error_stats_noalloc(int64_t batch, int64_t M, int64_t N, const float *dC
 
 int fmm_encode_noise_scratch_size(const fmm_plan *p, size_t *bytes) {
   if (!p || !bytes) return FMM_ERR_ARG;
-  if (p->pb.depth > 2) return FMM_ERR_UNSUPPORTED;
+  if (p->pb.depth > 2 || p->pb.shaped) return FMM_ERR_UNSUPPORTED;
   *bytes = fmm::encode_noise_scratch_bytes(p->pb);
   return FMM_OK;
 }
@@ -366,7 +397,7 @@ int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const 
                      void *dScratch, size_t scratch_bytes, void *stream) {
   if (!p) return FMM_ERR_ARG;
   const fmm::Problem &pb = p->pb;
-  if (pb.depth > 2) return FMM_ERR_UNSUPPORTED;
+  if (pb.depth > 2 || pb.shaped) return FMM_ERR_UNSUPPORTED;
   if (pb.batch == 0) return FMM_OK;
   if (!dOut || !dWs || (pb.M * pb.K > 0 && !dA) || (pb.K * pb.N > 0 && !dB)) return FMM_ERR_ARG;
   if (reinterpret_cast<uintptr_t>(dWs) % 256) return FMM_ERR_WORKSPACE;
@@ -378,7 +409,7 @@ int fmm_encode_noise(const fmm_plan *p, const float *dA, const float *dB, const 
 
 int fmm_cross_terms_scratch_size(const fmm_plan *p, size_t *bytes) {
   if (!p || !bytes) return FMM_ERR_ARG;
-  if (p->pb.depth != 1) return FMM_ERR_UNSUPPORTED;
+  if (p->pb.depth != 1 || p->pb.shaped) return FMM_ERR_UNSUPPORTED;
   *bytes = fmm::cross_terms_scratch_bytes(p->pb);
   return FMM_OK;
 }
@@ -387,7 +418,7 @@ int fmm_cross_terms(const fmm_plan *p, const float *dA, const float *dB, const v
                     void *dScratch, size_t scratch_bytes, void *stream) {
   if (!p) return FMM_ERR_ARG;
   const fmm::Problem &pb = p->pb;
-  if (pb.depth != 1) return FMM_ERR_UNSUPPORTED;
+  if (pb.depth != 1 || pb.shaped) return FMM_ERR_UNSUPPORTED;
   if (pb.batch == 0) return FMM_OK;
   if (!dOut || !dWs || (pb.M * pb.K > 0 && !dA) || (pb.K * pb.N > 0 && !dB)) return FMM_ERR_ARG;
   if (reinterpret_cast<uintptr_t>(dWs) % 256) return FMM_ERR_WORKSPACE;

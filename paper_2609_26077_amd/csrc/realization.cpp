@@ -1,13 +1,17 @@
 // Realizations of <2,2,2;R>: the named tables, the change-of-basis action,
 // the canonical gauge, Phi/Gamma/Brent, and the depth-l flattening into the
-// fp32 tables the kernels consume.  Host code only; compiled with
-// -ffp-contract=off so every binary64 expression rounds once per operation.
+// fp32 tables the kernels consume; and realizations of other shapes
+// <m,k,n;R> (Section 2.1), with the shape-independent parts of the same
+// (Brent residual, Phi/Gamma, the gauge, fp32 tables at one level).  Host
+// code only; compiled with -ffp-contract=off so every binary64 expression
+// rounds once per operation.
 #include "internal.h"
 
 #include <cmath>
 #include <initializer_list>
 #include <cstring>
 #include <new>
+#include <vector>
 
 namespace fmm {
 
@@ -241,6 +245,47 @@ void flatten(const double (*base)[4], int R, int depth, float *out) {
   }
 }
 
+// ---- other shapes <m,k,n;R> ------------------------------------------------
+// U_r indexed i k + j (A block (i, j)), V_r j n + l (B block (j, l)), W_r
+// l m + i (C block (i, l), the cyclic third factor of the <2,2,2> case).
+
+double brent_residual_shape(const Shaped &s) {
+  const int a_n = s.m * s.k, b_n = s.k * s.n, c_n = s.n * s.m;
+  double worst = 0.0;
+  for (int a = 0; a < a_n; ++a)
+    for (int b = 0; b < b_n; ++b)
+      for (int c = 0; c < c_n; ++c) {
+        double acc = 0.0;
+        for (int r = 0; r < s.R; ++r)
+          acc = acc + s.U[(size_t)r * a_n + a] * s.V[(size_t)r * b_n + b] * s.W[(size_t)r * c_n + c];
+        const int i = a / s.k, j = a % s.k, jp = b / s.n, l = b % s.n, lp = c / s.m, ip = c % s.m;
+        const double want = (j == jp && l == lp && i == ip) ? 1.0 : 0.0;
+        const double e = std::fabs(acc - want);
+        if (!(e <= worst)) worst = e;  // propagates NaN
+      }
+  return worst;
+}
+
+namespace {
+double sq_norm_n(const double *v, int len) {
+  double s = 0.0;
+  for (int c = 0; c < len; ++c) s = s + v[c] * v[c];
+  return s;
+}
+}  // namespace
+
+void phi_gamma_shape(const Shaped &s, double &phi, double &gamma) {
+  phi = 0.0;
+  gamma = 0.0;
+  const int a_n = s.m * s.k, b_n = s.k * s.n, c_n = s.n * s.m;
+  for (int r = 0; r < s.R; ++r) {
+    const double t = sq_norm_n(s.U + (size_t)r * a_n, a_n) * sq_norm_n(s.V + (size_t)r * b_n, b_n) *
+                     sq_norm_n(s.W + (size_t)r * c_n, c_n);
+    phi = phi + t;
+    gamma = gamma + std::sqrt(t);
+  }
+}
+
 }  // namespace fmm
 
 // ---------------------------------------------------------------------------
@@ -249,7 +294,11 @@ void flatten(const double (*base)[4], int R, int depth, float *out) {
 using fmm::Realization;
 
 struct fmm_real {
-  Realization d;
+  int m = 2, k = 2, n = 2;
+  Realization d;                   // <2,2,2>: the coefficients; other shapes: d.R only
+  std::vector<double> U, V, W;     // other shapes: R x mk, R x kn, R x nm
+  bool is222() const { return m == 2 && k == 2 && n == 2; }
+  fmm::Shaped shaped() const { return {m, k, n, d.R, U.data(), V.data(), W.data()}; }
 };
 
 extern "C" {
@@ -273,11 +322,33 @@ int fmm_realization_create(int m, int k, int n, int R, const double *U, const do
   if (!out) return FMM_ERR_ARG;
   *out = nullptr;
   if (m < 1 || k < 1 || n < 1) return FMM_ERR_ARG;
-  if (m != 2 || k != 2 || n != 2) return FMM_ERR_UNSUPPORTED;   // <2,2,2;R> only
-  if (!U || !V || !w || R < 1 || R > fmm::kMaxRank || !(tol >= 0.0)) return FMM_ERR_ARG;
+  if (int64_t(m) * k > fmm::kMaxGridBlocks || int64_t(k) * n > fmm::kMaxGridBlocks || int64_t(n) * m > fmm::kMaxGridBlocks)
+    return FMM_ERR_UNSUPPORTED;
+  const bool is222 = m == 2 && k == 2 && n == 2;
+  if (!U || !V || !w || R < 1 || R > (is222 ? fmm::kMaxRank : fmm::kMaxRankShape) || !(tol >= 0.0))
+    return FMM_ERR_ARG;
   fmm_real *h = new (std::nothrow) fmm_real;
   if (!h) return FMM_ERR_NOMEM;
   std::memset(&h->d, 0, sizeof(h->d));
+  if (!is222) {
+    h->m = m; h->k = k; h->n = n;
+    h->d.R = R;
+    try {
+      h->U.assign(U, U + (size_t)R * m * k);
+      h->V.assign(V, V + (size_t)R * k * n);
+      h->W.assign(w, w + (size_t)R * n * m);
+    } catch (...) {
+      delete h;
+      return FMM_ERR_NOMEM;
+    }
+    const double res = fmm::brent_residual_shape(h->shaped());
+    if (!(res <= tol)) {
+      delete h;
+      return FMM_ERR_NOT_EXACT;
+    }
+    *out = h;
+    return FMM_OK;
+  }
   h->d.R = R;
   for (int r = 0; r < R; ++r)
     for (int c = 0; c < 4; ++c) {
@@ -299,6 +370,7 @@ int fmm_realization_transform(const fmm_real *d, const double X[4], const double
   if (!out) return FMM_ERR_ARG;
   *out = nullptr;
   if (!d || !X || !Y || !Z) return FMM_ERR_ARG;
+  if (!d->is222()) return FMM_ERR_UNSUPPORTED;
   fmm_real *h = new (std::nothrow) fmm_real;
   if (!h) return FMM_ERR_NOMEM;
   const int st = fmm::realization_transform(d->d, X, Y, Z, h->d);
@@ -316,7 +388,31 @@ int fmm_realization_rebalance(const fmm_real *d, fmm_real **out) {
   if (!d) return FMM_ERR_ARG;
   fmm_real *h = new (std::nothrow) fmm_real;
   if (!h) return FMM_ERR_NOMEM;
-  fmm::realization_rebalance(d->d, h->d);
+  if (d->is222()) {
+    fmm::realization_rebalance(d->d, h->d);
+    *out = h;
+    return FMM_OK;
+  }
+  // other shapes: the same gauge on rows of length mk and kn
+  try {
+    *h = *d;
+  } catch (...) {
+    delete h;
+    return FMM_ERR_NOMEM;
+  }
+  const int a_n = d->m * d->k, b_n = d->k * d->n;
+  for (int r = 0; r < d->d.R; ++r) {
+    const double *u = d->U.data() + (size_t)r * a_n, *v = d->V.data() + (size_t)r * b_n;
+    double nu = 0.0, nv = 0.0;
+    for (int c = 0; c < a_n; ++c) nu = nu + u[c] * u[c];
+    for (int c = 0; c < b_n; ++c) nv = nv + v[c] * v[c];
+    nu = std::sqrt(nu);
+    nv = std::sqrt(nv);
+    if (nu == 0.0 || nv == 0.0) continue;
+    const double s = std::sqrt(nu / nv);
+    for (int c = 0; c < a_n; ++c) h->U[(size_t)r * a_n + c] = u[c] / s;
+    for (int c = 0; c < b_n; ++c) h->V[(size_t)r * b_n + c] = v[c] * s;
+  }
   *out = h;
   return FMM_OK;
 }
@@ -324,23 +420,43 @@ int fmm_realization_rebalance(const fmm_real *d, fmm_real **out) {
 int fmm_realization_metrics(const fmm_real *d, int depth, double *phi, double *gamma,
                             double *brent_resid) {
   if (!d || depth < 1 || depth > fmm::kMaxDepth) return FMM_ERR_ARG;
+  if (!d->is222() && depth != 1) return FMM_ERR_UNSUPPORTED;
   double p, g;
-  fmm::realization_phi_gamma(d->d, p, g);
+  if (d->is222())
+    fmm::realization_phi_gamma(d->d, p, g);
+  else
+    fmm::phi_gamma_shape(d->shaped(), p, g);
   if (phi) *phi = std::pow(p, depth);
   if (gamma) *gamma = std::pow(g, depth);
-  if (brent_resid) *brent_resid = fmm::brent_residual(d->d);
+  if (brent_resid) *brent_resid = d->is222() ? fmm::brent_residual(d->d) : fmm::brent_residual_shape(d->shaped());
   return FMM_OK;
 }
 
 int fmm_realization_terms(const fmm_real *d, int depth, int64_t *rank, int64_t *terms) {
   if (!d || depth < 1 || depth > fmm::kMaxDepth) return FMM_ERR_ARG;
+  if (!d->is222() && depth != 1) return FMM_ERR_UNSUPPORTED;
   if (rank) *rank = d->d.R;
   if (terms) *terms = fmm::ipow(d->d.R, depth);
   return FMM_OK;
 }
 
+int fmm_realization_shape(const fmm_real *d, int *m, int *k, int *n, int *R) {
+  if (!d) return FMM_ERR_ARG;
+  if (m) *m = d->m;
+  if (k) *k = d->k;
+  if (n) *n = d->n;
+  if (R) *R = d->d.R;
+  return FMM_OK;
+}
+
 int fmm_realization_coefficients(const fmm_real *d, double *U, double *V, double *w) {
   if (!d) return FMM_ERR_ARG;
+  if (!d->is222()) {
+    if (U) std::memcpy(U, d->U.data(), d->U.size() * sizeof(double));
+    if (V) std::memcpy(V, d->V.data(), d->V.size() * sizeof(double));
+    if (w) std::memcpy(w, d->W.data(), d->W.size() * sizeof(double));
+    return FMM_OK;
+  }
   for (int r = 0; r < d->d.R; ++r)
     for (int c = 0; c < 4; ++c) {
       if (U) U[4 * r + c] = d->d.U[r][c];
@@ -352,6 +468,16 @@ int fmm_realization_coefficients(const fmm_real *d, double *U, double *V, double
 
 int fmm_realization_tables(const fmm_real *d, int depth, float *U, float *V, float *w) {
   if (!d || depth < 1 || depth > fmm::kMaxDepth) return FMM_ERR_ARG;
+  if (!d->is222()) {
+    if (depth != 1) return FMM_ERR_UNSUPPORTED;
+    for (size_t i = 0; i < d->U.size(); ++i)
+      if (U) U[i] = static_cast<float>(d->U[i]);
+    for (size_t i = 0; i < d->V.size(); ++i)
+      if (V) V[i] = static_cast<float>(d->V[i]);
+    for (size_t i = 0; i < d->W.size(); ++i)
+      if (w) w[i] = static_cast<float>(d->W[i]);
+    return FMM_OK;
+  }
   if (U) fmm::flatten(d->d.U, d->d.R, depth, U);
   if (V) fmm::flatten(d->d.V, d->d.R, depth, V);
   if (w) fmm::flatten(d->d.W, d->d.R, depth, w);

@@ -121,23 +121,23 @@ def test_create_checks_exactness(fm):
         fm.fmm_realization_create(U, V, W, tol=-1.0)
 
 
-def test_create_accepts_only_222(fm):
-    """<m,k,n;R> other than <2,2,2> is refused as unsupported (e.g. the
-    <2,2,3;11> shape of Table E.1), before the coefficients are read; sizes
-    below one are argument errors."""
+def test_create_shape_limits(fm):
+    """Sizes below one are argument errors; grids of more than 64 blocks
+    (m k, k n or n m) are unsupported; both are refused before the
+    coefficients are read.  <2,2,2> takes R <= 8, other shapes R <= 4096."""
     import ctypes
     U, V, W = R.builtin_f64("strassen")
-    for shape, R_, status in (((2, 2, 3), 11, fm.FMM_ERR_UNSUPPORTED), ((3, 3, 3), 23, fm.FMM_ERR_UNSUPPORTED),
-                              ((2, 3, 2), 11, fm.FMM_ERR_UNSUPPORTED), ((0, 2, 2), 7, fm.FMM_ERR_ARG)):
+    for shape, R_, status in (((0, 2, 2), 7, fm.FMM_ERR_ARG), ((2, -1, 2), 7, fm.FMM_ERR_ARG),
+                              ((9, 8, 1), 72, fm.FMM_ERR_UNSUPPORTED), ((1, 8, 9), 72, fm.FMM_ERR_UNSUPPORTED),
+                              ((9, 1, 8), 72, fm.FMM_ERR_UNSUPPORTED), ((2, 2, 2), 9, fm.FMM_ERR_ARG),
+                              ((2, 2, 3), 4097, fm.FMM_ERR_ARG), ((2, 2, 3), 11, fm.FMM_ERR_ARG)):
         m, k, n = shape
         h = ctypes.c_void_p()
         st = fm._lib.fmm_realization_create(m, k, n, R_, None, None, None, 0.0, ctypes.byref(h))
         assert st == status and not h.value, (shape, st)
-    with pytest.raises(fm.FmmError) as e:
-        fm.fmm_realization_create(np.zeros((11, 6)), np.zeros((11, 6)), np.zeros((11, 4)), shape=(2, 3, 2))
-    assert e.value.status == fm.FMM_ERR_UNSUPPORTED
     d = fm.fmm_realization_create(U, V, W, tol=0.0, shape=(2, 2, 2))
     assert fm.fmm_realization_terms(d, 1) == (7, 7)
+    assert fm.fmm_realization_shape(d) == ((2, 2, 2), 7)
 
 
 @pytest.mark.parametrize("desc,status", [

@@ -10,45 +10,36 @@ import numpy as np
 import pytest
 
 import fmm_inputs as gen
+from fmm_inputs import shapes as S
 from oracle import e4m3, fmm, model, shapes
 from oracle import realizations as R
 
 
-def strassen():
-    return shapes.from_222(R.builtin_f64("strassen"))
-
-
 def shaped(name):
-    """The shapes the tests and the GPU path run (name -> realization)."""
+    """A realization of fmm_inputs.shapes.CATALOG built on the oracle's
+    <2,2,2> tables, or the oracle's Strassen itself."""
     if name == "222_strassen":
-        return strassen()
-    if name == "223_11":
-        return shapes.direct_sum(strassen(), shapes.cubic(2, 2, 1), "n")
-    if name == "322_11":
-        return shapes.direct_sum(strassen(), shapes.cubic(1, 2, 2), "m")
-    if name == "232_11":
-        return shapes.direct_sum(strassen(), shapes.cubic(2, 1, 2), "k")
-    if name == "223_tstar":
-        return shapes.direct_sum(shapes.from_222(R.builtin_f64("tstar")), shapes.cubic(2, 2, 1), "n")
-    if name == "333_27":
-        return shapes.cubic(3, 3, 3)
-    raise KeyError(name)
+        return S.from_222(R.builtin_f64("strassen"))
+    return S.build(name, R.builtin_f64)
 
 
 @pytest.mark.parametrize("mkn", [(2, 2, 3), (3, 2, 2), (2, 3, 2), (3, 3, 3), (1, 2, 3), (2, 1, 1)])
 def test_cubic_is_exact_with_phi_mkn(mkn):
-    D = shapes.cubic(*mkn)
+    D = S.cubic(*mkn)
     assert len(D[1]) == mkn[0] * mkn[1] * mkn[2]
     assert shapes.brent_exact(D)
     assert shapes.phi(D) == mkn[0] * mkn[1] * mkn[2]
 
 
-@pytest.mark.parametrize("name,shape,R_,phi", [("223_11", (2, 2, 3), 11, 36.0), ("322_11", (3, 2, 2), 11, 36.0),
-                                                ("232_11", (2, 3, 2), 11, 36.0),
-                                                ("223_tstar", (2, 2, 3), 11, 200 / 9 + 4)])
-def test_direct_sums_are_exact(name, shape, R_, phi):
+# Phi of a direct sum is the sum of the parts' Phi (the re-indexing keeps
+# every norm): Strassen's terms give 8 + 6 * 4 = 32, T*'s 200/9, a cubic term 1
+@pytest.mark.parametrize("name,phi", [("223_11", 32.0 + 4), ("322_11", 32.0 + 4), ("232_11", 32.0 + 4),
+                                      ("223_tstar", 200 / 9 + 4), ("333_26", 32.0 + 19),
+                                      ("333_27", 27.0), ("525_46", 4 * 32.0 + 18), ("454_80", 80.0)])
+def test_catalog_is_exact_with_its_phi(name, phi):
     D = shaped(name)
-    assert D[0] == shape and len(D[1]) == R_
+    shape, rank = S.CATALOG[name]
+    assert D[0] == shape and len(D[1]) == rank
     if name != "223_tstar":          # T*'s entries are irrational in binary64; exactness there is to rounding
         assert shapes.brent_exact(D)
     assert shapes.phi(D) == pytest.approx(phi, rel=1e-13)
@@ -56,12 +47,11 @@ def test_direct_sums_are_exact(name, shape, R_, phi):
 
 def test_perturbed_direct_sum_fails_brent():
     for part in (1, 2, 3):
-        D = shaped("223_11")
-        M = [list(r) for r in D[part]]
-        M[8][0] = 1 - M[8][0]                # flip one coefficient of a cubic term
-        D2 = list(D)
-        D2[part] = M
-        assert not shapes.brent_exact(tuple(D2))
+        D = list(shaped("223_11"))
+        M = np.array(D[part])
+        M[8, 0] = 1 - M[8, 0]                # flip one coefficient of a cubic term
+        D[part] = M
+        assert not shapes.brent_exact(tuple(D))
 
 
 @pytest.mark.parametrize("name", ["223_11", "322_11", "232_11", "333_27"])
@@ -95,7 +85,7 @@ def test_agrees_with_the_222_oracle_bit_for_bit():
     D = R.builtin_f64("strassen")
     A, B = gen.operands("gaussian", 1, 128, 256, 192, seed=0, cfg=16, trial=0)
     want = fmm.fmm(A[0], B[0], R.tables_f32(D, 1), 1, 32, e4m3.RULE_POW2_CEIL)
-    got = shapes.fmm_shape(A[0], B[0], shapes.from_222(D), 32, e4m3.RULE_POW2_CEIL)
+    got = shapes.fmm_shape(A[0], B[0], S.from_222(D), 32, e4m3.RULE_POW2_CEIL)
     assert np.array_equal(got["a"]["codes"], want["a"]["codes"])
     assert np.array_equal(got["b"]["codes"], want["b"]["codes"])
     assert np.array_equal(got["a"]["scales"], want["a"]["scales"])
