@@ -53,7 +53,9 @@ def parse():
     p.add_argument("--depth", type=int, default=1)
     p.add_argument("--block", type=int, default=32)
     p.add_argument("--rule", default="pow2_ceil")
-    p.add_argument("--realization", default="tstar")
+    p.add_argument("--realization", default="tstar",
+                   help="cubic8, strassen, winograd, tstar, or a realization of another shape (at depth 1): "
+                        "one of fmm_inputs.shapes.CATALOG or cubic_<m><k><n>")
     p.add_argument("--family", default="gaussian")
     p.add_argument("--exact-dot", action="store_true")
     p.add_argument("--large-tile", action="store_true",
@@ -61,7 +63,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-arms", action="store_true",
                    help="skip the comparison arms (cubic and Strassen realizations, heavy-tailed "
-                        "operands, the deployment granularity)")
+                        "operands, the deployment granularity, realizations of other shapes)")
     p.add_argument("--arm-batches", type=int, default=4,
                    help="interleaved rounds over the arms (each arm times --arm-steps steps a round)")
     p.add_argument("--arm-steps", type=int, default=5)
@@ -255,6 +257,58 @@ def interleaved_arms(args, dA, dB, stream):
                         "3 warm-up steps each, same seeded operands across arms", "arms": out}
 
 
+def shape_arms(args, stream):
+    """Realizations of other shapes <m,k,n;R> on the same path, each on
+    sub-blocks of the headline's (size / 2 on a side), Gaussian operands, the
+    headline's block and rule: <2,2,3;11> (Strassen and T* each beside a
+    cubic <2,2,1> part) and the cubic <2,2,3;12> on M = K = size,
+    N = 1.5 size; <3,3,3;26> (Strassen on the 2 x 2 x 2 corner) and the cubic
+    <3,3,3;27> on 1.5 size cubed.  Timed interleaved as interleaved_arms;
+    effective TFLOP/s = 2 M K N / step time."""
+    import torch
+    import fmm_inputs as gen
+    from paper_2609_26077_amd.controls import shaped_realization
+    from paper_2609_26077_amd.runner import FMM, error_stats, reference_f64
+    h = args.size // 2
+    groups = [((2 * h, 2 * h, 3 * h), ["223_11", "223_tstar", "cubic_223"]),
+              ((3 * h, 3 * h, 3 * h), ["333_26", "cubic_333"])]
+    out = {}
+    for (M, K, N), names in groups:
+        A, B = gen.operands("gaussian", 1, M, K, N, seed=SEED, cfg=3, trial=0)
+        dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+        del A, B
+        state = []
+        for name in names:
+            f = FMM(shaped_realization(name), 1, M, K, N, 1, args.block, args.rule, exact_dot=args.exact_dot)
+            C = torch.empty((1, M, N), dtype=torch.float32, device=dA.device)
+            warm_up(f, dA, dB, C, stream, 3, 20.0)
+            state.append({"name": name, "f": f, "C": C, "t": []})
+        for _ in range(args.arm_batches):
+            for s in state:
+                s["t"].append(time_steps(s["f"], dA, dB, s["C"], stream, args.arm_steps))
+        Cref = reference_f64(dA, dB)
+        for s in state:
+            step = np.concatenate([t["step"] for t in s["t"]])
+            prod = np.concatenate([t["products"] for t in s["t"]])
+            enc = np.concatenate([t["encode"] for t in s["t"]])
+            comb = np.concatenate([t["combine"] for t in s["t"]])
+            err2, ref2 = error_stats(s["C"], Cref)
+            from paper_2609_26077_amd import fmm_realization_metrics, fmm_realization_shape
+            shape, rank = fmm_realization_shape(s["f"].real)
+            out[s["name"]] = {"shape": list(shape), "rank": rank, "M": M, "K": K, "N": N,
+                              "phi": fmm_realization_metrics(s["f"].real, 1)["phi"],
+                              "value": 2.0 * M * K * N / (step.mean() * 1e-3) / 1e12, "unit": "TFLOP/s",
+                              "ms_per_step": float(step.mean()), "encode_ms": float(enc.mean()),
+                              "products_ms": float(prod.mean()), "combine_ms": float(comb.mean()),
+                              "rel_rms_error_vs_fp64": float(np.sqrt(err2.sum() / ref2.sum())),
+                              "steps": int(step.size)}
+            s.clear()
+        del Cref, dA, dB, state
+        torch.cuda.empty_cache()
+    return {"protocol": f"{args.arm_batches} interleaved rounds x {args.arm_steps} steps per arm within each "
+                        "shape, 3 warm-up steps each, same seeded operands within a shape", "arms": out}
+
+
 def paper_context():
     """The paper's own error figures under their stated setup, next to this
     path measured under the same setup (context, not a target): Table E.1's
@@ -354,13 +408,18 @@ def main():
     nb = args.batch
     # the comparison arms, the paper context and the oracle baseline go with
     # the headline shape (one cubic product)
-    headline = args.shape is None and nb == 1
+    headline = args.shape is None and nb == 1 and args.realization in ("cubic8", "strassen", "winograd", "tstar")
     A, B = gen.operands(args.family, nb, M, K, N, seed=SEED, cfg=0, trial=0)
     dA = torch.from_numpy(A).to(dev)
     dB = torch.from_numpy(B).to(dev)
     del A, B
     from paper_2609_26077_amd import FMM_FLAG_LARGE_TILE
-    f = FMM(args.realization, nb, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot,
+    real = args.realization
+    if real not in ("cubic8", "strassen", "winograd", "tstar"):
+        # a realization of another shape: fmm_inputs.shapes' catalog or cubic_<m><k><n>
+        from paper_2609_26077_amd.controls import shaped_realization
+        real = shaped_realization(args.realization)
+    f = FMM(real, nb, M, K, N, args.depth, args.block, args.rule, exact_dot=args.exact_dot,
             flags=FMM_FLAG_LARGE_TILE if args.large_tile else 0)
     C = torch.empty((nb, M, N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
@@ -387,8 +446,12 @@ def main():
     a_view, _ = fmm_operand_views(f.plan, f.ws)
     split = a_view.code_layout == FMM_LAYOUT_TILE256x64
     mkn = 2.0 * nb * M * N * K
-    mfma_flop = mkn * T / 8.0 ** args.depth
-    mp, kp, np_ = M // 2 ** args.depth, K // 2 ** args.depth, N // 2 ** args.depth
+    from paper_2609_26077_amd import fmm_realization_shape
+    (gm, gk, gn), _ = fmm_realization_shape(f.real)
+    if (gm, gk, gn) == (2, 2, 2):
+        gm = gk = gn = 2 ** args.depth
+    mp, kp, np_ = M // gm, K // gk, N // gn
+    mfma_flop = 2.0 * nb * T * mp * kp * np_
     sb = 4 if args.rule == "fp32_amax" else 1
     code_bytes = nb * T * (mp + np_) * kp
     scale_bytes = nb * T * (mp + np_) * (kp // args.block) * sb
@@ -451,6 +514,7 @@ def main():
                                + (", exact-dot sub-products" if args.exact_dot else ""),
                    "M": M, "K": K, "N": N, "depth": args.depth, "terms": T, "block": args.block,
                    "rule": args.rule, "realization": args.realization, "family": args.family,
+                   "realization_shape": list(fmm_realization_shape(f.real)[0]),
                    "exact_dot": bool(args.exact_dot),
                    "subproduct_path": ("large tiles (" + ("256x128" if exact else "256x256") +
                                        ") + separate W-combine") if split
@@ -487,6 +551,8 @@ def main():
         line["config"]["batch"] = nb
     if not args.no_arms and headline:
         line["arms"] = interleaved_arms(args, dA, dB, stream)
+        if args.depth == 1:
+            line["shape_arms"] = shape_arms(args, stream)
         line["paper_context"] = paper_context()
     if not args.no_cpu_baseline and headline:
         del dA, dB, C

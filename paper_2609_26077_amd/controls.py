@@ -20,9 +20,21 @@ simple statistics of what they return:
   library's cross-term kernels, on six arms (cubic, Strassen, Winograd raw
   and rebalanced, T*, a random orbit member of Strassen) at n = 512, Gaussian
   operands, four seeds, 1 x 128 blocks with fp32 amax/448 scales; the
-  armwise means (the paper reports -0.085% to 0.201%).
+  armwise means (the paper reports -0.085% to 0.201%);
+* cross-shape predictor (Section 3's breadth test; Appendix E's protocol and
+  Table E.1's setting): over realizations of several shapes <m,k,n;R> (the
+  <2,2,2> builtins and fmm_inputs.shapes' constructions), one level, signed-
+  uniform operands, eight paired samples at block edge 256, 1 x 128 blocks
+  with fp32 amax/448 scales, the mean relative Frobenius error e of each and
+  of the cubic algorithm of its shape on the same operands, and the
+  Spearman correlation (average ranks for ties) of e with the coefficient-
+  only predictors sqrt(Phi / mkn), sqrt(Phi) and GQ_chi (Appendix E: each
+  term rescaled to |U_r| = |V_r| = 1 with the magnitude moved into W_r;
+  chi_r^A = 0 when the rescaled U_r has exactly one entry of magnitude
+  >= 1e-6, else 1, chi_r^B likewise; GQ_chi = (mean_q sum_r W_rq^2
+  (chi_r^A + chi_r^B))^(1/2)).
 
-Usage: python -m paper_2609_26077_amd.controls [--quick]  (prints one JSON object)
+Usage: python -m paper_2609_26077_amd.controls [--quick] [--only NAME]  (prints one JSON object)
 """
 from __future__ import annotations
 
@@ -33,7 +45,8 @@ import math
 import numpy as np
 import torch
 
-from . import (fmm_realization_builtin, fmm_realization_metrics, fmm_realization_rebalance,
+from . import (fmm_realization_builtin, fmm_realization_coefficients, fmm_realization_create,
+               fmm_realization_metrics, fmm_realization_rebalance, fmm_realization_shape,
                fmm_realization_transform)
 from .runner import FMM, error_stats, reference_f64
 
@@ -134,20 +147,107 @@ def cross_r_residual(n=512, seeds=4):
             "paper_range_pct": [-0.085, 0.201]}
 
 
+def shaped_realization(name):
+    """A realization of fmm_inputs.shapes.CATALOG (or the cubic algorithm
+    "cubic_<m><k><n>") built on the library's own <2,2,2> tables."""
+    from fmm_inputs import shapes as S
+    if name.startswith("cubic_"):
+        (m, k, n), U, V, W = S.cubic(*(int(c) for c in name[6:]))
+    else:
+        (m, k, n), U, V, W = S.build(
+            name, lambda which: fmm_realization_coefficients(fmm_realization_builtin(which)))
+    return fmm_realization_create(U, V, W, tol=1e-9, shape=(m, k, n))
+
+
+def gq_chi(real):
+    """Appendix E's coefficient-growth heuristic GQ_chi of a realization."""
+    U, V, W = fmm_realization_coefficients(real)
+    nu = np.linalg.norm(U, axis=1)
+    nv = np.linalg.norm(V, axis=1)
+    ok = (nu > 0) & (nv > 0)
+    Ur = U[ok] / nu[ok, None]
+    Vr = V[ok] / nv[ok, None]
+    Wr = W[ok] * (nu[ok] * nv[ok])[:, None]
+    chi_a = (np.count_nonzero(np.abs(Ur) >= 1e-6, axis=1) != 1).astype(np.float64)
+    chi_b = (np.count_nonzero(np.abs(Vr) >= 1e-6, axis=1) != 1).astype(np.float64)
+    return float(np.sqrt(np.mean(np.sum(Wr ** 2 * (chi_a + chi_b)[:, None], axis=0))))
+
+
+def spearman(x, y):
+    """Spearman correlation with average ranks for ties."""
+    from scipy.stats import rankdata
+    rx, ry = rankdata(x), rankdata(y)
+    return float(np.corrcoef(rx, ry)[0, 1])
+
+
+CROSS_SHAPE_ROWS = ("strassen", "winograd", "tstar", "223_11", "223_tstar", "322_11", "232_11",
+                    "333_26", "525_46")
+
+
+def cross_shape_predictor(rows=CROSS_SHAPE_ROWS, samples=8, edge=256, seed=0):
+    rows_out, cubic_e = [], {}
+    for name in rows:
+        real = fmm_realization_builtin(name) if name in ("strassen", "winograd", "tstar") else shaped_realization(name)
+        (m, k, n), R = fmm_realization_shape(real)
+        M, K, N = m * edge, k * edge, n * edge
+        A, B = device_operands("uniform", samples, M, K, N, seed, 15)
+
+        def mean_rel_fro(d):
+            f = FMM(d, samples, M, K, N, 1, 128, "fp32_amax")
+            err2, ref2 = error_stats(f.matmul(A, B), reference_f64(A, B))
+            return float(np.mean(np.sqrt(err2 / ref2)))
+
+        key = (m, k, n, seed)
+        if key not in cubic_e:
+            cub = fmm_realization_builtin("cubic8") if (m, k, n) == (2, 2, 2) else shaped_realization(f"cubic_{m}{k}{n}")
+            cubic_e[key] = mean_rel_fro(cub)
+        e = mean_rel_fro(real)
+        phi = fmm_realization_metrics(real, 1)["phi"]
+        rows_out.append({"realization": name, "shape": [m, k, n], "rank": R, "phi": phi,
+                         "sqrt_phi_over_mkn": math.sqrt(phi / (m * k * n)), "gq_chi": gq_chi(real),
+                         "e": e, "e_cubic": cubic_e[key], "e_over_e_cubic": e / cubic_e[key]})
+    e = [r["e"] for r in rows_out]
+    return {"rows": rows_out,
+            "spearman_sqrt_phi_over_mkn": spearman([r["sqrt_phi_over_mkn"] for r in rows_out], e),
+            "spearman_sqrt_phi": spearman([math.sqrt(r["phi"]) for r in rows_out], e),
+            "spearman_gq_chi": spearman([r["gq_chi"] for r in rows_out], e),
+            "setting": {"family": "uniform", "samples": samples, "edge": edge, "block": 128,
+                        "rule": "fp32_amax", "depth": 1}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--quick", action="store_true", help="small shapes (a smoke run)")
+    ap.add_argument("--only", choices=("calibration_transport", "orbit_stability", "rademacher",
+                                       "cross_r_residual", "cross_shape_predictor"),
+                    help="run one control")
     args = ap.parse_args()
+    if args.only == "cross_shape_predictor":
+        print(json.dumps({args.only: cross_shape_predictor(samples=2 if args.quick else 8)}), flush=True)
+        return
+    if args.only == "cross_r_residual":
+        print(json.dumps({args.only: cross_r_residual(seeds=1 if args.quick else 4)}), flush=True)
+        return
     if args.quick:
         shapes = [(256, 256, 256), (512, 256, 384), (384, 512, 256)]
         orbit = dict(n_members=4, shape=(256, 256, 256))
     else:
         shapes = [(1024, 1024, 1024), (2048, 1024, 1536), (1536, 2048, 1024)]
         orbit = dict(n_members=15, shape=(1024, 1024, 1024))
+    if args.only == "calibration_transport":
+        print(json.dumps({args.only: calibration_transport(shapes)}), flush=True)
+        return
+    if args.only == "orbit_stability":
+        print(json.dumps({args.only: orbit_stability(**orbit)}), flush=True)
+        return
+    if args.only == "rademacher":
+        print(json.dumps({args.only: rademacher_cells(shapes)}), flush=True)
+        return
     out = {"calibration_transport": calibration_transport(shapes),
            "orbit_stability": orbit_stability(**orbit),
            "rademacher": rademacher_cells(shapes),
-           "cross_r_residual": cross_r_residual(seeds=1 if args.quick else 4)}
+           "cross_r_residual": cross_r_residual(seeds=1 if args.quick else 4),
+           "cross_shape_predictor": cross_shape_predictor(samples=2 if args.quick else 8)}
     print(json.dumps(out), flush=True)
 
 

@@ -73,9 +73,11 @@ constexpr int kA1Rows = 8, kA1Threads = 128;   // depth-1 A-side tile rows and t
 constexpr int kB1Rows = 32, kB1Threads = 512;  // depth-1 B-side tile rows (columns of B) and threads
 constexpr int kB3Rows = 8;          // depth-3 B-side tile rows (columns of B), 32 positions each, at blocks <= 32
 
-template <int DEPTH, int VEC, int SIDE, bool NARROW = false>
+// CAP: a realization of another shape, staged as up to CAP blocks of a grid
+// known at run time (0: the 2^l x 2^l grid of <2,2,2> at depth l).
+template <int DEPTH, int VEC, int SIDE, bool NARROW = false, int CAP = 0>
 struct Tile {
-  static constexpr int nblk = 1 << (2 * DEPTH);
+  static constexpr int nblk = CAP ? CAP : 1 << (2 * DEPTH);
   static constexpr int TL = NARROW ? (DEPTH == 3 ? 256 / kB3Rows : 64) : kTL;   // contracted positions per tile
   static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
   static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? kB1Rows : kA1Rows) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
@@ -282,13 +284,15 @@ constexpr bool narrow_b(int side, int depth, int bs, int mode) {
   return side == 1 && depth == 2 && bs <= 32 && mode == 0;
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE, bool GEN = false>
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE, int CAP = 0>
 __global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l, void *__restrict__ aux) {
   static_assert(MODE == 0 || MODE == 3 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
+  static_assert(CAP == 0 || (MODE == 0 && (DEPTH == 1 || CAP == 16)), "other shapes: the plain encoder");
+  constexpr bool GEN = CAP != 0;
   uint32_t *amax = reinterpret_cast<uint32_t *>(aux);
-  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>;
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE), CAP>;
   constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads, TL = TT::TL, STR = TT::stride;
   constexpr int RPW = 64 * 16 / TL;         // rows per wave: 8, or 16 in the narrow tile
   constexpr int WPT = TR / RPW;             // waves per term (1 (A) or 4 (B) at depth 1, 1 at depth 2)
@@ -616,15 +620,15 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) v
   }
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0, bool GEN = false>
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0, int CAP = 0>
 hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
                     uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
-  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>;
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE), CAP>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + TT::TL - 1) / TT::TL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE, GEN>), grid, dim3(TT::threads), 0, st, src, pb, cf,
+  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE, CAP>), grid, dim3(TT::threads), 0, st, src, pb, cf,
                      codes, scales, tiles_l, amax);
   return hipGetLastError();
 }
@@ -665,17 +669,17 @@ hipError_t launch_b_deploy_any(const Problem &pb, const float *src, const SideTa
   return hipErrorInvalidValue;
 }
 
-template <int SIDE, int DEPTH, bool GEN = false>
+template <int SIDE, int DEPTH, int CAP = 0>
 hipError_t launch_wide(const Problem &pb, const float *src, const SideTab &cf,
                        uint8_t *codes, uint8_t *scales, hipStream_t st) {
   const bool f32 = pb.rule == dev::RULE_FP32_AMAX;
   switch (pb.block) {
-    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 0, GEN>(pb, src, cf, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 16, false, 0, GEN>(pb, src, cf, codes, scales, st);
-    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 0, GEN>(pb, src, cf, codes, scales, st)
-                        : launch16<SIDE, DEPTH, 32, false, 0, GEN>(pb, src, cf, codes, scales, st);
-    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 0, GEN>(pb, src, cf, codes, scales, st)
-                         : launch16<SIDE, DEPTH, 128, false, 0, GEN>(pb, src, cf, codes, scales, st);
+    case 16: return f32 ? launch16<SIDE, DEPTH, 16, true, 0, CAP>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 16, false, 0, CAP>(pb, src, cf, codes, scales, st);
+    case 32: return f32 ? launch16<SIDE, DEPTH, 32, true, 0, CAP>(pb, src, cf, codes, scales, st)
+                        : launch16<SIDE, DEPTH, 32, false, 0, CAP>(pb, src, cf, codes, scales, st);
+    case 128: return f32 ? launch16<SIDE, DEPTH, 128, true, 0, CAP>(pb, src, cf, codes, scales, st)
+                         : launch16<SIDE, DEPTH, 128, false, 0, CAP>(pb, src, cf, codes, scales, st);
   }
   return hipErrorInvalidValue;
 }
@@ -716,11 +720,15 @@ template <int SIDE>
 hipError_t launch_side(const Problem &pb, const float *src, const SideTab &cf,
                        uint8_t *codes, uint8_t *scales, hipStream_t st) {
   if (pb.shaped) {
-    // another shape: the depth-2 tile (16 positions per lane) over a grid of
-    // up to 16 blocks, the depth-3 one (4 per lane) over up to 64
+    // another shape: the depth-1 tile staging 4 or 8 blocks (the sizes that
+    // keep as many bytes in flight per CU as the <2,2,2> encoder), the
+    // depth-2 tile (16 positions per lane, 16 waves) over up to 16 blocks,
+    // the depth-3 one (4 per lane) over up to 64
     const int nb = SIDE == 0 ? pb.gm * pb.gk : pb.gk * pb.gn;
-    return nb <= 16 ? launch_wide<SIDE, 2, true>(pb, src, cf, codes, scales, st)
-                    : launch_narrow4<SIDE, true>(pb, src, cf, codes, scales, st);
+    if (nb <= 4) return launch_wide<SIDE, 1, 4>(pb, src, cf, codes, scales, st);
+    if (nb <= 8) return launch_wide<SIDE, 1, 8>(pb, src, cf, codes, scales, st);
+    if (nb <= 16) return launch_wide<SIDE, 2, 16>(pb, src, cf, codes, scales, st);
+    return launch_narrow4<SIDE, true>(pb, src, cf, codes, scales, st);
   }
   switch (pb.depth) {
     case 1: return launch_wide<SIDE, 1>(pb, src, cf, codes, scales, st);

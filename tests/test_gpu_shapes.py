@@ -149,3 +149,32 @@ def test_empty_contraction_and_batch():
     f0 = FMM(lib_realization("223_11"), 0, 512, 256, 768, 1, 32, "pow2_ceil")
     f0.matmul(torch.empty((0, 512, 256), device="cuda"), torch.empty((0, 256, 768), device="cuda"))
     torch.cuda.synchronize()
+
+
+def test_cross_shape_predictor_matches_oracle():
+    """The cross-shape control (Table E.1's setting) on three rows and two
+    samples: each row's mean relative Frobenius error e and its cubic
+    reference e_cubic equal the oracle's on the same operands to 1%, and the
+    reported predictors are the realizations' own."""
+    import math
+    from paper_2609_26077_amd import controls
+    out = controls.cross_shape_predictor(rows=("strassen", "223_11", "333_26"), samples=2, edge=256)
+    for row in out["rows"]:
+        name = row["realization"]
+        m, k, n = row["shape"]
+        A, B = gen.operands("uniform", 2, m * 256, k * 256, n * 256, seed=0, cfg=15)
+        if name == "strassen":
+            D = S.from_222(R.builtin_f64("strassen"))
+            C = S.from_222(R.builtin_f64("cubic8"))
+        else:
+            D = S.build(name, R.builtin_f64)
+            C = S.cubic(m, k, n)
+        for real, key in ((D, "e"), (C, "e_cubic")):
+            rel = []
+            for b in range(2):
+                o = O.fmm_shape(A[b], B[b], real, 128, e4m3.RULE_FP32_AMAX)
+                e2, r2 = fmm.error_sums(o["C"], fmm.reference(A[b], B[b]))
+                rel.append(math.sqrt(e2 / r2))
+            assert row[key] == pytest.approx(np.mean(rel), rel=0.01), (name, key)
+        assert row["phi"] == pytest.approx(O.phi(D), rel=1e-14)
+    print(out, flush=True)
