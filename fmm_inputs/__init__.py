@@ -109,3 +109,23 @@ def rebasing_starts(count: int, seed: int = 0, cfg: int = 6) -> np.ndarray:
     for i, g in enumerate(basis_changes(count, seed=seed, cfg=cfg)):
         out[i] = np.concatenate([m.reshape(-1) for m in g])
     return out
+
+
+def rebasing_starts_shape(count: int, m: int, k: int, n: int, seed: int = 0, cfg: int = 16) -> np.ndarray:
+    """``count`` re-basing starts for a realization of another shape <m,k,n>,
+    as a (count, m^2 + k^2 + n^2) float64 array: row i is (X, Y, Z), each
+    I + 0.45 N(0,1) of size m, k, n (flattened row-major), a factor with
+    |det| < 1e-3 redrawn from the same stream (key [seed, cfg, i, 4]), as the
+    <2,2,2> starts are drawn."""
+    out = np.empty((count, m * m + k * k + n * n), dtype=np.float64)
+    for i in range(count):
+        rng = generator(seed, cfg, i, OPERAND_G)
+        parts = []
+        for size in (m, k, n):
+            while True:
+                g = np.eye(size) + 0.45 * rng.standard_normal((size, size))
+                if abs(np.linalg.det(g)) >= 1e-3:
+                    parts.append(g.reshape(-1))
+                    break
+        out[i] = np.concatenate(parts)
+    return out

@@ -193,8 +193,7 @@ int fmm_realization_builtin(int which, fmm_real **out);
  * rows of Table E.1 beyond <2,2,2>) take m k, k n, n m <= 64 and
  * 1 <= R <= 4096 (FMM_ERR_UNSUPPORTED for larger grids; m, k or n < 1 or R
  * out of range: FMM_ERR_ARG) and run at depth 1 only, on the large-tile plans
- * (FMM_LAYOUT_TILE256x64); the change of basis, the re-basing optimizer and
- * its gradient are <2,2,2>'s (FMM_ERR_UNSUPPORTED for other shapes). */
+ * (FMM_LAYOUT_TILE256x64). */
 int fmm_realization_create(int m, int k, int n, int R, const double *U, const double *V,
                            const double *w, double tol, fmm_real **out);
 
@@ -204,7 +203,13 @@ int fmm_realization_create(int m, int k, int n, int R, const double *U, const do
  * this order: the inverse by the adjugate (det = a d - b c, entries divided
  * by det), then the Kronecker matrix, then u K with each entry summed in
  * ascending index; no fused multiply-add.  |det| < 1e-12 gives
- * FMM_ERR_SINGULAR. */
+ * FMM_ERR_SINGULAR.
+ * Another shape <m,k,n> takes g in GL(m) x GL(k) x GL(n): X m x m, Y k x k,
+ * Z n x n row-major, the same formulas (u indexed i k + j, so
+ * X (x) Y^-T has entry [i k + j][i' k + j'] = X[i][i'] (Y^-T)[j][j'];
+ * likewise v, w), i.e. U_r -> X^T U_r Y^-T, V_r -> Y^T V_r Z^-T,
+ * W_r -> Z^T W_r X^-T as matrices; the inverses by Gauss-Jordan elimination
+ * with partial pivoting. */
 int fmm_realization_transform(const fmm_real *d, const double X[4], const double Y[4],
                               const double Z[4], fmm_real **out);
 
@@ -214,13 +219,15 @@ int fmm_realization_transform(const fmm_real *d, const double X[4], const double
 int fmm_realization_rebalance(const fmm_real *d, fmm_real **out);
 
 /* Re-basing (Section 3.1; the protocol of Appendix E.2): minimize Phi over
- * the change-of-basis orbit D . g, g = (X, Y, Z) in GL(2)^3 (eq. A.1).
+ * the change-of-basis orbit D . g, g = (X, Y, Z) in GL(2)^3 (eq. A.1), or in
+ * GL(m) x GL(k) x GL(n) for another shape (fmm_realization_transform's
+ * action; P = m^2 + k^2 + n^2 entries, 12 at <2,2,2>).
  * Starts: g = (I, I, I) (the realization itself) and, for s < nstarts, the
- * caller's triple starts[12 s .. 12 s + 11] = (X, Y, Z), each 2x2 row-major
+ * caller's triple starts[P s .. P s + P - 1] = (X, Y, Z), each row-major
  * (the paper draws X, Y, Z as I + 0.45 N(0,1) and rejects |det| < 1e-3; the
  * caller does the drawing).  Each start runs limited-memory BFGS (memory 10)
  * with a strong-Wolfe line search (c1 = 1e-4, c2 = 0.9) in binary64 over the
- * 12 entries of g, with the exact gradient, until the largest gradient entry
+ * P entries of g, with the exact gradient, until the largest gradient entry
  * is at most gtol * max(1, Phi), progress falls below rounding, or max_iter
  * iterations.  The terminal g gives D . g by fmm_realization_transform's
  * arithmetic; among the terminal realizations with a finite Phi and a Brent
@@ -236,9 +243,11 @@ int fmm_realization_optimize(const fmm_real *d, int nstarts, const double *start
 
 /* Phi(D . g) for g = (X, Y, Z) = g[0..3], g[4..7], g[8..11] (row-major 2x2
  * each; eq. A.1) and its gradient with respect to those 12 entries, the
- * objective fmm_realization_optimize minimizes.  phi may be NULL.  Errors:
- * FMM_ERR_ARG (null d, g or grad).  A singular g gives non-finite values. */
-int fmm_realization_phi_gradient(const fmm_real *d, const double g[12], double *phi, double grad[12]);
+ * objective fmm_realization_optimize minimizes (another shape: X, Y, Z of
+ * m^2, k^2, n^2 entries in that order, P in all, and grad of P entries).
+ * phi may be NULL.  Errors: FMM_ERR_ARG (null d, g or grad).  A singular g
+ * gives non-finite values. */
+int fmm_realization_phi_gradient(const fmm_real *d, const double *g, double *phi, double *grad);
 
 /* Phi = sum_r |U_r|^2 |V_r|^2 |W_r|^2 and Gamma = sum_r |U_r||V_r||W_r|
  * (Section 2.1) of the depth-l flattening (Phi^l, Gamma^l), and the Brent

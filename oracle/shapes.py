@@ -31,6 +31,7 @@ from __future__ import annotations
 from fractions import Fraction
 
 import numpy as np
+import sympy
 
 from . import e4m3, fmm
 
@@ -132,3 +133,120 @@ def exact_product(A: np.ndarray, B: np.ndarray, D) -> np.ndarray:
     P = [sum(u[b] * Ab[b] for b in range(m * k)) @ sum(v[b] * Bb[b] for b in range(k * n))
          for u, v in zip(U, V)]
     return wcombine(P, np.asarray(W, np.float64), (m, k, n), A.shape[0], B.shape[1])
+
+
+# ---- the change-of-basis orbit GL(m) x GL(k) x GL(n) -------------------------
+#
+# eq. A.1's right action written for any shape: u -> u (X (x) Y^-T),
+# v -> v (Y (x) Z^-T), w -> w (Z (x) X^-T) with the Kronecker index order of
+# the flattened grids (u index i k + j pairs X's row index i with Y^-T's j).
+# Re-basing (Section 3.1; Appendix E.2's protocol) minimizes Phi(D . g) over
+# it; here by scipy's L-BFGS-B with the gradient by the chain rule through
+# the Kronecker matrices (as oracle/rebase.py does at <2,2,2>).
+
+def split_g(g, shape):
+    m, k, n = shape
+    g = np.asarray(g, dtype=np.float64)
+    return (g[:m * m].reshape(m, m), g[m * m:m * m + k * k].reshape(k, k), g[m * m + k * k:].reshape(n, n))
+
+
+def kron_parts(P, Q):
+    """K = P (x) Q^-T and N = Q^-T (numpy's inverse)."""
+    N = np.linalg.inv(Q).T
+    return np.kron(P, N), N
+
+
+def act(D, X, Y, Z):
+    """D . (X, Y, Z) in binary64: each row times its Kronecker matrix."""
+    shape, U, V, W = D
+    KU, _ = kron_parts(np.asarray(X, float), np.asarray(Y, float))
+    KV, _ = kron_parts(np.asarray(Y, float), np.asarray(Z, float))
+    KW, _ = kron_parts(np.asarray(Z, float), np.asarray(X, float))
+    return shape, np.asarray(U, float) @ KU, np.asarray(V, float) @ KV, np.asarray(W, float) @ KW
+
+
+def act_exact(D, X, Y, Z):
+    """D . (X, Y, Z) in rational arithmetic (X, Y, Z of Fractions or ints)."""
+    shape, U, V, W = D
+
+    def kron_inv_t(P, Q):
+        Ni = sympy.Matrix(Q).inv().T
+        return sympy.kronecker_product(sympy.Matrix(P), Ni)
+
+    def rows(M, K):
+        return [list(sympy.Matrix([[sympy.Rational(str(Fraction(x))) for x in r]]) * K) for r in np.asarray(M).tolist()]
+    X, Y, Z = ([[sympy.Rational(str(Fraction(x))) for x in r] for r in M] for M in (X, Y, Z))
+    return (shape, rows(U, kron_inv_t(X, Y)), rows(V, kron_inv_t(Y, Z)), rows(W, kron_inv_t(Z, X)))
+
+
+def phi_and_grad(D, g):
+    """Phi(D . g) and its gradient over the m^2 + k^2 + n^2 entries of g."""
+    (m, k, n), U, V, W = D
+    U, V, W = (np.asarray(M, dtype=np.float64) for M in (U, V, W))
+    X, Y, Z = split_g(g, (m, k, n))
+    KU, NY = kron_parts(X, Y)
+    KV, NZ = kron_parts(Y, Z)
+    KW, NX = kron_parts(Z, X)
+    uK, vK, wK = U @ KU, V @ KV, W @ KW
+    a, b, c = (np.sum(M * M, axis=1) for M in (uK, vK, wK))
+    phi = float(np.sum(a * b * c))
+    HU = 2.0 * np.einsum("r,ra,rc->ac", b * c, U, uK)      # dPhi/dK_U
+    HV = 2.0 * np.einsum("r,ra,rc->ac", a * c, V, vK)
+    HW = 2.0 * np.einsum("r,ra,rc->ac", a * b, W, wK)
+
+    def parts(H, P, N):
+        p, q = P.shape[0], N.shape[0]
+        H4 = H.reshape(p, q, p, q)                          # [i, j, i', j']
+        return np.einsum("ijkl,jl->ik", H4, N), np.einsum("ijkl,ik->jl", H4, P)
+
+    dX1, dNY = parts(HU, X, NY)
+    dY1, dNZ = parts(HV, Y, NZ)
+    dZ1, dNX = parts(HW, Z, NX)
+    dY2 = -NY @ dNY.T @ NY          # N = Q^-T: dN = -N dQ^T N
+    dZ2 = -NZ @ dNZ.T @ NZ
+    dX2 = -NX @ dNX.T @ NX
+    return phi, np.concatenate([(dX1 + dX2).ravel(), (dY1 + dY2).ravel(), (dZ1 + dZ2).ravel()])
+
+
+def brent_residual(D) -> float:
+    """max |sum_r U_r (x) V_r (x) W_r - <m,k,n>| in binary64."""
+    (m, k, n), U, V, W = D
+    T = np.einsum("ra,rb,rc->abc", np.asarray(U, float), np.asarray(V, float), np.asarray(W, float))
+    want = np.zeros_like(T)
+    for i in range(m):
+        for j in range(k):
+            for l in range(n):
+                want[i * k + j, j * n + l, l * m + i] = 1.0
+    return float(np.abs(T - want).max())
+
+
+def rebase(D, starts=None, max_iter: int = 1000, gtol: float = 1e-10, tol: float = 1e-9):
+    """(D . g of least Phi, that Phi, terminal Phi per start) over the identity
+    start and ``starts``; NaN marks a start that ended singular, non-finite or
+    not exact within ``tol``."""
+    from scipy.optimize import minimize
+    (m, k, n) = D[0]
+    ident = np.concatenate([np.eye(m).ravel(), np.eye(k).ravel(), np.eye(n).ravel()])
+    xs = [ident] + ([] if starts is None else list(np.asarray(starts, dtype=np.float64)))
+
+    def f(x):
+        try:
+            return phi_and_grad(D, x)
+        except np.linalg.LinAlgError:
+            return np.inf, np.zeros_like(x)
+    best, best_phi, terminal = None, np.inf, []
+    for x0 in xs:
+        res = minimize(f, np.array(x0), jac=True, method="L-BFGS-B",
+                       options={"maxiter": max_iter, "gtol": gtol, "ftol": 1e-16, "maxcor": 10})
+        t = np.nan
+        try:
+            Dg = act(D, *split_g(res.x, (m, k, n)))
+            p = phi(Dg)
+            if np.isfinite(p) and brent_residual(Dg) <= tol:
+                t = p
+                if p < best_phi:
+                    best, best_phi = Dg, p
+        except np.linalg.LinAlgError:
+            pass
+        terminal.append(t)
+    return best, best_phi, np.array(terminal)

@@ -224,10 +224,17 @@ def fmm_realization_create(U, V, w, tol: float = 1e-9, shape=(2, 2, 2)) -> Reali
     return Realization(h.value)
 
 
+def _orbit_sizes(d: Realization):
+    (m, k, n), _ = fmm_realization_shape(d)
+    return m * m, k * k, n * n
+
+
 def fmm_realization_transform(d: Realization, X, Y, Z) -> Realization:
-    Xa, Xp = _darr(X, 4)
-    Ya, Yp = _darr(Y, 4)
-    Za, Zp = _darr(Z, 4)
+    """D . (X, Y, Z): 2 x 2 factors at <2,2,2>; m x m, k x k, n x n for another shape."""
+    sx, sy, sz = _orbit_sizes(d)
+    Xa, Xp = _darr(X, sx)
+    Ya, Yp = _darr(Y, sy)
+    Za, Zp = _darr(Z, sz)
     h = _vp()
     _check(_lib.fmm_realization_transform(d.handle, Xp, Yp, Zp, ctypes.byref(h)),
            "fmm_realization_transform")
@@ -237,13 +244,15 @@ def fmm_realization_transform(d: Realization, X, Y, Z) -> Realization:
 def fmm_realization_optimize(d: Realization, starts=None, max_iter: int = 1000, gtol: float = 1e-10,
                              tol: float = 1e-9):
     """Re-basing: (realization of least Phi, its Phi, per-start terminal Phi).
-    starts: None or an (n, 12) array of (X, Y, Z) triples, row-major 2x2 each;
-    the identity start is always run first."""
+    starts: None or an (n, P) array of (X, Y, Z) triples, row-major each
+    (P = 12 at <2,2,2>, m^2 + k^2 + n^2 for another shape); the identity
+    start is always run first."""
     import numpy as np
+    P = sum(_orbit_sizes(d))
     if starts is None:
         n, sp = 0, None
     else:
-        sa = np.ascontiguousarray(starts, dtype=np.float64).reshape(-1, 12)
+        sa = np.ascontiguousarray(starts, dtype=np.float64).reshape(-1, P)
         n, sp = sa.shape[0], sa.ctypes.data_as(_dp)
     start_phi = np.empty(n + 1, dtype=np.float64)
     phi = ctypes.c_double()
@@ -255,10 +264,12 @@ def fmm_realization_optimize(d: Realization, starts=None, max_iter: int = 1000, 
 
 
 def fmm_realization_phi_gradient(d: Realization, g):
-    """(Phi(D . g), gradient over the 12 entries of g = (X, Y, Z))."""
+    """(Phi(D . g), gradient over the P entries of g = (X, Y, Z); P = 12 at
+    <2,2,2>, m^2 + k^2 + n^2 for another shape)."""
     import numpy as np
-    ga, gp = _darr(g, 12)
-    grad = np.empty(12, dtype=np.float64)
+    P = sum(_orbit_sizes(d))
+    ga, gp = _darr(g, P)
+    grad = np.empty(P, dtype=np.float64)
     phi = ctypes.c_double()
     _check(_lib.fmm_realization_phi_gradient(d.handle, gp, ctypes.byref(phi), grad.ctypes.data_as(_dp)),
            "fmm_realization_phi_gradient")

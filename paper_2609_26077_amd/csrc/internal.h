@@ -3,6 +3,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include "../../include/fmm8.h"
 
@@ -45,6 +46,17 @@ struct Shaped {
 };
 double brent_residual_shape(const Shaped &s);
 void phi_gamma_shape(const Shaped &s, double &phi, double &gamma);
+// inverse of the n x n row-major G by Gauss-Jordan elimination with partial
+// pivoting in binary64; returns the determinant (0 when a pivot vanishes)
+double inverse_gj(const double *G, int n, double *inv);
+// D . g for X (m x m), Y (k x k), Z (n x n), row-major: U' rows = u (X (x) Y^-T)
+// etc.; FMM_ERR_SINGULAR if some |det| < 1e-12
+int transform_shape(const Shaped &s, const double *X, const double *Y, const double *Z, std::vector<double> &U,
+                    std::vector<double> &V, std::vector<double> &W);
+double rebase_phi_grad_shape(const Shaped &S, const double *g, double *grad);
+int realization_optimize_shape(const Shaped &S, int nstarts, const double *starts, int max_iter, double gtol,
+                               double tol, std::vector<double> &U, std::vector<double> &V, std::vector<double> &W,
+                               double &best_phi, double *start_phi);
 
 // ---- device-side coefficient tables -------------------------------------
 // For one operand side: the nonzero coefficients of each flattened term in

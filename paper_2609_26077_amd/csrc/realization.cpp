@@ -11,6 +11,7 @@
 #include <initializer_list>
 #include <cstring>
 #include <new>
+#include <utility>
 #include <vector>
 
 namespace fmm {
@@ -274,6 +275,75 @@ double sq_norm_n(const double *v, int len) {
 }
 }  // namespace
 
+double inverse_gj(const double *G, int n, double *inv) {
+  std::vector<double> A(G, G + (size_t)n * n);
+  for (int i = 0; i < n * n; ++i) inv[i] = 0.0;
+  for (int i = 0; i < n; ++i) inv[i * n + i] = 1.0;
+  double det = 1.0;
+  for (int c = 0; c < n; ++c) {
+    int piv = c;
+    for (int r = c + 1; r < n; ++r)
+      if (std::fabs(A[r * n + c]) > std::fabs(A[piv * n + c])) piv = r;
+    const double pv = A[piv * n + c];
+    if (pv == 0.0 || !std::isfinite(pv)) return 0.0;
+    if (piv != c) {
+      for (int j = 0; j < n; ++j) {
+        std::swap(A[piv * n + j], A[c * n + j]);
+        std::swap(inv[piv * n + j], inv[c * n + j]);
+      }
+      det = -det;
+    }
+    det = det * pv;
+    for (int j = 0; j < n; ++j) {
+      A[c * n + j] = A[c * n + j] / pv;
+      inv[c * n + j] = inv[c * n + j] / pv;
+    }
+    for (int r = 0; r < n; ++r) {
+      if (r == c) continue;
+      const double f = A[r * n + c];
+      if (f == 0.0) continue;
+      for (int j = 0; j < n; ++j) {
+        A[r * n + j] = A[r * n + j] - f * A[c * n + j];
+        inv[r * n + j] = inv[r * n + j] - f * inv[c * n + j];
+      }
+    }
+  }
+  return det;
+}
+
+namespace {
+// rows of M (R x p q) times K = P (x) Qinv^T (K[a q + b][a' q + b'] = P[a][a'] Qinv[b'][b]),
+// each output entry summed over the input index in ascending order
+void rows_times_kron(const double *M, int R, const double *P, int p, const double *Qinv, int q,
+                     std::vector<double> &out) {
+  const int w = p * q;
+  std::vector<double> K((size_t)w * w);
+  for (int a = 0; a < p; ++a)
+    for (int b = 0; b < q; ++b)
+      for (int a2 = 0; a2 < p; ++a2)
+        for (int b2 = 0; b2 < q; ++b2) K[(size_t)(a * q + b) * w + a2 * q + b2] = P[a * p + a2] * Qinv[b2 * q + b];
+  out.assign((size_t)R * w, 0.0);
+  for (int r = 0; r < R; ++r)
+    for (int c = 0; c < w; ++c) {
+      double s = M[(size_t)r * w] * K[c];
+      for (int a = 1; a < w; ++a) s = s + M[(size_t)r * w + a] * K[(size_t)a * w + c];
+      out[(size_t)r * w + c] = s;
+    }
+}
+}  // namespace
+
+int transform_shape(const Shaped &s, const double *X, const double *Y, const double *Z, std::vector<double> &U,
+                    std::vector<double> &V, std::vector<double> &W) {
+  std::vector<double> Xi((size_t)s.m * s.m), Yi((size_t)s.k * s.k), Zi((size_t)s.n * s.n);
+  const double dets[3] = {inverse_gj(X, s.m, Xi.data()), inverse_gj(Y, s.k, Yi.data()), inverse_gj(Z, s.n, Zi.data())};
+  for (double d : dets)
+    if (!(std::fabs(d) >= 1e-12)) return FMM_ERR_SINGULAR;
+  rows_times_kron(s.U, s.R, X, s.m, Yi.data(), s.k, U);     // u (X (x) Y^-T)
+  rows_times_kron(s.V, s.R, Y, s.k, Zi.data(), s.n, V);     // v (Y (x) Z^-T)
+  rows_times_kron(s.W, s.R, Z, s.n, Xi.data(), s.m, W);     // w (Z (x) X^-T)
+  return FMM_OK;
+}
+
 void phi_gamma_shape(const Shaped &s, double &phi, double &gamma) {
   phi = 0.0;
   gamma = 0.0;
@@ -370,7 +440,25 @@ int fmm_realization_transform(const fmm_real *d, const double X[4], const double
   if (!out) return FMM_ERR_ARG;
   *out = nullptr;
   if (!d || !X || !Y || !Z) return FMM_ERR_ARG;
-  if (!d->is222()) return FMM_ERR_UNSUPPORTED;
+  if (!d->is222()) {
+    fmm_real *h = new (std::nothrow) fmm_real;
+    if (!h) return FMM_ERR_NOMEM;
+    int st;
+    try {
+      h->m = d->m; h->k = d->k; h->n = d->n;
+      std::memset(&h->d, 0, sizeof(h->d));
+      h->d.R = d->d.R;
+      st = fmm::transform_shape(d->shaped(), X, Y, Z, h->U, h->V, h->W);
+    } catch (...) {
+      st = FMM_ERR_NOMEM;
+    }
+    if (st != FMM_OK) {
+      delete h;
+      return st;
+    }
+    *out = h;
+    return FMM_OK;
+  }
   fmm_real *h = new (std::nothrow) fmm_real;
   if (!h) return FMM_ERR_NOMEM;
   const int st = fmm::realization_transform(d->d, X, Y, Z, h->d);

@@ -153,10 +153,14 @@ def test_empty_contraction_and_batch():
 
 def test_cross_shape_predictor_matches_oracle():
     """The cross-shape control (Table E.1's setting) on three rows and two
-    samples: each row's mean relative Frobenius error e and its cubic
-    reference e_cubic equal the oracle's on the same operands to 1%, and the
-    reported predictors are the realizations' own."""
+    samples: each row's mean relative Frobenius error e, its cubic reference
+    e_cubic and the error of its re-based realization equal the oracle's on
+    the same operands to 1% (the re-based realization, the library's
+    optimizer's output from the control's own starts, is the oracle's input),
+    and the reported Phi are the realizations' own."""
     import math
+    import fmm_inputs as gen_
+    import paper_2609_26077_amd as fm
     from paper_2609_26077_amd import controls
     out = controls.cross_shape_predictor(rows=("strassen", "223_11", "333_26"), samples=2, edge=256)
     for row in out["rows"]:
@@ -166,10 +170,14 @@ def test_cross_shape_predictor_matches_oracle():
         if name == "strassen":
             D = S.from_222(R.builtin_f64("strassen"))
             C = S.from_222(R.builtin_f64("cubic8"))
+            lib = fm.fmm_realization_builtin("strassen")
         else:
             D = S.build(name, R.builtin_f64)
             C = S.cubic(m, k, n)
-        for real, key in ((D, "e"), (C, "e_cubic")):
+            lib = controls.shaped_realization(name)
+        reb, phi_reb, _ = fm.fmm_realization_optimize(lib, gen_.rebasing_starts_shape(23, m, k, n, seed=0, cfg=16))
+        Dreb = ((m, k, n),) + tuple(fm.fmm_realization_coefficients(reb))
+        for real, key in ((D, "e"), (C, "e_cubic"), (Dreb, "e_rebased")):
             rel = []
             for b in range(2):
                 o = O.fmm_shape(A[b], B[b], real, 128, e4m3.RULE_FP32_AMAX)
@@ -177,4 +185,7 @@ def test_cross_shape_predictor_matches_oracle():
                 rel.append(math.sqrt(e2 / r2))
             assert row[key] == pytest.approx(np.mean(rel), rel=0.01), (name, key)
         assert row["phi"] == pytest.approx(O.phi(D), rel=1e-14)
+        assert row["phi_rebased"] == pytest.approx(phi_reb, rel=1e-14)
+        assert row["phi_rebased"] < row["phi"] * (1 - 1e-9)
+    assert out["error_lowered_rows"] == out["rebased_rows"] == 3
     print(out, flush=True)

@@ -88,18 +88,84 @@ def test_gauge_of_other_shapes(fm):
     assert mg["phi"] == pytest.approx(fm.fmm_realization_metrics(d, 1)["phi"], rel=1e-14)
 
 
-def test_222_only_calls_refuse_other_shapes(fm):
+def test_deeper_levels_refuse_other_shapes(fm):
     d = lib_shaped(fm, "223_11")
-    I = np.eye(2).ravel()
-    for call in (lambda: fm.fmm_realization_transform(d, I, I, I),
-                 lambda: fm.fmm_realization_optimize(d),
-                 lambda: fm.fmm_realization_phi_gradient(d, np.tile(I, 3)),
-                 lambda: fm.fmm_realization_metrics(d, 2),
+    for call in (lambda: fm.fmm_realization_metrics(d, 2),
                  lambda: fm.fmm_realization_terms(d, 2),
                  lambda: fm.fmm_realization_tables(d, 2)):
         with pytest.raises(fm.FmmError) as e:
             call()
         assert e.value.status == fm.FMM_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("name", ["223_11", "232_11", "333_26", "525_46"])
+def test_transform_matches_oracle(fm, name):
+    """The orbit action u -> u (X (x) Y^-T) etc. over GL(m) x GL(k) x GL(n):
+    the library (Gauss-Jordan inverses) against the oracle (numpy's) to
+    rounding, and the result exact to rounding."""
+    import fmm_inputs as gen
+    d = lib_shaped(fm, name)
+    D = S.build(name, R.builtin_f64)
+    (m, k, n) = D[0]
+    for g in gen.rebasing_starts_shape(4, m, k, n, seed=0, cfg=21):
+        X, Y, Z = O.split_g(g, (m, k, n))
+        got = fm.fmm_realization_coefficients(fm.fmm_realization_transform(d, X, Y, Z))
+        want = O.act(D, X, Y, Z)[1:]
+        for a, b in zip(got, want):
+            assert np.allclose(a, b, rtol=1e-13, atol=1e-13 * np.abs(b).max())
+        assert fm.fmm_realization_metrics(fm.fmm_realization_transform(d, X, Y, Z))["brent_residual"] < 1e-12
+
+
+def test_transform_rejects_singular(fm):
+    d = lib_shaped(fm, "223_11")
+    Z = np.eye(3); Z[2] = Z[1]
+    with pytest.raises(fm.FmmError) as e:
+        fm.fmm_realization_transform(d, np.eye(2), np.eye(2), Z)
+    assert e.value.status == fm.FMM_ERR_SINGULAR
+
+
+@pytest.mark.parametrize("name", ["223_11", "333_26", "525_46"])
+def test_phi_gradient_matches_oracle(fm, name):
+    """The library's closed-form gradient (2 X^-T sum_r (b c U'U'^T -
+    a b W'^T W') and its companions) against the oracle's chain rule through
+    the Kronecker matrices."""
+    import fmm_inputs as gen
+    d = lib_shaped(fm, name)
+    D = S.build(name, R.builtin_f64)
+    (m, k, n) = D[0]
+    for g in gen.rebasing_starts_shape(3, m, k, n, seed=0, cfg=22):
+        phi, grad = fm.fmm_realization_phi_gradient(d, g)
+        phi_o, grad_o = O.phi_and_grad(D, g)
+        assert phi == pytest.approx(phi_o, rel=1e-13)
+        assert np.allclose(grad, grad_o, rtol=1e-11, atol=1e-11 * np.abs(grad_o).max())
+
+
+def test_optimize_matches_oracle(fm):
+    """Re-basing <2,2,3;11> from the identity and 8 perturbed starts: the
+    least terminal Phi equals the oracle's (scipy L-BFGS-B from the same
+    starts), every start's terminal realization is exact, and Phi drops
+    from 36."""
+    import fmm_inputs as gen
+    d = lib_shaped(fm, "223_11")
+    D = S.build("223_11", R.builtin_f64)
+    starts = gen.rebasing_starts_shape(8, 2, 2, 3, seed=0, cfg=23)
+    best, phi, term = fm.fmm_realization_optimize(d, starts)
+    _, phi_o, term_o = O.rebase(D, starts)
+    assert phi == pytest.approx(phi_o, rel=1e-9)
+    assert phi < 36.0 - 1.0
+    assert fm.fmm_realization_metrics(best)["brent_residual"] < 1e-12
+    assert np.all(np.isfinite(term))
+
+
+def test_optimize_cubic_returns_mkn(fm):
+    """The cubic algorithm's orbit minimum is mkn (the oracle's test states
+    why): from random starts the library returns 24 for <2,3,4>."""
+    import fmm_inputs as gen
+    from paper_2609_26077_amd.controls import shaped_realization
+    d = shaped_realization("cubic_234")
+    best, phi, term = fm.fmm_realization_optimize(d, gen.rebasing_starts_shape(4, 2, 3, 4, seed=0, cfg=24))
+    assert phi == pytest.approx(24.0, rel=1e-9)
+    assert np.allclose(term, 24.0, rtol=1e-8)
 
 
 @pytest.mark.parametrize("name,desc,status", [

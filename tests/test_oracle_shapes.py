@@ -112,3 +112,96 @@ def test_model_predicts_measured(name):
     s_a2, s_b2 = np.mean(sa), np.mean(sb)
     pred = (s_a2 + s_b2 + s_a2 * s_b2) * shapes.phi(D) / (m * k * n)
     assert pred / rel == pytest.approx(1.0, abs=0.06), (pred, rel)
+
+
+# ---- the orbit GL(m) x GL(k) x GL(n) and re-basing ---------------------------
+
+def rational_g(rng, shape):
+    """A random rational (X, Y, Z) with nonzero determinants."""
+    from fractions import Fraction
+    out = []
+    for size in shape:
+        while True:
+            M = [[Fraction(int(rng.integers(-4, 5)), int(rng.integers(1, 4))) + (1 if i == j else 0)
+                  for j in range(size)] for i in range(size)]
+            import sympy
+            if sympy.Matrix(M).det() != 0:
+                out.append(M)
+                break
+    return out
+
+
+@pytest.mark.parametrize("name", ["223_11", "232_11", "333_26"])
+def test_action_keeps_exactness_in_rational_arithmetic(name):
+    """u -> u (X (x) Y^-T) and its cyclic companions keep the Brent equations
+    exactly (<U', A> = <U, X A Y^-1>, so the trilinear form becomes
+    tr(X A B C X^-1)); Y^-1 in place of Y^-T breaks them."""
+    import sympy
+    D = shaped(name)
+    rng = np.random.default_rng(3)
+    X, Y, Z = rational_g(rng, D[0])
+    Dg = shapes.act_exact(D, X, Y, Z)
+    assert shapes.brent_exact(Dg)
+    # the plausible slip: no transpose on the inverse
+    (m, k, n), U, V, W = D
+    Ky = sympy.kronecker_product(sympy.Matrix(X), sympy.Matrix(Y).inv())
+    bad = (D[0], [list(sympy.Matrix([[sympy.Rational(x) for x in r]]) * Ky) for r in np.asarray(U).astype(int).tolist()],
+           Dg[2], Dg[3])
+    assert not shapes.brent_exact(bad)
+
+
+def test_action_at_222_is_the_222_oracles():
+    D = R.builtin_f64("strassen")
+    for g in gen.basis_changes(5, seed=0, cfg=17):
+        _, U, V, W = shapes.act(S.from_222(D), *g)
+        want = R.act_f64(D, g)
+        for a, b in zip((U, V, W), want):
+            assert np.allclose(a, np.asarray(b, float), rtol=1e-14, atol=1e-14)
+
+
+@pytest.mark.parametrize("name", ["223_11", "333_26", "525_46"])
+def test_gradient_against_central_differences(name):
+    D = shaped(name)
+    (m, k, n) = D[0]
+    g = gen.rebasing_starts_shape(1, m, k, n, seed=0, cfg=18)[0]
+    f, grad = shapes.phi_and_grad(D, g)
+    h = 1e-6
+    for i in range(0, g.size, max(1, g.size // 12)):
+        e = np.zeros_like(g); e[i] = h
+        fd = (shapes.phi_and_grad(D, g + e)[0] - shapes.phi_and_grad(D, g - e)[0]) / (2 * h)
+        assert fd == pytest.approx(grad[i], rel=1e-6, abs=1e-6 * np.abs(grad).max())
+
+
+@pytest.mark.parametrize("mkn", [(2, 2, 3), (2, 3, 4), (3, 3, 3)])
+def test_cubic_orbit_minimum_is_mkn(mkn):
+    """The cubic algorithm's orbit has Phi >= mkn, equality at g = 1: term
+    (i, j, l) maps to rank-one matrices, |X^T e_i e_j^T Y^-T|^2 =
+    |X^T e_i|^2 |Y^-1 e_j|^2, so Phi(cubic . g) factors into
+    (sum_i |X^T e_i|^2 |X^-1 e_i|^2)(sum_j ...)(sum_l ...), and each summand
+    is >= 1 by Cauchy-Schwarz, since row i of X times column i of X^-1 is 1.
+    Random orbit points respect the bound and re-basing from random starts
+    returns mkn."""
+    m, k, n = mkn
+    C = S.cubic(m, k, n)
+    starts = gen.rebasing_starts_shape(6, m, k, n, seed=0, cfg=19)
+    for g in starts:
+        assert shapes.phi(shapes.act(C, *shapes.split_g(g, mkn))) >= m * k * n * (1 - 1e-12)
+    _, best, term = shapes.rebase(C, starts)
+    assert best == pytest.approx(m * k * n, rel=1e-9)
+    assert np.allclose(term, m * k * n, rtol=1e-8)
+
+
+def test_scalar_gauge_leaves_phi():
+    D = shaped("333_26")
+    I3 = np.eye(3)
+    assert shapes.phi(shapes.act(D, 2.0 * I3, 0.5 * I3, 3.0 * I3)) == pytest.approx(shapes.phi(D), rel=1e-14)
+
+
+def test_rebase_lowers_phi_and_stays_exact():
+    D = shaped("223_11")
+    best, phi, term = shapes.rebase(D, gen.rebasing_starts_shape(5, 2, 2, 3, seed=0, cfg=20))
+    assert phi < shapes.phi(D) - 1.0
+    assert shapes.brent_residual(best) < 1e-12
+    ident = np.concatenate([np.eye(2).ravel(), np.eye(2).ravel(), np.eye(3).ravel()])
+    _, grad = shapes.phi_and_grad(best, ident)          # stationary where it ended
+    assert np.abs(grad).max() <= 1e-6 * phi
