@@ -539,7 +539,7 @@ __device__ __forceinline__ uint32_t quantize4(const Problem &pb, float m, float 
 constexpr bool narrow_b3(int side, int bs) { return side == 1 && bs <= 256 / kB3Rows; }
 
 template <int SIDE, int BS, bool F32, bool GEN = false>
-__global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) void encode4_kernel(
+__global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads), 8) void encode4_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l) {
   using TT = Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>;
@@ -563,60 +563,92 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads)) v
   const int row = pos / (TL / 4), c4 = pos % (TL / 4);
   static_assert(BS <= TL, "a block lies in one row of the tile");
   const Out o = out_of(pb, rows, row0 + row, l0 + 4 * c4, (c4 % GL) == 0);
+  // a lane's offsets inside a (batch, term) plane fit in 32 bits
+  const uint32_t o_code = (uint32_t)o.code, o_scale = (uint32_t)o.scale;
+  const bool o_valid = o.valid, o_leader = o.leader;
   const int64_t code_plane = rows * pb.kp;
   const int64_t scale_plane = scale_plane_of(pb, rows);
   const float *lrow = lds + row * STR + 4 * c4;
-  // the term's dense coefficient row (block b in lane b; 64 blocks) is loaded
-  // one term ahead by a vector load; its nonzero blocks come from the wave's
-  // ballot in ascending order, four per pass
+  // A wave takes a group of up to kG consecutive terms at once: at depth 3 the
+  // R terms that share their two outer digits (T* flattened: 17 nonzero
+  // blocks per term on average, 26 in the union of a group of 7), so each
+  // block is read from LDS once per group rather than once per term.  Every
+  // term's x = sum_b c_b a_b still runs over its own nonzero blocks in
+  // ascending b with products and sums rounded separately, its first block
+  // giving x = c a.  The terms' dense coefficient rows (block b in lane b)
+  // give each term's nonzero blocks by a ballot; their union is walked in
+  // ascending order.
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  constexpr int WSTEP = NT / 64;             // a wave per term
-  float cnext = 0.0f;
-  if (wave < T) cnext = cf.dense[wave * 64 + lane];
-  for (int64_t r = wave; r < T; r += WSTEP) {
-    const float c = cnext;
-    if (r + WSTEP < T) cnext = cf.dense[(r + WSTEP) * 64 + lane];
-    uint64_t mask = __ballot(c != 0.0f);
-    float x0 = 0.f, x1 = 0.f, x2 = 0.f, x3 = 0.f;
-    bool first = true;
-    while (mask != 0) {
-      int b[4];
-      bool have[4];
-      b[0] = next_block(mask, 0);
-      have[0] = true;
+  // Whole rounds of groups (every wave one group per round) go first; the
+  // terms left over are taken one per wave, which keeps the waves' loads
+  // within one term of each other (343 terms in groups of 7: 48 groups in
+  // three rounds, then 7 single terms).
+  constexpr int WSTEP = NT / 64;
+  constexpr int kG = 8;
+  const int G = GEN ? kG : pb.R;             // R <= 8 at <2,2,2>
+  const int64_t nfull = ((T + G - 1) / G / WSTEP) * WSTEP;      // groups taken in whole rounds
+  const int64_t tail0 = nfull * G < T ? nfull * G : T;          // the first term taken alone
+  const int64_t units = nfull + (T - tail0);
+  for (int64_t u = wave; u < units; u += WSTEP) {
+    const int64_t g0 = u < nfull ? u * G : tail0 + (u - nfull);
+    const int gn = u < nfull ? (int)(T - g0 < G ? T - g0 : G) : 1;
+    float c[kG];
 #pragma unroll
-      for (int j = 1; j < 4; ++j) {
-        have[j] = mask != 0;
-        b[j] = next_block(mask, b[j - 1]);
-      }
-      float4 v[4];
+    for (int j = 0; j < kG; ++j) c[j] = j < gn ? cf.dense[(g0 + j) * 64 + lane] : 0.0f;
+    uint64_t m[kG];
+    uint64_t uni = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4 *>(lrow + b[j] * (TR * STR));
+    for (int j = 0; j < kG; ++j) {
+      m[j] = __ballot(c[j] != 0.0f);
+      uni |= m[j];
+    }
+    // accumulators start at -0: -0 + t = t exactly for every t, so a term's
+    // first block gives x = c a as the definition does; a term without
+    // nonzero blocks ends at +0
+    float x[kG][4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (have[j]) {
-          const float cb = lane_coef(c, b[j]);
-          const float t0 = __fmul_rn(cb, v[j].x), t1 = __fmul_rn(cb, v[j].y);
-          const float t2 = __fmul_rn(cb, v[j].z), t3 = __fmul_rn(cb, v[j].w);
-          if (first && j == 0) {
-            x0 = t0; x1 = t1; x2 = t2; x3 = t3;
-          } else {
-            x0 = __fadd_rn(x0, t0); x1 = __fadd_rn(x1, t1);
-            x2 = __fadd_rn(x2, t2); x3 = __fadd_rn(x3, t3);
+    for (int j = 0; j < kG; ++j) x[j][0] = x[j][1] = x[j][2] = x[j][3] = -0.0f;
+    if (uni != 0) {
+      // the next block's values are read while this block's are used
+      int b = __builtin_ctzll(uni);
+      uni &= uni - 1;
+      float4 v = *reinterpret_cast<const float4 *>(lrow + b * (TR * STR));
+      while (true) {
+        const bool more = uni != 0;
+        const int bn = more ? __builtin_ctzll(uni) : b;
+        uni &= uni - 1;
+        const float4 vn = *reinterpret_cast<const float4 *>(lrow + bn * (TR * STR));
+#pragma unroll
+        for (int j = 0; j < kG; ++j) {
+          if ((m[j] >> b) & 1) {
+            const float cb = lane_coef(c[j], b);
+            x[j][0] = __fadd_rn(x[j][0], __fmul_rn(cb, v.x));
+            x[j][1] = __fadd_rn(x[j][1], __fmul_rn(cb, v.y));
+            x[j][2] = __fadd_rn(x[j][2], __fmul_rn(cb, v.z));
+            x[j][3] = __fadd_rn(x[j][3], __fmul_rn(cb, v.w));
           }
         }
+        if (!more) break;
+        b = bn;
+        v = vn;
       }
-      first = false;
     }
-    const float m = __uint_as_float(
-        group_max_bits<GL>(__float_as_uint(fmaxf(fmaxf(fabsf(x0), fabsf(x1)), fmaxf(fabsf(x2), fabsf(x3))))));
-    uint32_t stored;
-    const uint32_t w = quantize4<F32>(pb, m, x0, x1, x2, x3, stored);
-    // the plane's base is uniform; a lane's offset inside it fits in 32 bits
-    const int64_t plane = bt * T + r;
-    if (o.valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + (uint32_t)o.code) = w;
-    if (o.leader) store_scale(pb, scales, plane * scale_plane + (uint32_t)o.scale, stored);
+#pragma unroll
+    for (int j = 0; j < kG; ++j)
+      if (m[j] == 0) x[j][0] = x[j][1] = x[j][2] = x[j][3] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kG; ++j) {
+      if (j < gn) {
+        const float mx = __uint_as_float(group_max_bits<GL>(__float_as_uint(
+            fmaxf(fmaxf(fabsf(x[j][0]), fabsf(x[j][1])), fmaxf(fabsf(x[j][2]), fabsf(x[j][3]))))));
+        uint32_t stored;
+        const uint32_t w = quantize4<F32>(pb, mx, x[j][0], x[j][1], x[j][2], x[j][3], stored);
+        const int64_t plane = bt * T + g0 + j;      // uniform
+        if (o_valid) *reinterpret_cast<uint32_t *>(codes + plane * code_plane + o_code) = w;
+        if (o_leader) store_scale(pb, scales, plane * scale_plane + o_scale, stored);
+      }
+    }
   }
 }
 
