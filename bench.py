@@ -473,7 +473,7 @@ def main():
         prod_kernel = ("gemm_exact256x128_kernel" if sb == 4 else
                        "gemm_dq256x128_kernel" if exact else "gemm_tile256x256_kernel")
     elif a_view.code_layout == 2:
-        prod_kernel = "gemm_mx_fast_kernel" + (" (exact-dot form)" if exact else "")
+        prod_kernel = "gemm_dq8_kernel" if exact else "gemm_mx_fast_kernel"
     else:
         prod_kernel = "gemm_promote_kernel" if exact else "gemm_mx_kernel"
     traffic = None

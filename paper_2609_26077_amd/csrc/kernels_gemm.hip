@@ -19,11 +19,13 @@
 // products to the group's largest and keeps 13 bits below it (measured:
 // 1 + 2^-13 survives, 1 + 2^-14 returns 1; groups are summed at fp32 grade).
 //
-// Exact-dot path (fp32 scales, block 16, or FMM_FLAG_EXACT_DOT): the codes are
-// converted exactly to bf16 (v_cvt_scalef32_pk_bf16_fp8 at scale 1) and fed to
-// v_mfma_f32_32x32x16_bf16 (lane (r, h) holds row r, elements [8h, 8h+8);
-// 23 retained bits), summed per block in a temporary and scaled by sA * sB in
-// fp32 -- the products of the dequantized operands accumulated in fp32.
+// Exact-dot paths (FMM_FLAG_EXACT_DOT, fp32 scales or block 16): the codes are
+// converted exactly to bf16 and fed to v_mfma_f32_32x32x16_bf16 (lane (r, h)
+// holds row r, elements [8h, 8h+8); 23 retained bits).  With E8M0 scales on
+// the tile layout (gemm_dq8_kernel) each code's conversion applies its block's
+// power of two; otherwise (gemm_promote_kernel) the codes convert at scale 1,
+// each block's products are summed in a temporary and scaled by sA * sB in
+// fp32 -- in both, the products of the dequantized operands accumulated in fp32.
 //
 // Output layout of the 32x32 instructions: lane l, register j holds
 // column l % 32, row 8 (j / 4) + 4 (l / 32) + j % 4.
@@ -381,9 +383,8 @@ __device__ __forceinline__ void item_of(int tiles_m, int tiles_n, int &tm, int &
 }
 
 // Operands of one K step for one wave: fragments [substep s][tile i] and,
-// for each of its A and B row tiles, the E8M0 scale bytes: on the fp8 path
-// the two of the lane's blocks (byte s: substep s), on the exact-dot path
-// the row's whole record of the step.
+// for each of its A and B row tiles, the E8M0 scale bytes of the lane's two
+// blocks (byte s: substep s).
 struct MxFrags {
   v8i a[2][2], b[2][2];
   int sa[2], sb[2];
@@ -407,18 +408,8 @@ __device__ __forceinline__ float e8m0_at(int w, int i) {
   return __uint_as_float((((uint32_t)w >> (8 * i)) & 0xffu) << 23);
 }
 
-// DQ = false: the fp8 matrix cores with the E8M0 scales applied by the
-// scaled MFMA.  DQ = true (exact-dot plans with E8M0 scales): the same
-// transfers, fragments and fused W-combine, but every 64-byte substep runs as
-// four v_mfma_f32_32x32x16_bf16 per tile pair on the dequantized operands,
-// each code converted to bf16 together with its block's power of two
-// (v_cvt_scalef32_pk_bf16_fp8; exact for every scale the rules produce), so
-// the products of the dequantized operands are summed across the whole
-// contracted axis at fp32 grade.  Instruction t of substep s takes, in lane
-// half h, bytes 64 s + 32 (t >> 1) + 16 h + 8 (t & 1) .. + 7 of the row on both
-// operands, which lie in block 2 s + (t >> 1) at block 32 (record byte
-// 2 (t >> 1) + s, the record holding blocks 0, 2, 1, 3).
-template <int BS, bool DQ>
+// The fp8 matrix cores with the E8M0 scales applied by the scaled MFMA.
+template <int BS>
 __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, int tiles_m) {
   __shared__ uint4 lds_raw[kSlots * kSlot / 16];
   __shared__ float lds_w[4 * kMaxRank];
@@ -478,13 +469,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     const uint8_t *lsb = lsa + BM * 4;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      if (DQ) {
-        f.sa[i] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + 32 * i + r32));
-        f.sb[i] = *reinterpret_cast<const int *>(lsb + 4 * (wrow_b + 32 * i + r32));
-      } else {
-        f.sa[i] = *reinterpret_cast<const uint16_t *>(lsa + 4 * (wrow_a + 32 * i + r32) + 2 * h);
-        f.sb[i] = *reinterpret_cast<const uint16_t *>(lsb + 4 * (wrow_b + 32 * i + r32) + 2 * h);
-      }
+      f.sa[i] = *reinterpret_cast<const uint16_t *>(lsa + 4 * (wrow_a + 32 * i + r32) + 2 * h);
+      f.sb[i] = *reinterpret_cast<const uint16_t *>(lsb + 4 * (wrow_b + 32 * i + r32) + 2 * h);
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -520,25 +506,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
     if (step + 3 < total) issue(step + 3);
     const int ks = step % nk;
     load(step + 1, nxt);
-    if constexpr (DQ) {
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-          const int c = tt >> 1, d = 4 * c + 2 * (tt & 1);
-          const int sbyte = BS == 32 ? 2 * c + ss : 0;
-          v8bf fa[2], fb[2];
-#pragma unroll
-          for (int i = 0; i < 2; ++i) fa[i] = dequant8(cur.a[ss][i], d, e8m0_at(cur.sa[i], sbyte));
-#pragma unroll
-          for (int j = 0; j < 2; ++j) fb[j] = dequant8(cur.b[ss][j], d, e8m0_at(cur.sb[j], sbyte));
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-        }
-    } else {
+    {
 #define FMM_MFMA_SIJ(S, I, J)                                                                      \
   acc[I][J] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.a[S][I], cur.b[S][J], acc[I][J], 0, 0, \
                                                               S, cur.sa[I], S, cur.sb[J])
@@ -607,6 +575,288 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_mx_fast_kernel(GemmArgs g, i
         for (int e = 0; e < 16; ++e) v[e] = agpr_read(quad[q][i][j][e]);
         store_tile(g, bt, ro, q, pm0 + wrow_a + 32 * i, pn0 + wrow_b + 32 * j, v);
       }
+}
+
+// ---------------------------------------------------------------------------
+// Exact-dot fused sub-products on the 128 x 128 tile layout (E8M0 scales,
+// blocks 32 and 128), two waves per SIMD.
+//
+// One persistent workgroup of eight waves per CU walks a list of (tile,
+// outer term, batch) items; its (item, term, K step) sequence is a single
+// transfer pipeline, so the codes of the next item are in flight while the
+// current one ends.  Each wave owns 64 rows x 32 columns of the 128 x 128
+// tile (two 32 x 32 MFMA tiles), which leaves room for its four W-combine
+// quadrants (128 floats a lane) in the architectural registers beside the
+// accumulators: a term-end combine is one multiply-add per nonzero weight and
+// element, and while one wave converts codes or combines, the other wave on
+// its SIMD keeps the matrix core busy.
+//
+// The MFMAs take the B fragment as their first operand, so a lane holds one
+// row of P and, in each register quadruple, four consecutive columns: the
+// output is written with 16-byte stores.
+//
+// Transfers and fragments are those of gemm_mx_fast_kernel (the 128 x 128
+// tile images through a four-slot ring).  Each 64-byte substep runs as four
+// v_mfma_f32_32x32x16_bf16 per tile pair on operands converted by
+// v_cvt_scalef32_pk_bf16_fp8 with the block's E8M0 scale as the scale
+// operand (the dequantized value, exact for every scale the rules produce),
+// so the products of the dequantized operands are summed across the whole
+// contracted axis at fp32 grade.  Instruction t of substep s takes, in lane
+// half h, bytes 64 s + 32 (t >> 1) + 16 h + 8 (t & 1) .. + 7 of the row on
+// both operands, which lie in block 2 s + (t >> 1) at block 32 (record byte
+// 2 (t >> 1) + s, the record holding blocks 0, 2, 1, 3).  P_r starts from
+// zero at each term, and quadrant q of an item accumulates w[r_i][q] * P_r by
+// a fused multiply-add in ascending r_i.
+// Requires m', n', k' multiples of 128 (the layout's).
+// ---------------------------------------------------------------------------
+constexpr int kDqThreads = 512;
+
+// s_barrier after this wave's LDS reads have completed; the transfers a wave
+// waits for are tracked by wait_vmcnt, and no global store needs to drain here
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int BS>
+__global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int tiles_m, int nitems) {
+  __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+  __shared__ float lds_w[4 * kMaxRank];
+  uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
+  const uint32_t lds_base = dma::lds_addr(lds_raw);
+  const int t = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int lane = t & 63;
+  const int r32 = lane & 31, h = lane >> 5;
+  const int wrow_a = (wave >> 2) * 64, wrow_b = (wave & 3) * 32;
+  const int tiles_n = g.tiles_n, ntiles = tiles_m * tiles_n;
+  const int nk = (int)(g.kp / FBK), R = g.R, To = (int)g.To;
+  if (t < 4 * kMaxRank) lds_w[t] = g.w[t];   // read only after the first barrier
+
+  // This workgroup's items.  Workgroups are dispatched round-robin over the
+  // eight XCDs, so XCD x = blockIdx.x mod 8 is given a contiguous range of
+  // items and its P workgroups take every P-th item of it: at any time the
+  // workgroups of one XCD work on neighbouring tiles (eight tile rows by four
+  // tile columns of one term) and share their codes in its L2.
+  int it0, itstep, nmine;
+  {
+    const int nwg = gridDim.x, b = blockIdx.x;
+    if ((nwg & 7) == 0) {
+      const int P = nwg >> 3, x = b & 7, j = b >> 3;
+      const int lo = (int)((int64_t)x * nitems / 8), hi = (int)((int64_t)(x + 1) * nitems / 8);
+      it0 = lo + j;
+      itstep = P;
+      nmine = hi > it0 ? (hi - it0 + P - 1) / P : 0;
+    } else {
+      it0 = b;
+      itstep = nwg;
+      nmine = nitems > it0 ? (nitems - it0 + nwg - 1) / nwg : 0;
+    }
+  }
+  if (nmine == 0) return;                  // uniform over the workgroup
+  const int64_t total = (int64_t)nmine * R * nk;   // K steps of this workgroup
+
+  // item id -> tile (tm, tn) in groups of eight tile rows, outer term, batch
+  struct Item {
+    int tm, tn, ro, bt;
+  };
+  auto item_of_id = [&](int id) {
+    Item x;
+    const int rest = id / ntiles, tile = id - rest * ntiles;
+    x.ro = rest % To;
+    x.bt = rest / To;
+    constexpr int GM = 8;
+    const int per_group = GM * tiles_n, group = tile / per_group, first_m = group * GM;
+    const int gm = min(tiles_m - first_m, GM), in = tile - group * per_group;
+    x.tm = first_m + in % gm;
+    x.tn = in / gm;
+    return x;
+  };
+
+  // Transfers of one step: A and B code regions 2 wave, 2 wave + 1 (tile
+  // rows 8 region .. + 7); waves 0-3 also move a 256-byte quarter of the
+  // scales (A rows 0-63, 64-127, then B).  The tile indices ta, tb of the
+  // next step to transfer advance by one per step and by (tiles - 1) k'/128
+  // more at a term's end.
+  const int64_t tma = g.mp / BM, tna = g.np / BN;
+  const int64_t da = (tma - 1) * nk, db = (tna - 1) * nk;
+  int ri_i = 0, ks_i = 0, k_i = 0;
+  int64_t ta = 0, tb = 0;
+  auto start_item = [&](int k) {
+    const Item x = item_of_id(it0 + k * itstep);
+    const int64_t r0 = (int64_t)x.bt * g.T + (int64_t)x.ro * R;
+    ta = (r0 * tma + x.tm) * nk;
+    tb = (r0 * tna + x.tn) * nk;
+  };
+  const bool scale_wave = wave < 4, scale_b = wave >= 2;
+  const uint32_t lds_sc = 2 * BM * FBK + (scale_b ? BM * 4 : 0) + (wave & 1) * 256;
+  auto issue_next = [&](int64_t step) {
+    const uint8_t *xa = g.xa + ta * (BM * FBK);
+    const uint8_t *xb = g.xb + tb * (BN * FBK);
+    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int region = 2 * wave + j;
+      copy16(16u * (uint32_t)lane, xa + region * 1024, m0 + region * 1024);
+      copy16(16u * (uint32_t)lane, xb + region * 1024, m0 + BM * FBK + region * 1024);
+    }
+    if (scale_wave) {
+      const uint8_t *sbase = scale_b ? g.sb + tb * (BN * 4) : g.sa + ta * (BM * 4);
+      copy4(4u * (uint32_t)lane + (wave & 1) * 256u, sbase, m0 + lds_sc);
+    }
+    ++ta;
+    ++tb;
+    if (++ks_i == nk) {
+      ks_i = 0;
+      ta += da;
+      tb += db;
+      if (++ri_i == R) {
+        ri_i = 0;
+        if (++k_i < nmine) start_item(k_i);
+      }
+    }
+  };
+
+  // fragments of one 64-byte substep: A row tiles i = 0, 1 and the B column tile
+  struct Frag {
+    v8i a[2], b;
+  };
+  auto read_frag = [&](int64_t step, int ss, Frag &f) {
+    const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *lb = la + BM * FBK;
+    f.a[0] = frag_mx(la, wrow_a + r32, ss, h);
+    f.a[1] = frag_mx(la, wrow_a + 32 + r32, ss, h);
+    f.b = frag_mx(lb, wrow_b + r32, ss, h);
+  };
+  // the rows' whole scale records of one step (blocks 0, 2, 1, 3 at block 32)
+  auto read_scales = [&](int64_t step, int (&sa)[2], int &sb) {
+    const uint8_t *lsa = lds + (step & (kSlots - 1)) * kSlot + 2 * BM * FBK;
+    const uint8_t *lsb = lsa + BM * 4;
+    sa[0] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + r32));
+    sa[1] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + 32 + r32));
+    sb = *reinterpret_cast<const int *>(lsb + 4 * (wrow_b + r32));
+  };
+
+  v16f acc[2];
+  float quad[4][2][16];
+  acc[0] = (v16f){};
+  acc[1] = (v16f){};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) quad[q][i][e] = 0.0f;
+
+  auto mfma_sub = [&](const Frag &f, int ss, const int (&sa)[2], int sb) {
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+      const int c = tt >> 1, d = 4 * c + 2 * (tt & 1);
+      const int sbyte = BS == 32 ? 2 * c + ss : 0;
+      const v8bf fb = dequant8(f.b, d, e8m0_at(sb, sbyte));
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const v8bf fa = dequant8(f.a[i], d, e8m0_at(sa[i], sbyte));
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb, fa, acc[i], 0, 0, 0);
+      }
+    }
+  };
+
+  // output of one item: quadrant q = 2 k + i of the tile; lane (r, h) holds
+  // row r of each 32-row tile i and columns 8 a + 4 h .. + 3 in registers
+  // 4 a .. 4 a + 3
+  const int64_t ld = g.depth == 1 ? g.N : g.np;
+  const int lane_off = r32 * (int)ld + 4 * h;
+  auto store_item = [&](int k) {
+    const Item x = item_of_id(it0 + k * itstep);
+    const int64_t pm0 = (int64_t)x.tm * BM + wrow_a, pn0 = (int64_t)x.tn * BN + wrow_b;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int iq = q & 1, kq = q >> 1;
+      float *base = g.depth == 1
+                        ? g.out + x.bt * g.M * g.N + (iq * g.mp + pm0) * g.N + kq * g.np + pn0
+                        : g.out + ((((int64_t)x.bt * To + x.ro) * 4 + q) * g.mp + pm0) * g.np + pn0;
+      base += lane_off;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float4 v = make_float4(quad[q][i][4 * a], quad[q][i][4 * a + 1], quad[q][i][4 * a + 2],
+                                 quad[q][i][4 * a + 3]);
+          *reinterpret_cast<float4 *>(base + 32 * i * ld + 8 * a) = v;
+        }
+    }
+  };
+
+  // prologue: steps 0, 1, 2 in flight, step 0 waited for
+  start_item(0);
+  issue_next(0);
+  if (total > 1) issue_next(1);
+  if (total > 2) issue_next(2);
+  if (total > 2) {
+    if (scale_wave) wait_vmcnt<10>(); else wait_vmcnt<8>();
+  } else if (total > 1) {
+    if (scale_wave) wait_vmcnt<5>(); else wait_vmcnt<4>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  lds_barrier();
+
+  // compute stream: item k_c, term ri_c, step ks_c
+  int k_c = 0, ri_c = 0, ks_c = 0;
+  Frag f0, f1;
+  int sa[2], sb;
+  read_frag(0, 0, f0);
+  read_scales(0, sa, sb);
+  int sa_n[2] = {sa[0], sa[1]}, sb_n = sb;
+  for (int64_t step = 0; step < total; ++step) {
+    read_frag(step, 1, f1);
+    mfma_sub(f0, 0, sa, sb);
+    if (step + 1 < total) {
+      // step + 1 transferred (step + 2 may still be in flight) and every wave
+      // done reading step - 1's slot, which step + 3 then takes
+      if (step + 2 < total) {
+        if (scale_wave) wait_vmcnt<5>(); else wait_vmcnt<4>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      lds_barrier();
+      if (step + 3 < total) issue_next(step + 3);
+      read_frag(step + 1, 0, f0);
+      read_scales(step + 1, sa_n, sb_n);
+    }
+    mfma_sub(f1, 1, sa, sb);
+    sa[0] = sa_n[0];
+    sa[1] = sa_n[1];
+    sb = sb_n;
+    if (++ks_c == nk) {
+      ks_c = 0;
+      // end of term ri_c: quadrant q += w[ri_c][q] * P
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float wq = __builtin_bit_cast(
+            float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, lds_w[4 * ri_c + q])));
+        if (wq != 0.0f) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) quad[q][i][e] = __fmaf_rn(wq, acc[i][e], quad[q][i][e]);
+        }
+      }
+      acc[0] = (v16f){};
+      acc[1] = (v16f){};
+      if (++ri_c == R) {
+        ri_c = 0;
+        store_item(k_c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) quad[q][i][e] = 0.0f;
+        ++k_c;
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -858,14 +1108,23 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
   // the 128 x 128 tile layout: E8M0 scales at blocks 32 and 128 (fp8 path, or
   // the exact-dot path with each block's power of two folded into the codes)
   const bool aligned = pb.layout == FMM_LAYOUT_TILE128x128;
-  if (aligned && pb.exact_dot && pb.block == 32)
-    hipLaunchKernelGGL((gemm_mx_fast_kernel<32, true>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
-  else if (aligned && pb.exact_dot)
-    hipLaunchKernelGGL((gemm_mx_fast_kernel<128, true>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
-  else if (aligned && pb.block == 32)
-    hipLaunchKernelGGL((gemm_mx_fast_kernel<32, false>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+  if (aligned && pb.exact_dot) {
+    // one persistent workgroup per CU (its LDS ring and registers fill one)
+    const int64_t items = tiles_m * tiles_n * pb.To * pb.batch;
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+      ncu = 256;
+    if (items > INT32_MAX) return hipErrorInvalidValue;
+    const dim3 pgrid((unsigned)(items < ncu ? items : ncu));
+    if (pb.block == 32)
+      hipLaunchKernelGGL(gemm_dq8_kernel<32>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
+    else
+      hipLaunchKernelGGL(gemm_dq8_kernel<128>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
+  } else if (aligned && pb.block == 32)
+    hipLaunchKernelGGL(gemm_mx_fast_kernel<32>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
   else if (aligned)
-    hipLaunchKernelGGL((gemm_mx_fast_kernel<128, false>), grid, dim3(kThreads), 0, st, g, (int)tiles_m);
+    hipLaunchKernelGGL(gemm_mx_fast_kernel<128>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
   else if (mx)
     hipLaunchKernelGGL(gemm_mx_kernel, grid, dim3(kThreads), 0, st, g);
   else
