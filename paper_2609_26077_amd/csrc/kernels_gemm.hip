@@ -31,6 +31,8 @@
 // column l % 32, row 8 (j / 4) + 4 (l / 32) + j % 4.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 #include "lds_dma.h"
@@ -716,24 +718,47 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
     }
   };
 
-  // fragments of one 64-byte substep: A row tiles i = 0, 1 and the B column tile
+  // fragments of one 64-byte substep: A row tiles i = 0, 1 and the B column
+  // tile.  The rows a lane reads (wrow_a + r32, + 32, wrow_b + r32) agree
+  // mod 16, so they share the swizzle: chunk 2 k + h (k = 0 .. 3; substep s
+  // uses k = 2 s, 2 s + 1) of each sits at one lane offset per k, and the
+  // second A tile 4096 bytes further.
   struct Frag {
     v8i a[2], b;
   };
-  auto read_frag = [&](int64_t step, int ss, Frag &f) {
-    const uint8_t *la = lds + (step & (kSlots - 1)) * kSlot;
-    const uint8_t *lb = la + BM * FBK;
-    f.a[0] = frag_mx(la, wrow_a + r32, ss, h);
-    f.a[1] = frag_mx(la, wrow_a + 32 + r32, ss, h);
-    f.b = frag_mx(lb, wrow_b + r32, ss, h);
+  uint32_t la_k[4], lb_k[4];
+  {
+    const uint32_t x = (uint32_t)((r32 & 7) ^ ((r32 >> 3) & 1));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t ch = 16u * (((uint32_t)(2 * k + h)) ^ x);
+      la_k[k] = (uint32_t)(wrow_a + r32) * BK + ch;
+      lb_k[k] = (uint32_t)(BM * FBK) + (uint32_t)(wrow_b + r32) * BK + ch;
+    }
+  }
+  auto read_frag = [&](int64_t step, auto ssc, Frag &f) {
+    constexpr int SS = decltype(ssc)::value;
+    const uint8_t *slot = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *pa0 = slot + la_k[2 * SS], *pa1 = slot + la_k[2 * SS + 1];
+    const uint8_t *pb0 = slot + lb_k[2 * SS], *pb1 = slot + lb_k[2 * SS + 1];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint4 lo = *reinterpret_cast<const uint4 *>(pa0 + i * 32 * BK);
+      const uint4 hi = *reinterpret_cast<const uint4 *>(pa1 + i * 32 * BK);
+      f.a[i] = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+    }
+    const uint4 lo = *reinterpret_cast<const uint4 *>(pb0);
+    const uint4 hi = *reinterpret_cast<const uint4 *>(pb1);
+    f.b = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
   };
   // the rows' whole scale records of one step (blocks 0, 2, 1, 3 at block 32)
+  const uint32_t lsa_off = 2 * BM * FBK + 4 * (uint32_t)(wrow_a + r32);
+  const uint32_t lsb_off = 2 * BM * FBK + BM * 4 + 4 * (uint32_t)(wrow_b + r32);
   auto read_scales = [&](int64_t step, int (&sa)[2], int &sb) {
-    const uint8_t *lsa = lds + (step & (kSlots - 1)) * kSlot + 2 * BM * FBK;
-    const uint8_t *lsb = lsa + BM * 4;
-    sa[0] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + r32));
-    sa[1] = *reinterpret_cast<const int *>(lsa + 4 * (wrow_a + 32 + r32));
-    sb = *reinterpret_cast<const int *>(lsb + 4 * (wrow_b + r32));
+    const uint8_t *slot = lds + (step & (kSlots - 1)) * kSlot;
+    sa[0] = *reinterpret_cast<const int *>(slot + lsa_off);
+    sa[1] = *reinterpret_cast<const int *>(slot + lsa_off + 128);
+    sb = *reinterpret_cast<const int *>(slot + lsb_off);
   };
 
   v16f acc[2];
@@ -747,11 +772,13 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
 #pragma unroll
       for (int e = 0; e < 16; ++e) quad[q][i][e] = 0.0f;
 
-  auto mfma_sub = [&](const Frag &f, int ss, const int (&sa)[2], int sb) {
+  // the MFMAs of substep SS (the B fragment as the first operand)
+  auto mfma_sub = [&](auto ssc, const Frag &f, const int (&sa)[2], int sb) {
+    constexpr int SS = decltype(ssc)::value;
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
       const int c = tt >> 1, d = 4 * c + 2 * (tt & 1);
-      const int sbyte = BS == 32 ? 2 * c + ss : 0;
+      const int sbyte = BS == 32 ? 2 * c + SS : 0;
       const v8bf fb = dequant8(f.b, d, e8m0_at(sb, sbyte));
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -805,12 +832,12 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
   int k_c = 0, ri_c = 0, ks_c = 0;
   Frag f0, f1;
   int sa[2], sb;
-  read_frag(0, 0, f0);
+  read_frag(0, std::integral_constant<int, 0>(), f0);
   read_scales(0, sa, sb);
   int sa_n[2] = {sa[0], sa[1]}, sb_n = sb;
   for (int64_t step = 0; step < total; ++step) {
-    read_frag(step, 1, f1);
-    mfma_sub(f0, 0, sa, sb);
+    read_frag(step, std::integral_constant<int, 1>(), f1);
+    mfma_sub(std::integral_constant<int, 0>(), f0, sa, sb);
     if (step + 1 < total) {
       // step + 1 transferred (step + 2 may still be in flight) and every wave
       // done reading step - 1's slot, which step + 3 then takes
@@ -821,10 +848,10 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
       }
       lds_barrier();
       if (step + 3 < total) issue_next(step + 3);
-      read_frag(step + 1, 0, f0);
+      read_frag(step + 1, std::integral_constant<int, 0>(), f0);
       read_scales(step + 1, sa_n, sb_n);
     }
-    mfma_sub(f1, 1, sa, sb);
+    mfma_sub(std::integral_constant<int, 1>(), f1, sa, sb);
     sa[0] = sa_n[0];
     sa[1] = sa_n[1];
     sb = sb_n;
