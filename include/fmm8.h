@@ -144,19 +144,21 @@ enum {
    * byte 4 (32 h + j) + i; fp32 scales (FMM_RULE_FP32_AMAX) are in row order.
    * Used by plans whose sub-products run on 256-row tiles: depth 1 or 2,
    * M / 2^l and N / 2^l multiples of 256, K / 2^l a multiple of 64 (of 128
-   * at block 128), and either the exact-dot path (fp32 scales, block 16, or
-   * FMM_FLAG_EXACT_DOT) or E8M0 scales at block 32 or 128 on the fp8 matrix
-   * cores with K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE; and every plan of a
+   * at block 128), and either fp32 scales (the exact-dot path) or E8M0
+   * scales with K / 2^l >= 1024 or FMM_FLAG_LARGE_TILE (the fp8 matrix cores
+   * at blocks 32 and 128, the exact-dot path at block 16 or with
+   * FMM_FLAG_EXACT_DOT); and every plan of a
    * realization of another shape (rows M / m and N / n, kdim K / k).  The B
    * side is read as 128-row halves of these tiles. */
   FMM_LAYOUT_TILE256x64 = 1,
   /* codes [batch][terms][rows / 128][kdim / 128][128][128]: 128-row x 128-byte
    * tiles, each contiguous; inside a tile, 16-byte chunk c of tile row t sits
    * at chunk c ^ (t & 7) ^ ((t >> 3) & 1) of that row.
-   * scales [batch][terms][rows / 128][kdim / 128][128][4]: for each tile row
-   * and 128-byte step, 4 E8M0 bytes: at block 32 the step's blocks 0, 2, 1, 3
-   * in that order, at block 128 the step's one block repeated 4 times.
-   * Used by the other plans with E8M0 scales at block 32 or 128 whose
+   * scales [batch][terms][rows / 128][kdim / 128][128][4 or 8]: for each tile
+   * row and 128-byte step, 4 E8M0 bytes: at block 32 the step's blocks 0, 2,
+   * 1, 3 in that order, at block 128 the step's one block repeated 4 times;
+   * at block 16, 8 bytes: the step's blocks 0, 2, 4, 6, then 1, 3, 5, 7.
+   * Used by the other plans with E8M0 scales (blocks 16, 32 and 128) whose
    * M / 2^l and N / 2^l are multiples of 128 and K / 2^l a multiple of 128. */
   FMM_LAYOUT_TILE128x128 = 2
 };

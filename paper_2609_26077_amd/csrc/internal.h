@@ -100,7 +100,7 @@ inline bool exact_split(const Problem &pb) { return pb.exact_dot || pb.scale_byt
 
 // Bytes of one (batch, term) plane of scales for `rows` rows.
 inline int64_t scale_plane_bytes(const Problem &pb, int64_t rows) {
-  if (pb.layout == FMM_LAYOUT_TILE128x128) return rows * (pb.kp / 128) * 4;
+  if (pb.layout == FMM_LAYOUT_TILE128x128) return rows * (pb.kp / 128) * (pb.block == 16 ? 8 : 4);
   return rows * pb.kblocks * pb.scale_bytes;
 }
 

@@ -59,9 +59,14 @@ __device__ __forceinline__ double decoded(const Problem &pb, const uint8_t *code
     const int64_t t = row & 127, c = (l & 127) >> 4;
     const int64_t tile = (plane * (rows / 128) + row / 128) * (pb.kp / 128) + l / 128;
     code = codes[(tile * 128 + t) * 128 + 16 * (c ^ (t & 7) ^ ((t >> 3) & 1)) + (l & 15)];
-    const int64_t kk = (l & 127) >> 5;                       // block of 32 within the step
-    const int64_t byte = pb.block == 32 ? (((kk & 1) << 1) | (kk >> 1)) : 0;   // record: blocks 0, 2, 1, 3
-    s = ldexp(1.0, (int)scales[(tile * 128 + t) * 4 + byte] - 127);
+    if (pb.block == 16) {
+      const int64_t b = (l & 127) >> 4;                      // record: blocks 0, 2, 4, 6, 1, 3, 5, 7
+      s = ldexp(1.0, (int)scales[(tile * 128 + t) * 8 + 4 * (b & 1) + (b >> 1)] - 127);
+    } else {
+      const int64_t kk = (l & 127) >> 5;                     // block of 32 within the step
+      const int64_t byte = pb.block == 32 ? (((kk & 1) << 1) | (kk >> 1)) : 0;   // record: blocks 0, 2, 1, 3
+      s = ldexp(1.0, (int)scales[(tile * 128 + t) * 4 + byte] - 127);
+    }
   } else {
     code = codes[(plane * rows + row) * pb.kp + l];
     const int64_t si = (plane * rows + row) * pb.kblocks + kb;

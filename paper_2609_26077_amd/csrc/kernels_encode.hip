@@ -200,7 +200,8 @@ __device__ __forceinline__ void stage_tile(float *lds, const float *__restrict__
 //   128 x 128 tiles: codes as the 128-row x 128-byte tile image (chunk c of
 //           tile row t at c ^ (t & 7) ^ ((t >> 3) & 1)); scales 4 bytes per
 //           tile row and 128-byte step (blocks 0, 2, 1, 3 at block 32; the
-//           one block repeated at block 128)
+//           one block repeated at block 128), 8 at block 16 (blocks 0, 2, 4,
+//           6, then 1, 3, 5, 7)
 // `lead`: this run starts its block (its lane stores the block's scale).
 struct Out {
   int64_t code, scale;
@@ -219,8 +220,13 @@ __device__ __forceinline__ Out out_of(const Problem &pb, int64_t rows, int64_t p
   } else if (pb.layout == FMM_LAYOUT_TILE128x128) {
     const int64_t t = p & 127, c = (l >> 4) & 7, tile = (p >> 7) * (kp >> 7) + (l >> 7);
     o.code = (tile << 14) + t * 128 + 16 * (c ^ (t & 7) ^ ((t >> 3) & 1)) + (l & 15);
-    const int64_t kq = (l >> 5) & 3;                       // block of the step (block 32)
-    o.scale = tile * 512 + t * 4 + (pb.block == 32 ? ((kq & 1) << 1) | (kq >> 1) : 0);
+    if (pb.block == 16) {
+      const int64_t b = (l >> 4) & 7;                      // block of the step
+      o.scale = tile * 1024 + t * 8 + 4 * (b & 1) + (b >> 1);
+    } else {
+      const int64_t kq = (l >> 5) & 3;                     // block of the step (block 32)
+      o.scale = tile * 512 + t * 4 + (pb.block == 32 ? ((kq & 1) << 1) | (kq >> 1) : 0);
+    }
   } else {
     o.code = p * kp + l;
     o.scale = p * pb.kblocks + kb;
@@ -228,9 +234,11 @@ __device__ __forceinline__ Out out_of(const Problem &pb, int64_t rows, int64_t p
   return o;
 }
 
-// elements of scales per (batch, term) plane (the 128 x 128 layout keeps 4 bytes per row and step)
+// elements of scales per (batch, term) plane (the 128 x 128 layout keeps 4
+// bytes per row and step, 8 at block 16)
 __device__ __forceinline__ int64_t scale_plane_of(const Problem &pb, int64_t rows) {
-  return pb.layout == FMM_LAYOUT_TILE128x128 ? rows * (pb.kp / 128) * 4 : rows * pb.kblocks;
+  return pb.layout == FMM_LAYOUT_TILE128x128 ? rows * (pb.kp / 128) * (pb.block == 16 ? 8 : 4)
+                                              : rows * pb.kblocks;
 }
 
 __device__ __forceinline__ void store_scale(const Problem &pb, uint8_t *scales, int64_t at, uint32_t stored) {

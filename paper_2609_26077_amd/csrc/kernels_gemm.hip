@@ -621,7 +621,10 @@ __device__ __forceinline__ void lds_barrier() {
 
 template <int BS>
 __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int tiles_m, int nitems) {
-  __shared__ uint4 lds_raw[kSlots * kSlot / 16];
+  // scale record per row and step: 4 bytes (blocks 32, 128) or 8 (block 16)
+  constexpr int REC = BS == 16 ? 8 : 4;
+  constexpr int SLOT = 2 * BM * FBK + 2 * BM * REC;
+  __shared__ uint4 lds_raw[kSlots * SLOT / 16];
   __shared__ float lds_w[4 * kMaxRank];
   uint8_t *lds = reinterpret_cast<uint8_t *>(lds_raw);
   const uint32_t lds_base = dma::lds_addr(lds_raw);
@@ -675,10 +678,11 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
   };
 
   // Transfers of one step: A and B code regions 2 wave, 2 wave + 1 (tile
-  // rows 8 region .. + 7); waves 0-3 also move a 256-byte quarter of the
-  // scales (A rows 0-63, 64-127, then B).  The tile indices ta, tb of the
-  // next step to transfer advance by one per step and by (tiles - 1) k'/128
-  // more at a term's end.
+  // rows 8 region .. + 7), and 256-byte pieces of the scales (A then B: four
+  // pieces at block 16, moved by all eight waves; two at blocks 32 and 128,
+  // moved by waves 0-3).  The tile indices ta, tb of the next step to
+  // transfer advance by one per step and by (tiles - 1) k'/128 more at a
+  // term's end.
   const int64_t tma = g.mp / BM, tna = g.np / BN;
   const int64_t da = (tma - 1) * nk, db = (tna - 1) * nk;
   int ri_i = 0, ks_i = 0, k_i = 0;
@@ -689,12 +693,14 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
     ta = (r0 * tma + x.tm) * nk;
     tb = (r0 * tna + x.tn) * nk;
   };
-  const bool scale_wave = wave < 4, scale_b = wave >= 2;
-  const uint32_t lds_sc = 2 * BM * FBK + (scale_b ? BM * 4 : 0) + (wave & 1) * 256;
+  constexpr int SPIECES = BM * REC / 256;                  // 256-byte pieces per side
+  const bool scale_wave = wave < 2 * SPIECES, scale_b = wave >= SPIECES;
+  const uint32_t piece = 256u * (uint32_t)(wave % SPIECES);
+  const uint32_t lds_sc = 2 * BM * FBK + (scale_b ? BM * REC : 0) + piece;
   auto issue_next = [&](int64_t step) {
     const uint8_t *xa = g.xa + ta * (BM * FBK);
     const uint8_t *xb = g.xb + tb * (BN * FBK);
-    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * kSlot;
+    const uint32_t m0 = lds_base + (uint32_t)(step & (kSlots - 1)) * SLOT;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int region = 2 * wave + j;
@@ -702,8 +708,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
       copy16(16u * (uint32_t)lane, xb + region * 1024, m0 + BM * FBK + region * 1024);
     }
     if (scale_wave) {
-      const uint8_t *sbase = scale_b ? g.sb + tb * (BN * 4) : g.sa + ta * (BM * 4);
-      copy4(4u * (uint32_t)lane + (wave & 1) * 256u, sbase, m0 + lds_sc);
+      const uint8_t *sbase = scale_b ? g.sb + tb * (BN * REC) : g.sa + ta * (BM * REC);
+      copy4(4u * (uint32_t)lane + piece, sbase, m0 + lds_sc);
     }
     ++ta;
     ++tb;
@@ -738,7 +744,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
   }
   auto read_frag = [&](int64_t step, auto ssc, Frag &f) {
     constexpr int SS = decltype(ssc)::value;
-    const uint8_t *slot = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *slot = lds + (step & (kSlots - 1)) * SLOT;
     const uint8_t *pa0 = slot + la_k[2 * SS], *pa1 = slot + la_k[2 * SS + 1];
     const uint8_t *pb0 = slot + lb_k[2 * SS], *pb1 = slot + lb_k[2 * SS + 1];
 #pragma unroll
@@ -751,13 +757,16 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
     const uint4 hi = *reinterpret_cast<const uint4 *>(pb1);
     f.b = (v8i){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
   };
-  // the rows' whole scale records of one step (blocks 0, 2, 1, 3 at block 32)
-  const uint32_t lsa_off = 2 * BM * FBK + 4 * (uint32_t)(wrow_a + r32);
-  const uint32_t lsb_off = 2 * BM * FBK + BM * 4 + 4 * (uint32_t)(wrow_b + r32);
+  // scales of one step: at blocks 32 and 128 the rows' whole records
+  // (blocks 0, 2, 1, 3 at block 32); at block 16 the word of the lane half,
+  // h = 0: blocks 0, 2, 4, 6, h = 1: blocks 1, 3, 5, 7 (instruction t of
+  // substep s reads block 4 s + 2 (t >> 1) + h)
+  const uint32_t lsa_off = 2 * BM * FBK + REC * (uint32_t)(wrow_a + r32) + (BS == 16 ? 4 * h : 0);
+  const uint32_t lsb_off = 2 * BM * FBK + BM * REC + REC * (uint32_t)(wrow_b + r32) + (BS == 16 ? 4 * h : 0);
   auto read_scales = [&](int64_t step, int (&sa)[2], int &sb) {
-    const uint8_t *slot = lds + (step & (kSlots - 1)) * kSlot;
+    const uint8_t *slot = lds + (step & (kSlots - 1)) * SLOT;
     sa[0] = *reinterpret_cast<const int *>(slot + lsa_off);
-    sa[1] = *reinterpret_cast<const int *>(slot + lsa_off + 128);
+    sa[1] = *reinterpret_cast<const int *>(slot + lsa_off + 32 * REC);
     sb = *reinterpret_cast<const int *>(slot + lsb_off);
   };
 
@@ -778,7 +787,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
       const int c = tt >> 1, d = 4 * c + 2 * (tt & 1);
-      const int sbyte = BS == 32 ? 2 * c + SS : 0;
+      const int sbyte = BS == 16 ? 2 * SS + c : BS == 32 ? 2 * c + SS : 0;
       const v8bf fb = dequant8(f.b, d, e8m0_at(sb, sbyte));
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -1135,7 +1144,7 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
   // the 128 x 128 tile layout: E8M0 scales at blocks 32 and 128 (fp8 path, or
   // the exact-dot path with each block's power of two folded into the codes)
   const bool aligned = pb.layout == FMM_LAYOUT_TILE128x128;
-  if (aligned && pb.exact_dot) {
+  if (aligned && (pb.exact_dot || pb.block == 16)) {
     // one persistent workgroup per CU (its LDS ring and registers fill one)
     const int64_t items = tiles_m * tiles_n * pb.To * pb.batch;
     int dev = 0, ncu = 0;
@@ -1144,7 +1153,9 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
       ncu = 256;
     if (items > INT32_MAX) return hipErrorInvalidValue;
     const dim3 pgrid((unsigned)(items < ncu ? items : ncu));
-    if (pb.block == 32)
+    if (pb.block == 16)
+      hipLaunchKernelGGL(gemm_dq8_kernel<16>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
+    else if (pb.block == 32)
       hipLaunchKernelGGL(gemm_dq8_kernel<32>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
     else
       hipLaunchKernelGGL(gemm_dq8_kernel<128>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);

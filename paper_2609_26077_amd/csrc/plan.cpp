@@ -101,8 +101,8 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   // against the fused path's none: plans with a fused kernel take it by
   // default where that round trip costs less than the fused path's smaller
   // tiles, k' >= 1024 (measured on both forms: the large tiles win at 1024
-  // and above, lose at 512 and below); fp32 scales and block 16 whenever the
-  // shape allows (their fused promote kernel is slower at every measured k').
+  // and above, lose at 512 and below); fp32 scales whenever the shape allows
+  // (their fused promote kernel is slower at every measured k').
   // Plans of other shapes take it always (their W-combine fans each P_r out
   // to up to m n blocks of C), K = 0 included (C is then zero).
   const int64_t mp = q.M / gm, kp = q.K / gk, np = q.N / gn;
@@ -127,15 +127,16 @@ int fmm_plan_create(const fmm_real *d, const fmm_plan_desc *desc, fmm_plan **out
   pb.exact_dot = (q.flags & FMM_FLAG_EXACT_DOT) ? 1 : 0;
   pb.b_rows = (q.flags & FMM_FLAG_B_BLOCK128) ? 128 : 1;
   pb.b_bf16 = (q.flags & FMM_FLAG_B_BF16) ? 1 : 0;
-  // E8M0 scales at blocks 32 and 128 have a fused 128 x 128 kernel on either
-  // path (the fp8 matrix cores, or the exact-dot flag's folded-scale form);
-  // fp32 scales and block 16 only the large-tile exact-dot kernels
-  const bool fused_exists = pb.scale_bytes == 1 && (q.block == 32 || q.block == 128);
+  // E8M0 scales have a fused 128 x 128 kernel: at blocks 32 and 128 on either
+  // path (the fp8 matrix cores, or the exact-dot flag's folded-scale form),
+  // at block 16 the folded-scale form (block 16 always runs exact-dot); fp32
+  // scales only the large-tile exact-dot kernels
+  const bool fused_exists = pb.scale_bytes == 1 && (q.block == 16 || q.block == 32 || q.block == 128);
   pb.split = shaped || (split_shape &&
              (!fused_exists || pb.kp >= fmm::kSplitMinK || (q.flags & FMM_FLAG_LARGE_TILE)));
   // fused 128 x 128 path: E8M0 scales at blocks 32 and 128 (the fp8 matrix
-  // cores, or the exact-dot flag's folded-scale bf16 form), whole 128-row
-  // tiles and 128-byte K steps
+  // cores, or the exact-dot flag's folded-scale bf16 form) and block 16 (the
+  // folded-scale form), whole 128-row tiles and 128-byte K steps
   const bool tile128 = fused_exists && pb.mp % 128 == 0 && pb.np % 128 == 0 && pb.kp > 0 &&
                        pb.kp % 128 == 0 && pb.kp < (int64_t(1) << 26);
   pb.layout = pb.split ? FMM_LAYOUT_TILE256x64 : tile128 ? FMM_LAYOUT_TILE128x128 : FMM_LAYOUT_ROWS;

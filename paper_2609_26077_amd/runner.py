@@ -140,7 +140,7 @@ class FMM:
                     scales = _unpermute_scales256(self.ws[s0:s0 + ns], v.batch, v.terms, v.rows, v.kblocks)
             elif v.code_layout == FMM_LAYOUT_TILE128x128:
                 codes = _untile128x128(raw, v.batch, v.terms, v.rows, v.kdim)
-                nrec = v.batch * v.terms * v.rows * (v.kdim // 128) * 4
+                nrec = v.batch * v.terms * v.rows * (v.kdim // 128) * (8 if v.kblocks == v.kdim // 16 else 4)
                 scales = _unpack_scales128(self.ws[s0:s0 + nrec], v.batch, v.terms, v.rows, v.kdim,
                                            v.kblocks)
             else:
@@ -174,11 +174,15 @@ def _untile128x128(raw, batch, terms, rows, kdim):
 
 def _unpack_scales128(raw, batch, terms, rows, kdim, kblocks):
     """[batch][terms][rows][kblocks] copy of E8M0 scales in FMM_LAYOUT_TILE128x128."""
-    t = raw.view(batch, terms, rows // 128, kdim // 128, 128, 4)
-    if kblocks == kdim // 32:                  # block 32: record order is blocks 0, 2, 1, 3
-        t = t[..., torch.tensor([0, 2, 1, 3], device=raw.device)]
-    else:                                      # block 128: the byte repeated
-        t = t[..., :1]
+    if kblocks == kdim // 16:                  # block 16: record order is blocks 0, 2, 4, 6, 1, 3, 5, 7
+        t = raw.view(batch, terms, rows // 128, kdim // 128, 128, 8)
+        t = t[..., torch.tensor([0, 4, 1, 5, 2, 6, 3, 7], device=raw.device)]
+    else:
+        t = raw.view(batch, terms, rows // 128, kdim // 128, 128, 4)
+        if kblocks == kdim // 32:              # block 32: record order is blocks 0, 2, 1, 3
+            t = t[..., torch.tensor([0, 2, 1, 3], device=raw.device)]
+        else:                                  # block 128: the byte repeated
+            t = t[..., :1]
     return t.permute(0, 1, 2, 4, 3, 5).reshape(batch, terms, rows, kblocks)
 
 

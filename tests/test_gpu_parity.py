@@ -438,12 +438,25 @@ def test_dq_basis_changes():
     ("cubic8", "gaussian", 1, 1536, 2048, 1536, 2, 128, 1),    # depth 2, 64 terms, block 128
     ("tstar", "rowscaled", 1, 1024, 2048, 1024, 3, 32, 1),     # depth 3, 343 terms
     ("winograd", "student_t3", 16, 256, 256, 256, 1, 32, 1),   # a batch of small products
+    ("strassen", "student_t3", 2, 512, 1024, 768, 1, 16, 1),   # block 16: 8-byte records, 2 x 3 tiles, batch
+    ("tstar", "rowscaled", 1, 256, 256, 256, 1, 16, 2),        # block 16, OCP, one tile, one k-step
+    ("cubic8", "gaussian", 1, 1024, 1024, 512, 2, 16, 1),      # block 16, depth 2, 64 terms
+    ("tstar", "rowscaled", 1, 1024, 2048, 1024, 3, 16, 1),     # block 16, depth 3
 ])
 def test_dq_fused_path(case):
     """The fused 128 x 128 kernel in its exact-dot form (each block's power
     of two folded into the codes' conversion to bf16; W-combine quadrants in
-    registers): codes and scales bit-exact, C within 1e-5 |C|_F, relMSE."""
+    registers) at blocks 16, 32 and 128: codes and scales bit-exact, C within
+    1e-5 |C|_F, relMSE."""
     spec, fam, b, M, K, N, depth, bs, rule = case
     r = check_case(spec, fam, b, M, K, N, depth, bs, rule, seed=41, cfg=12, exact=True,
                    layout=FMM_LAYOUT_TILE128x128)
     print(case, r, flush=True)
+
+
+def test_block16_takes_the_fused_path():
+    """E8M0 scales at block 16 without the exact-dot flag (block 16 always
+    runs exact-dot) take the fused 128 x 128 path below k' = 1024."""
+    r = check_case("winograd", "student_t3", 8, 256, 512, 256, 1, 16, 1, seed=42, cfg=12,
+                   layout=FMM_LAYOUT_TILE128x128)
+    print(r, flush=True)

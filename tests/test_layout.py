@@ -95,10 +95,11 @@ def test_untile128_inverts_the_documented_layout():
 def test_unpack_scales128_inverts_the_documented_layout():
     rng = np.random.default_rng(3)
     b, T, rows, kdim = 2, 2, 256, 384
-    for block in (32, 128):
+    for block in (16, 32, 128):
         kb = kdim // block
+        rec = 8 if block == 16 else 4
         scales = rng.integers(0, 256, size=(b, T, rows, kb), dtype=np.uint8)
-        raw = np.empty(b * T * rows * (kdim // 128) * 4, dtype=np.uint8)
+        raw = np.empty(b * T * rows * (kdim // 128) * rec, dtype=np.uint8)
         pos = 0
         for bi in range(b):
             for r in range(T):
@@ -106,11 +107,13 @@ def test_unpack_scales128_inverts_the_documented_layout():
                     for ks in range(kdim // 128):
                         for t in range(128):
                             p = 128 * tile + t
-                            if block == 32:
-                                rec = [scales[bi, r, p, 4 * ks + q] for q in (0, 2, 1, 3)]
+                            if block == 16:
+                                record = [scales[bi, r, p, 8 * ks + q] for q in (0, 2, 4, 6, 1, 3, 5, 7)]
+                            elif block == 32:
+                                record = [scales[bi, r, p, 4 * ks + q] for q in (0, 2, 1, 3)]
                             else:
-                                rec = [scales[bi, r, p, ks]] * 4
-                            raw[pos:pos + 4] = rec
-                            pos += 4
+                                record = [scales[bi, r, p, ks]] * 4
+                            raw[pos:pos + rec] = record
+                            pos += rec
         back = _unpack_scales128(torch.from_numpy(raw), b, T, rows, kdim, kb).numpy()
         assert np.array_equal(back, scales), block
