@@ -5,8 +5,10 @@
 // (one flattened (term, k-step) pipeline), and after each term adds
 // w[r_i][q] * P_r into four quadrant accumulators q = 2k + i held in
 // registers.  At depth 1 the quadrants are the four blocks of C and are
-// written once; at depth >= 2 they are the inner-level partial products,
-// combined over r_o by outer_combine_kernel.
+// written once; at depth >= 2 they are the inner-level partial products
+// Q[r_o][q], stored [batch][m'][T_o][4][n'] (the T_o 4 partials of one row
+// adjacent, so that the outer combine streams one region of HBM), combined
+// over r_o by outer_combine_kernel.
 //
 // MX path (power-of-two scales, block 32 or 128): v_mfma_scale_f32_32x32x64_f8f6f4
 // applies the E8M0 block scales in hardware.  Operand layout of that
@@ -164,7 +166,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs &g, int64_t bt, int64_
       if (g.depth == 1) {
         g.out[bt * g.M * g.N + (iq * g.mp + row) * g.N + kq * g.np + col] = v[j];
       } else {
-        g.out[(((bt * g.To + ro) * 4 + q) * g.mp + row) * g.np + col] = v[j];
+        g.out[(((bt * g.mp + row) * g.To + ro) * 4 + q) * g.np + col] = v[j];
       }
     }
   }
@@ -800,8 +802,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
   // output of one item: quadrant q = 2 k + i of the tile; lane (r, h) holds
   // row r of each 32-row tile i and columns 8 a + 4 h .. + 3 in registers
   // 4 a .. 4 a + 3
-  const int64_t ld = g.depth == 1 ? g.N : g.np;
-  const int lane_off = r32 * (int)ld + 4 * h;
+  const int64_t ld = g.depth == 1 ? g.N : (int64_t)To * 4 * g.np;   // one row of C, or of the partials
+  const int64_t lane_off = (int64_t)r32 * ld + 4 * h;
   auto store_item = [&](int k) {
     const Item x = item_of_id(it0 + k * itstep);
     const int64_t pm0 = (int64_t)x.tm * BM + wrow_a, pn0 = (int64_t)x.tn * BN + wrow_b;
@@ -810,7 +812,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
       const int iq = q & 1, kq = q >> 1;
       float *base = g.depth == 1
                         ? g.out + x.bt * g.M * g.N + (iq * g.mp + pm0) * g.N + kq * g.np + pn0
-                        : g.out + ((((int64_t)x.bt * To + x.ro) * 4 + q) * g.mp + pm0) * g.np + pn0;
+                        : g.out + ((((int64_t)x.bt * g.mp + pm0) * To + x.ro) * 4 + q) * g.np + pn0;
       base += lane_off;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -1053,7 +1055,7 @@ __global__ __launch_bounds__(256) void outer_combine_kernel(const float *__restr
 #pragma unroll
   for (int o = 0; o < NO; ++o) acc[o] = 0.f;
   for (int64_t ro = 0; ro < pb.To; ++ro) {
-    const float v = Q[(((bt * pb.To + ro) * 4 + iq) * pb.mp + p) * pb.np + q];
+    const float v = Q[(((bt * pb.mp + p) * pb.To + ro) * 4 + iq) * pb.np + q];
 #pragma unroll
     for (int o = 0; o < NO; ++o) acc[o] = __fmaf_rn(wo[ro * NO + o], v, acc[o]);
   }
@@ -1082,8 +1084,8 @@ __global__ __launch_bounds__(256) void outer_combine4_kernel(const float *__rest
   const int64_t bt = blockIdx.z;
   if (pos >= pb.mp * n4) return;
   const int64_t p = pos / n4, q4 = pos - p * n4;
-  const int64_t plane = 4 * pb.mp * pb.np;                             // floats per outer term
-  const float *src = Q + ((bt * pb.To * 4 + iq) * pb.mp + p) * pb.np + 4 * q4;
+  const int64_t plane = 4 * pb.np;                                     // outer term r_o at src + r_o plane
+  const float *src = Q + ((bt * pb.mp + p) * pb.To * 4 + iq) * pb.np + 4 * q4;
   f4v acc[NO];
 #pragma unroll
   for (int o = 0; o < NO; ++o) acc[o] = (f4v){0.f, 0.f, 0.f, 0.f};

@@ -23,6 +23,12 @@
 //      W-combine of the 128 x 128 path); combine2_kernel the same over the
 //      T = R^2 flattened terms and 16 blocks of depth 2.
 //
+// P is stored [batch][m'][T][n']: the T terms of one output row sit in
+// consecutive n'-float rows, so the W-combine, which reads all T values of a
+// position, streams one region of HBM instead of T planes far apart (a probe
+// of the depth-2 pattern, 49 terms into 16 outputs: 5.1 TB/s from planes,
+// 5.9-6.1 TB/s with the terms interleaved in 4-64 KB pieces).
+//
 // Scales of these plans are stored K-block-major by the encoder: for each
 // (term, K block) the E8M0 bytes of all rows, permuted inside every 256-row
 // tile so that row 128 wm + 32 i + r sits at byte 4 (32 wm + r) + i.  One
@@ -72,7 +78,7 @@ constexpr int kCodeB = TN * SK;       // 8 KB of B codes per step
 struct SplitArgs {
   const uint8_t *xa, *xb;      // codes [batch][T][rows / 256][kp / 64][256 x 64 tile image]
   const uint8_t *sat, *sbt;    // scales [batch][T][kblocks][rows] (rows permuted per 256-row tile)
-  float *P;                    // products [batch][T][mp][np]
+  float *P;                    // products [batch][mp][T][np]: the T terms of a row adjacent
   int64_t mp, np, kp, kblocks, T;
   int tiles_m, tiles_n;        // mp / 256, np / 128
 };
@@ -224,7 +230,8 @@ __global__ __launch_bounds__(big::kThreadsB, 1) void gemm_tile256x256_kernel(Spl
   // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32.
   // The stores are nontemporal: P_r is read once, by the W-combine, and
   // caching it only displaces the codes the other workgroups still read.
-  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 128) * g.np + pn0 + wn * 64 + r32;
+  const int64_t pstride = g.T * g.np;                     // one row of P: all T terms
+  float *out = g.P + ((bt * g.mp + pm0 + wm * 128) * g.T + r) * g.np + pn0 + wn * 64 + r32;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -232,7 +239,7 @@ __global__ __launch_bounds__(big::kThreadsB, 1) void gemm_tile256x256_kernel(Spl
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * pstride + 32 * j);
       }
 }
 
@@ -398,7 +405,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_dq256x128_kernel(SplitArgs g
     step_mfma(step);
   }
 
-  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 128) * g.np + pn0 + wn * 64 + r32;
+  const int64_t pstride = g.T * g.np;                     // one row of P: all T terms
+  float *out = g.P + ((bt * g.mp + pm0 + wm * 128) * g.T + r) * g.np + pn0 + wn * 64 + r32;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -406,7 +414,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_dq256x128_kernel(SplitArgs g
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * pstride + 32 * j);
       }
 }
 
@@ -654,7 +662,8 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
   }
 
   // P_r tile: lane l, register e of MFMA tile (i, j) holds row 8 (e / 4) + 4 h + e % 4, column l % 32.
-  float *out = g.P + ((bt * g.T + r) * g.mp + pm0 + wm * 64) * g.np + pn0 + wn * 64 + r32;
+  const int64_t pstride = g.T * g.np;                     // one row of P: all T terms
+  float *out = g.P + ((bt * g.mp + pm0 + wm * 64) * g.T + r) * g.np + pn0 + wn * 64 + r32;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -662,7 +671,7 @@ __global__ __launch_bounds__(ex::kThreadsX, 1) void gemm_exact256x128_kernel(Spl
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int row = 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * g.np + 32 * j);
+        __builtin_nontemporal_store(acc[i][j][e], out + (int64_t)row * pstride + 32 * j);
       }
 }
 
@@ -688,7 +697,7 @@ __global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__
   for (int r = 0; r < kMaxRank; ++r) {
     if (r < pb.T) {
       // P_r is dead after this read: nontemporal, so it does not displace C in the caches
-      const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(P + ((bt * pb.T + r) * pb.mp + p) * pb.np + 4 * q4));
+      const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(P + ((bt * pb.mp + p) * pb.T + r) * pb.np + 4 * q4));
       const float4 v = make_float4(x.x, x.y, x.z, x.w);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -729,8 +738,7 @@ __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__
   const int64_t bt = blockIdx.y;
   if (pos >= pb.mp * n4) return;
   const int64_t p = pos / n4, q4 = pos - p * n4;
-  const int64_t plane = pb.mp * pb.np;
-  const float *src = P + (bt * pb.T * pb.mp + p) * pb.np + 4 * q4;
+  const float *src = P + (bt * pb.mp + p) * pb.T * pb.np + 4 * q4;   // term r at src + r n'
   float4 acc[16];
 #pragma unroll
   for (int b = 0; b < 16; ++b) acc[b] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -742,7 +750,7 @@ __global__ __launch_bounds__(256) void combine2_kernel(const float *__restrict__
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int r = min(r0 + j, T - 1);
-      x[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(src + r * plane));
+      x[j] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(src + r * pb.np));
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -785,8 +793,7 @@ __global__ __launch_bounds__(256) void combine64_kernel(const float *__restrict_
   const int64_t bt = blockIdx.y;
   if (pos >= pb.mp * pb.np) return;
   const int64_t p = pos / pb.np, q = pos - p * pb.np;
-  const int64_t plane = pb.mp * pb.np;
-  const float *src = P + bt * pb.T * plane + pos;
+  const float *src = P + (bt * pb.mp + p) * pb.T * pb.np + q;       // term r at src + r n'
   float acc[64];
 #pragma unroll
   for (int b = 0; b < 64; ++b) acc[b] = 0.0f;
@@ -796,7 +803,7 @@ __global__ __launch_bounds__(256) void combine64_kernel(const float *__restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int r = min(r0 + j, T - 1);
-      x[j] = __builtin_nontemporal_load(src + r * plane);
+      x[j] = __builtin_nontemporal_load(src + r * pb.np);
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
