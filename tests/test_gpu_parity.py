@@ -454,6 +454,16 @@ def test_dq_fused_path(case):
     print(case, r, flush=True)
 
 
+def test_dq_fused_uneven_item_ranges():
+    """273 items (products of 256^3, one 128 x 128 tile each) on the
+    persistent exact-dot kernel: more items than CUs, split over the eight
+    XCDs in ranges of 34 and 35, so some workgroups take two items and some
+    one; every eighth product checked against the oracle."""
+    r = check_case("tstar", "student_t3", 273, 256, 256, 256, 1, 32, 1, seed=43, cfg=12, exact=True,
+                   check_every=8, layout=FMM_LAYOUT_TILE128x128)
+    print(r, flush=True)
+
+
 def test_block16_takes_the_fused_path():
     """E8M0 scales at block 16 without the exact-dot flag (block 16 always
     runs exact-dot) take the fused 128 x 128 path below k' = 1024."""
