@@ -693,12 +693,19 @@ __global__ __launch_bounds__(256) void combine1_kernel(const float *__restrict__
   float4 acc[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) acc[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  // every term's load is issued before the first multiply-add (past the last
+  // term the index is clamped and the load unused); P_r is dead after this
+  // read: nontemporal, so it does not displace C in the caches
+  const int T = (int)pb.T;
+  const float *src = P + (bt * pb.mp + p) * pb.T * pb.np + 4 * q4;   // term r at src + r n'
+  f4v xs[kMaxRank];
+#pragma unroll
+  for (int r = 0; r < kMaxRank; ++r)
+    xs[r] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(src + min(r, T - 1) * pb.np));
 #pragma unroll
   for (int r = 0; r < kMaxRank; ++r) {
-    if (r < pb.T) {
-      // P_r is dead after this read: nontemporal, so it does not displace C in the caches
-      const f4v x = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(P + ((bt * pb.mp + p) * pb.T + r) * pb.np + 4 * q4));
-      const float4 v = make_float4(x.x, x.y, x.z, x.w);
+    if (r < T) {
+      const float4 v = make_float4(xs[r].x, xs[r].y, xs[r].z, xs[r].w);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float wq = wr[r][q];
