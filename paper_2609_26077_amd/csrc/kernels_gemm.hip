@@ -621,7 +621,9 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int BS>
+// VEC: C (depth 1) is 16-byte aligned, so its rows take 16-byte stores (the
+// partials of depth >= 2 sit in the workspace and always do).
+template <int BS, bool VEC>
 __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int tiles_m, int nitems) {
   // scale record per row and step: 4 bytes (blocks 32, 128) or 8 (block 16)
   constexpr int REC = BS == 16 ? 8 : 4;
@@ -818,9 +820,16 @@ __global__ __launch_bounds__(kDqThreads, 1) void gemm_dq8_kernel(GemmArgs g, int
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
-          float4 v = make_float4(quad[q][i][4 * a], quad[q][i][4 * a + 1], quad[q][i][4 * a + 2],
-                                 quad[q][i][4 * a + 3]);
-          *reinterpret_cast<float4 *>(base + 32 * i * ld + 8 * a) = v;
+          float *dst = base + 32 * i * ld + 8 * a;
+          if (VEC || g.depth != 1) {
+            *reinterpret_cast<float4 *>(dst) = make_float4(quad[q][i][4 * a], quad[q][i][4 * a + 1],
+                                                           quad[q][i][4 * a + 2], quad[q][i][4 * a + 3]);
+          } else {
+            dst[0] = quad[q][i][4 * a];
+            dst[1] = quad[q][i][4 * a + 1];
+            dst[2] = quad[q][i][4 * a + 2];
+            dst[3] = quad[q][i][4 * a + 3];
+          }
         }
     }
   };
@@ -1155,12 +1164,17 @@ int launch_products(const Problem &pb, const DeviceTables &tab, const uint8_t *w
       ncu = 256;
     if (items > INT32_MAX) return hipErrorInvalidValue;
     const dim3 pgrid((unsigned)(items < ncu ? items : ncu));
-    if (pb.block == 16)
-      hipLaunchKernelGGL(gemm_dq8_kernel<16>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
-    else if (pb.block == 32)
-      hipLaunchKernelGGL(gemm_dq8_kernel<32>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
-    else
-      hipLaunchKernelGGL(gemm_dq8_kernel<128>, pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items);
+    const bool vec = pb.depth != 1 || (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+#define FMM_DQ8(BSV, VECV) \
+  hipLaunchKernelGGL((gemm_dq8_kernel<BSV, VECV>), pgrid, dim3(kDqThreads), 0, st, g, (int)tiles_m, (int)items)
+    if (pb.block == 16) {
+      if (vec) FMM_DQ8(16, true); else FMM_DQ8(16, false);
+    } else if (pb.block == 32) {
+      if (vec) FMM_DQ8(32, true); else FMM_DQ8(32, false);
+    } else {
+      if (vec) FMM_DQ8(128, true); else FMM_DQ8(128, false);
+    }
+#undef FMM_DQ8
   } else if (aligned && pb.block == 32)
     hipLaunchKernelGGL(gemm_mx_fast_kernel<32>, grid, dim3(kThreads), 0, st, g, (int)tiles_m);
   else if (aligned)

@@ -351,6 +351,22 @@ def test_large_tile_split_path_unaligned_output():
     assert torch.equal(C1, C2)
 
 
+def test_dq_fused_path_unaligned_output():
+    """C at an address that is 4 but not 16 bytes aligned: the exact-dot fused
+    kernel stores C by scalars there; the result equals the aligned one."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    A, B = gen.operands("student_t3", 2, 512, 512, 256, seed=15)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f = FMM("strassen", 2, 512, 512, 256, 1, 32, "pow2_ceil", exact_dot=True)
+    C1 = f.matmul(dA, dB).clone()
+    buf = torch.full((1 + 2 * 512 * 256,), float("nan"), device="cuda:0")
+    C2 = buf[1:].view(2, 512, 256)
+    assert C2.data_ptr() % 16 == 4
+    f.matmul(dA, dB, C2)
+    assert torch.equal(C1, C2)
+
+
 @pytest.mark.parametrize("shape,depth,flags", [((1, 512, 256, 512), 1, 8),    # large-tile plan
                                                ((1, 1024, 512, 1024), 2, 8),  # large tiles, depth 2
                                                ((1, 256, 256, 384), 1, 0),    # combine fused into the GEMM
