@@ -486,3 +486,39 @@ def test_block16_takes_the_fused_path():
     r = check_case("winograd", "student_t3", 8, 256, 512, 256, 1, 16, 1, seed=42, cfg=12,
                    layout=FMM_LAYOUT_TILE128x128)
     print(r, flush=True)
+
+
+
+_PATHS = [
+    (1, (512, 512, 512), 0, False),                       # fp8 fused 128 x 128
+    (1, (512, 512, 512), FMM_FLAG_LARGE_TILE, False),     # fp8 large tiles + W-combine pass
+    (1, (512, 512, 512), 0, True),                        # exact-dot fused (eight waves)
+    (1, (512, 512, 512), FMM_FLAG_LARGE_TILE, True),      # exact-dot large tiles
+    (2, (1024, 512, 1024), 0, False),                     # depth 2, fused + outer combine
+    (2, (1024, 512, 1024), FMM_FLAG_LARGE_TILE, True),    # depth 2, exact-dot large tiles, 16-block combine
+    (3, (1024, 1024, 1024), 0, True),                     # depth 3, exact-dot fused + outer combine
+]
+
+
+@pytest.mark.parametrize("name,depth,shape,flags,exact",
+                         [(n,) + p for n in ("cubic8", "strassen", "winograd") for p in _PATHS
+                          if not (n == "winograd" and p[0] == 3)])
+def test_sign_operands_exact_222(name, depth, shape, flags, exact):
+    """+-1 / 0 operands on realizations with coefficients in {0, +-1}: every
+    encoded combination is an integer with at most 4 significant bits (|x| <=
+    1 for cubic, <= 2^depth for Strassen, <= 16 for Winograd up to depth 2;
+    Winograd's reach 64 at depth 3, which e4m3 cannot hold), so it is exact
+    in e4m3 after its power-of-two scale; the products are integers of at
+    most 256, which the fp8 matrix cores' group alignment keeps (13 bits
+    below a group's largest), and every sum is an integer below 2^24, so C
+    equals A B exactly on every path and depth."""
+    import torch
+    from paper_2609_26077_amd.runner import FMM
+    M, K, N = shape
+    rng = np.random.default_rng(7 + depth)
+    A = rng.integers(-1, 2, size=(1, M, K)).astype(np.float32)
+    B = rng.integers(-1, 2, size=(1, K, N)).astype(np.float32)
+    f = FMM(name, 1, M, K, N, depth, 32, "pow2_ceil", exact_dot=exact, flags=flags)
+    C = f.matmul(torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy()[0].astype(np.float64), A[0].astype(np.float64) @ B[0].astype(np.float64))
