@@ -522,3 +522,46 @@ def test_sign_operands_exact_222(name, depth, shape, flags, exact):
     C = f.matmul(torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
     torch.cuda.synchronize()
     assert np.array_equal(C.cpu().numpy()[0].astype(np.float64), A[0].astype(np.float64) @ B[0].astype(np.float64))
+
+
+
+@pytest.mark.parametrize("depth,rule,flags,exact", [
+    (1, "pow2_ceil", 0, False),                    # fp8 fused 128 x 128
+    (1, "pow2_ceil", FMM_FLAG_LARGE_TILE, False),  # fp8 large tiles
+    (1, "pow2_ceil", 0, True),                     # exact-dot fused
+    (1, "fp32_amax", FMM_FLAG_LARGE_TILE, True),   # fp32 scales, exact-dot large tiles
+    (2, "pow2_ocp", 0, False),                     # depth 2, OCP rule, fused + outer combine
+])
+def test_power_of_two_gauge_bit_identity(depth, rule, flags, exact):
+    """A power-of-two rescaling of each term that keeps the product
+    (u_r 2^a_r, v_r 2^b_r, w_r 2^(-a_r - b_r)) moves every encoded
+    combination by an exact power of two: the codes stay identical, each
+    block's scale moves by 2^a_r (A side) or 2^b_r (B side), and C is
+    identical to the last bit."""
+    import torch
+    from paper_2609_26077_amd import fmm_realization_create
+    from paper_2609_26077_amd.runner import FMM
+    U, V, W = (np.array(x, dtype=np.float64) for x in R.builtin_f64("tstar"))
+    a = np.array([1, -2, 3, 0, -1, 2, -3])
+    b = np.array([-1, 1, 2, -2, 0, 3, 1])
+    D2 = fmm_realization_create(U * 2.0 ** a[:, None], V * 2.0 ** b[:, None], W * 2.0 ** (-a - b)[:, None])
+    M = K = N = 512 * depth
+    A, B = gen.operands("gaussian", 1, M, K, N, seed=44)
+    dA, dB = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    f1 = FMM("tstar", 1, M, K, N, depth, 32, rule, exact_dot=exact, flags=flags)
+    f2 = FMM(D2, 1, M, K, N, depth, 32, rule, exact_dot=exact, flags=flags)
+    C1, C2 = f1.matmul(dA, dB), f2.matmul(dA, dB)
+    torch.cuda.synchronize()
+    assert torch.equal(C1, C2)
+    o1, o2 = f1.operands(), f2.operands()
+    # the flattened term (r_1 .. r_l) carries 2^(a_r1 + .. + a_rl)
+    T = 7 ** depth
+    idx = np.array(np.unravel_index(np.arange(T), (7,) * depth))
+    for side, (codes, scales), shift in ((0, (0, 1), a), (1, (2, 3), b)):
+        assert torch.equal(o1[codes], o2[codes]), side
+        sh = torch.from_numpy(shift[idx].sum(axis=0)).cuda()[None, :, None, None]
+        s1, s2 = o1[scales], o2[scales]
+        if rule == "fp32_amax":
+            assert torch.equal(torch.ldexp(s1, sh.to(torch.int32).expand_as(s1)), s2), side
+        else:
+            assert torch.equal(s1.to(torch.int32) + sh.to(torch.int32), s2.to(torch.int32)), side
