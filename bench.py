@@ -21,6 +21,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import subprocess
@@ -99,10 +100,26 @@ def source_hash(names=None):
     return h.hexdigest()
 
 
+def kernel_source_hash():
+    """sha256 over the device code a counter summary measures: the HIP
+    sources and headers under csrc/, and the public header with its comments
+    removed (host-side sources and comment edits leave the kernels as they
+    are; a plan change that runs other kernels shows as other kernel names)."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_26077_amd", "csrc")
+    for name in sorted(n for n in os.listdir(csrc) if n.endswith((".hip", ".h"))):
+        with open(os.path.join(csrc, name), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "fmm8.h")) as fh:
+        text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+    h.update(re.sub(r"\s+", " ", text).encode())
+    return h.hexdigest()
+
+
 def recorded_counters(workload_key):
     """Per-launch HBM bytes (FETCH_SIZE, WRITE_SIZE scaled to bytes) of each
     kernel of the step from the committed counter summary of this workload,
-    if it was taken on the sources as they are now; otherwise None."""
+    if it was taken on the device code as it is now; otherwise None."""
     path = os.path.join(ROOT, "profiles", f"step_counters_{workload_key}.md")
     if not os.path.exists(path):
         return None
@@ -118,7 +135,7 @@ def recorded_counters(workload_key):
                     rows[c[0].strip("`")] = {"role": c[1], "read": float(c[2]) * 1e6, "written": float(c[3]) * 1e6}
                 except ValueError:
                     pass
-    if fields.get("source sha256") != source_hash() or not rows:
+    if fields.get("kernel source sha256") != kernel_source_hash() or not rows:
         return None
     return rows
 

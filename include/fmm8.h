@@ -334,7 +334,8 @@ void fmm_plan_destroy(fmm_plan *p);
 int fmm_reference_f64(int64_t batch, int64_t M, int64_t K, int64_t N, const float *dA,
                       const float *dB, double *dCref, void *stream);
 
-/* Device scratch the reduction below needs. */
+/* Device scratch the reduction below needs (bytes; the scratch passed must
+ * hold at least that many and be 8-byte aligned, else FMM_ERR_WORKSPACE). */
 int fmm_error_stats_scratch_size(int64_t batch, int64_t M, int64_t N, size_t *bytes);
 
 /* Per product b: dOut[2b] = sum (C - Cref)^2, dOut[2b+1] = sum Cref^2, binary64,

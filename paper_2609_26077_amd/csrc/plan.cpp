@@ -367,7 +367,9 @@ int fmm_error_stats(int64_t batch, int64_t M, int64_t N, const float *dC, const 
   if (batch < 0 || M < 0 || N < 0 || batch > 65535) return FMM_ERR_ARG;
   if (batch == 0) return FMM_OK;
   if (!dOut || (M * N > 0 && (!dC || !dCref))) return FMM_ERR_ARG;
-  if (!dScratch || scratch_bytes < fmm::error_stats_scratch_bytes(batch, M, N)) return FMM_ERR_WORKSPACE;
+  if (!dScratch || scratch_bytes < fmm::error_stats_scratch_bytes(batch, M, N) ||
+      reinterpret_cast<uintptr_t>(dScratch) % 8)
+    return FMM_ERR_WORKSPACE;
   return hip_status(fmm::launch_error_stats(batch, M, N, dC, dCref, dOut, dScratch, stream));
 }
 

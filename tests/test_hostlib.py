@@ -256,3 +256,21 @@ def test_noalloc_error_stats_rejects_before_any_device_call(fm):
     assert fm._lib.fmm_error_stats_noalloc(-1, 4, 4, None, None, None, None) == fm.FMM_ERR_ARG
     assert fm._lib.fmm_error_stats_noalloc(0, 4, 4, None, None, None, None) == fm.FMM_OK
     assert fm._lib.fmm_error_stats_noalloc(2, 4, 4, None, None, None, None) == fm.FMM_ERR_ARG
+
+
+def test_error_stats_scratch_checks_before_any_device_call(fm):
+    """fmm_error_stats refuses a scratch that is too small or not 8-byte
+    aligned, and bad sizes, before any device call (the pointers below are
+    never dereferenced; this runs on a CPU)."""
+    lib = fm._lib
+    need = ctypes.c_size_t(0)
+    assert lib.fmm_error_stats_scratch_size(3, 64, 64, ctypes.byref(need)) == fm.FMM_OK
+    assert need.value > 0
+    fake = 1 << 40                                   # non-null, 256-byte aligned
+    args = (3, 64, 64, fake, fake, fake)
+    assert lib.fmm_error_stats(*args, fake, need.value - 1, None) == fm.FMM_ERR_WORKSPACE
+    assert lib.fmm_error_stats(*args, fake + 4, need.value, None) == fm.FMM_ERR_WORKSPACE
+    assert lib.fmm_error_stats(*args, None, need.value, None) == fm.FMM_ERR_WORKSPACE
+    assert lib.fmm_error_stats(-1, 64, 64, fake, fake, fake, fake, need.value, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_error_stats(3, 64, 64, fake, fake, None, fake, need.value, None) == fm.FMM_ERR_ARG
+    assert lib.fmm_error_stats(0, 64, 64, None, None, None, None, 0, None) == fm.FMM_OK
