@@ -352,8 +352,8 @@ def test_large_tile_split_path_unaligned_output():
 
 
 def test_dq_fused_path_unaligned_output():
-    """C at an address that is 4 but not 16 bytes aligned: the exact-dot fused
-    kernel stores C by scalars there; the result equals the aligned one."""
+    """C at an address that is 4 but not 16 bytes aligned (the ABI asks for 4):
+    the exact-dot fused kernel's scalar stores give the aligned result."""
     import torch
     from paper_2609_26077_amd.runner import FMM
     A, B = gen.operands("student_t3", 2, 512, 512, 256, seed=15)
