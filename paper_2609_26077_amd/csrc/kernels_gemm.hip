@@ -407,9 +407,13 @@ __device__ __forceinline__ v8bf dequant8(const v8i &f, int d, float s) {
   return r;
 }
 
-// 2^(byte - 127) of byte i of a scale record (byte >= 1 for every rule's scale)
+// A float whose exponent field is byte i of a scale record, as the scale
+// operand of v_cvt_scalef32_pk_bf16_fp8, which reads the exponent field alone
+// (its sign and mantissa bits, here parts of the neighbouring bytes, leave
+// the result unchanged: every code at every exponent -48 .. 120 measured), so
+// one shift places the byte
 __device__ __forceinline__ float e8m0_at(int w, int i) {
-  return __uint_as_float((((uint32_t)w >> (8 * i)) & 0xffu) << 23);
+  return __uint_as_float(i == 3 ? (uint32_t)w >> 1 : (uint32_t)w << (23 - 8 * i));
 }
 
 // The fp8 matrix cores with the E8M0 scales applied by the scaled MFMA.

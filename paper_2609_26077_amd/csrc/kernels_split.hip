@@ -291,9 +291,11 @@ __device__ __forceinline__ v8bfq dequant8(uint32_t lo, uint32_t hi, float s) {
   return r;
 }
 
-// 2^(byte - 127) for E8M0 byte i of word w (byte >= 1 for every rule's scale)
+// A float whose exponent field is E8M0 byte i of word w, as the scale operand
+// of v_cvt_scalef32_pk_bf16_fp8, which reads the exponent field alone (the
+// neighbouring bytes in its sign and mantissa bits do not change the result)
 __device__ __forceinline__ float e8m0_byte(uint32_t w, int i) {
-  return __uint_as_float(((w >> (8 * i)) & 0xffu) << 23);
+  return __uint_as_float(i == 3 ? w >> 1 : w << (23 - 8 * i));
 }
 
 template <int BS>
