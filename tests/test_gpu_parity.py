@@ -565,3 +565,13 @@ def test_power_of_two_gauge_bit_identity(depth, rule, flags, exact):
             assert torch.equal(torch.ldexp(s1, sh.to(torch.int32).expand_as(s1)), s2), side
         else:
             assert torch.equal(s1.to(torch.int32) + sh.to(torch.int32), s2.to(torch.int32)), side
+
+
+@pytest.mark.parametrize("exact", [False, True])
+def test_maximum_batch(exact):
+    """The largest batch a plan takes (65535, the launch grid's batch axis) of
+    2 x 64 x 2 products: every launch spans the whole axis; products at both
+    ends and in between against the oracle (a 2 x 2 output is outside the
+    fp8 path's 1e-5 bar, which its exact-dot twin asserts)."""
+    check_case("strassen", "gaussian", 65535, 2, 64, 2, 1, 32, 1, check_every=16383,
+               exact=exact, ns=exact)
