@@ -175,7 +175,7 @@ def oracle_rows(M, table, depth, bs, rule, side, rows):
 
 
 def sampled_parity(spec, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nrows, rng,
-                   exact=False, b_rows=1, b_bf16=False):
+                   exact=False, b_rows=1, b_bf16=False, ends=False):
     """The oracle on sampled rows of a full-size GPU run (quantization runs
     along the contracted axis, so a row's codes depend on that row alone):
     for each batch element in ``bsel``, ``nrows`` random rows of A's and of
@@ -186,7 +186,8 @@ def sampled_parity(spec, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nr
     codes_scales_identical, within_dot_bound, ref_ok, max_rel_fro (over the
     sampled entries, against |C_oracle|_F estimated by the fp64 reference's
     norm), rel_mse_gpu / rel_mse_oracle over the sampled entries, and
-    per-element details of the first failure."""
+    per-element details of the first failure.  ends: the first and last row
+    of each side are sampled as well (the largest offsets)."""
     D = oracle_realization(spec)
     U, V, W = R.tables_f32(D, depth)
     T = U.shape[0]
@@ -204,6 +205,9 @@ def sampled_parity(spec, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nr
     for b in bsel:
         prow = np.sort(rng.choice(mp, size=min(nrows, mp), replace=False))
         qrow = np.sort(rng.choice(np_, size=min(nrows, np_), replace=False))
+        if ends:
+            prow = np.union1d(prow, [0, mp - 1])
+            qrow = np.union1d(qrow, [0, np_ - 1])
         xc, xs, xd = oracle_rows(A[b], U, depth, bs, rule, "A", prow)
         yc, ys, yd = oracle_rows(B[b], V, depth, bs, rule, "B", qrow)
         gs_a = asc[b][:, prow, :].cpu().numpy()

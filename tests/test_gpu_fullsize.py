@@ -41,7 +41,7 @@ def log(msg):
 
 
 def check_sampled(name, family, batch, M, K, N, depth, bs, rule_name, seed, cfg, bsel, nrows=12,
-                  trial=0, exact=False, ns=True):
+                  trial=0, exact=False, ns=True, ends=False):
     """Full-size GPU run; oracle on sampled rows of batch elements `bsel`.
     ns: assert the 1e-5 |C|_F bar (the fp8 path's group truncation can exceed
     it on heavy tails and four-decade row scales; those run an exact-dot twin)."""
@@ -63,7 +63,7 @@ def check_sampled(name, family, batch, M, K, N, depth, bs, rule_name, seed, cfg,
     assert np.allclose(ref2, (Cref * Cref).sum(dim=(1, 2)).cpu().numpy(), rtol=1e-10)
     del d
     r = sampled_parity(name, A, B, f, C, Cref, err2, ref2, depth, bs, rule, bsel, nrows,
-                       np.random.default_rng(1234 + seed), exact=exact)
+                       np.random.default_rng(1234 + seed), exact=exact, ends=ends)
     log(f"sampled: {r}")
     assert r["codes_scales_identical"], "codes or scales differ"
     assert r["within_dot_bound"], "elements beyond the dot-product bound"
@@ -117,3 +117,15 @@ def test_headline_heavy_tailed_sampled(exact):
     r = check_sampled("tstar", "student_t3", 1, 8192, 8192, 8192, 1, 32, "pow2_ceil", seed=0, cfg=0,
                       bsel=[0], nrows=12, exact=exact, ns=False)
     log(f"8192^3 student_t3 exact={exact}: max_rel_fro {r['max_rel_fro']:.3e}")
+
+
+@pytest.mark.parametrize("exact", [False, True])
+def test_beyond_32bit_offsets_sampled(exact):
+    """32768 x 16384 x 49152, depth 1, Strassen 1969, N(0,1) (the large-tile
+    path): A is 2 GiB and C 6 GiB, and the fp32 sub-products hold 2.8e9
+    elements, so every byte offset and the sub-products' element indices pass
+    2^31; sampled rows of A and B, the last ones among them, against the
+    oracle."""
+    r = check_sampled("strassen", "gaussian", 1, 32768, 16384, 49152, 1, 32, "pow2_ceil", seed=0, cfg=6,
+                      bsel=[0], nrows=8, exact=exact, ends=True)
+    log(f"32768x16384x49152 exact={exact}: max_rel_fro {r['max_rel_fro']:.3e}")
