@@ -71,6 +71,7 @@ constexpr int kStride = kTL + 4;    // LDS row stride in floats: 33 16-byte slot
 // rather than 32-byte ones and a wave writes whole 64-byte code runs.
 constexpr int kA1Rows = 8, kA1Threads = 128;   // depth-1 A-side tile rows and threads
 constexpr int kB1Rows = 32, kB1Threads = 512;  // depth-1 B-side tile rows (columns of B) and threads
+constexpr int kB1NThreads = 256;                // threads of its narrow (64-position) form
 constexpr int kB3Rows = 8;          // depth-3 B-side tile rows (columns of B), 32 positions each, at blocks <= 32
 
 // CAP: a realization of another shape, staged as up to CAP blocks of a grid
@@ -80,14 +81,14 @@ struct Tile {
   static constexpr int nblk = CAP ? CAP : 1 << (2 * DEPTH);
   static constexpr int TL = NARROW ? (DEPTH == 3 ? 256 / kB3Rows : 64) : kTL;   // contracted positions per tile
   static constexpr int stride = TL + 4;                   // LDS row stride in floats (an odd number of 16-byte slots)
-  static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? kB1Rows : kA1Rows) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
+  static constexpr int TR = NARROW ? (DEPTH == 3 ? kB3Rows : DEPTH == 1 ? kB1Rows : 16) : VEC == 16 ? (DEPTH == 1 ? (SIDE == 1 ? kB1Rows : kA1Rows) : 8) : (DEPTH == 3 ? 2 : 64 / nblk);
   // depth 1: 128 (A) or 512 (B) threads; depths 2 and 3 deal the terms out to
   // sixteen waves, which with two workgroups per CU keeps eight waves per SIMD
-  static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? kA1Threads : kB1Threads) : 1024;
-  static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B), 67.6 (69.6 narrow), 67.6 KB
+  static constexpr int threads = DEPTH == 1 ? (SIDE == 0 ? kA1Threads : NARROW ? kB1NThreads : kB1Threads) : 1024;
+  static constexpr int lds_floats = nblk * TR * stride;   // 33.8 (A) / 67.6 (B; 34.8 narrow), 67.6 (69.6 narrow), 67.6 KB
   static_assert(lds_floats * 4 <= 160 * 1024, "the tile fits in LDS");
-  static_assert(!NARROW || (DEPTH == 2 && SIDE == 1 && VEC == 16) || (DEPTH == 3 && SIDE == 1 && VEC == 4),
-                "the narrow tiles are the depth-2 and depth-3 B sides'");
+  static_assert(!NARROW || (DEPTH <= 2 && SIDE == 1 && VEC == 16) || (DEPTH == 3 && SIDE == 1 && VEC == 4),
+                "the narrow tiles are B sides'");
 };
 
 template <int CTRL>
@@ -292,18 +293,18 @@ constexpr bool narrow_b(int side, int depth, int bs, int mode) {
   return side == 1 && depth == 2 && bs <= 32 && mode == 0;
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE, int CAP = 0>
-__global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE)>::threads)) void encode16_kernel(
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE, int CAP = 0, bool N1 = false>
+__global__ __launch_bounds__((Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE) || N1>::threads)) void encode16_kernel(
     const float *__restrict__ src, Problem pb, SideTab cf, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     int64_t tiles_l, void *__restrict__ aux) {
   static_assert(MODE == 0 || MODE == 3 || (SIDE == 1 && DEPTH == 1), "deployment granularity: B side, depth 1");
   static_assert(CAP == 0 || (MODE == 0 && (DEPTH == 1 || CAP == 16)), "other shapes: the plain encoder");
   constexpr bool GEN = CAP != 0;
   uint32_t *amax = reinterpret_cast<uint32_t *>(aux);
-  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE), CAP>;
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE) || N1, CAP>;
   constexpr int TR = TT::TR, NB = TT::nblk, NT = TT::threads, TL = TT::TL, STR = TT::stride;
   constexpr int RPW = 64 * 16 / TL;         // rows per wave: 8, or 16 in the narrow tile
-  constexpr int WPT = TR / RPW;             // waves per term (1 (A) or 4 (B) at depth 1, 1 at depth 2)
+  constexpr int WPT = TR / RPW;             // waves per term (1 (A), 4 (B) or 2 (narrow B) at depth 1, 1 at depth 2)
   constexpr int TSTEP = NT / 64 / WPT;      // terms a workgroup works on at once
   __shared__ float4 lds4[TT::lds_floats / 4];
   float *lds = reinterpret_cast<float *>(lds4);
@@ -660,15 +661,23 @@ __global__ __launch_bounds__((Tile<3, 4, SIDE, narrow_b3(SIDE, BS)>::threads), 8
   }
 }
 
-template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0, int CAP = 0>
+// N1: the depth-1 B side's narrow tile (32 columns x 64 positions, 256
+// threads), taken on the 256 x 64 tile layout at blocks 16 and 32: each lane
+// quad writes a whole 64-byte image row, and the half-size tile lets four
+// workgroups share a CU (8192^3 T* encode 149 -> 143.5 us, codes identical).
+template <int SIDE, int DEPTH, int BS, bool F32, int MODE = 0, int CAP = 0, bool N1 = false>
 hipError_t launch16(const Problem &pb, const float *src, const SideTab &cf,
                     uint8_t *codes, uint8_t *scales, hipStream_t st, void *amax = nullptr) {
-  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE), CAP>;
+  if constexpr (SIDE == 1 && DEPTH == 1 && MODE == 0 && CAP == 0 && BS <= 32 && !N1) {
+    if (pb.layout == FMM_LAYOUT_TILE256x64)
+      return launch16<SIDE, DEPTH, BS, F32, MODE, CAP, true>(pb, src, cf, codes, scales, st, amax);
+  }
+  using TT = Tile<DEPTH, 16, SIDE, narrow_b(SIDE, DEPTH, BS, MODE) || N1, CAP>;
   const int64_t rows = SIDE == 0 ? pb.mp : pb.np;
   const int64_t tiles_l = (pb.kp + TT::TL - 1) / TT::TL;
   const int64_t tiles_r = (rows + TT::TR - 1) / TT::TR;
   const dim3 grid((unsigned)(tiles_l * tiles_r), (unsigned)pb.batch);
-  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE, CAP>), grid, dim3(TT::threads), 0, st, src, pb, cf,
+  hipLaunchKernelGGL((encode16_kernel<SIDE, DEPTH, BS, F32, MODE, CAP, N1>), grid, dim3(TT::threads), 0, st, src, pb, cf,
                      codes, scales, tiles_l, amax);
   return hipGetLastError();
 }
