@@ -409,8 +409,8 @@ def main():
         calibrate_copy()
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: the path has no cross-GPU step and this build runs on a "
-              f"single MI355X (--gpus {args.gpus} is not supported)", file=sys.stderr)
+        print(f"bench.py measures one GPU: the path has no cross-GPU step, and the benchmark times "
+              f"a single MI355X (--gpus {args.gpus} is not supported)", file=sys.stderr)
         sys.exit(2)
 
     import torch

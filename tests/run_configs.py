@@ -2,7 +2,7 @@
 (configuration, arm, depth, block, trial), each with the oracle check made on
 it.  Test infrastructure (it calls the oracle): run on an MI355X as
 
-    python -m tests.run_configs --config C2 --out gpurun_out/records/C2.jsonl
+    python -m tests.run_configs --config C2 --out records/C2.jsonl
 
 Configurations (seeded synthetic operands, fmm_inputs streams
 SeedSequence([0, cfg, trial, operand]); the same operands for every arm of a
