@@ -357,9 +357,9 @@ def paper_context():
 def cpu_baseline(args):
     """The oracle, unchanged, timed on this host's cores on a bounded sample
     of the benchmark configurations: the 100 trials of the 256^3
-    configuration for the cubic and Strassen 1969 realizations, and one trial
-    of the headline workload.  BLAS threads are held to the cores this
-    process may run on."""
+    configuration for the cubic and Strassen 1969 realizations, one trial of
+    the 4096^3 configuration (T*) and one trial of the headline workload.
+    BLAS threads are held to the cores this process may run on."""
     from threadpoolctl import threadpool_limits
     from oracle import e4m3, fmm
     from oracle import realizations as R
@@ -380,6 +380,15 @@ def cpu_baseline(args):
             flop += 100 * 2.0 * 256 ** 3
             parts.append(f"100 x 256^3 {name} {dt:.2f} s")
         del A, B
+        A, B = gen.operands("gaussian", 1, 4096, 4096, 4096, seed=SEED, cfg=2, trial=0)
+        tabs = R.tables_f32(R.builtin_f64("tstar"), 1)
+        t0 = time.perf_counter()
+        fmm.fmm(A[0], B[0], tabs, 1, 32, rule, keep=False)
+        dt = time.perf_counter() - t0
+        t += dt
+        flop += 2.0 * 4096 ** 3
+        parts.append(f"1 x 4096^3 tstar {dt:.2f} s")
+        del A, B
         n = args.size
         A, B = gen.operands(args.family, 1, n, n, n, seed=SEED, cfg=0, trial=0)
         tabs = R.tables_f32(R.builtin_f64(args.realization), args.depth)
@@ -397,7 +406,8 @@ def cpu_baseline(args):
         pass
     return {"value": flop / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "sample": "the 100 trials of the 256^3 configuration (N(0,1), block 32, cubic8 and Strassen "
-                      f"1969) and one trial of the headline workload ({args.rule}, block {args.block}): "
+                      f"1969), one trial of the 4096^3 configuration (T*) and one trial of the headline "
+                      f"workload ({args.rule}, block {args.block}): "
                       "numpy fp32 encode + e4m3 codec, fp64 BLAS sub-products, W-combine; "
                       + "; ".join(parts),
             "seconds": t, "cpu_model": cpu}
