@@ -575,3 +575,35 @@ def test_maximum_batch(exact):
     fp8 path's 1e-5 bar, which its exact-dot twin asserts)."""
     check_case("strassen", "gaussian", 65535, 2, 64, 2, 1, 32, 1, check_every=16383,
                exact=exact, ns=exact)
+
+
+@pytest.mark.parametrize("shape,flags,layout", [((256, 256, 256), 0, FMM_LAYOUT_TILE128x128),
+                                                ((512, 128, 512), FMM_FLAG_LARGE_TILE, FMM_LAYOUT_TILE256x64)])
+@pytest.mark.parametrize("rule", [1, 2])
+def test_exact_dot_scale_range(shape, flags, layout, rule):
+    """Rows of A from 1e-11 to 1e34 and columns of B from 1e-8 to 1e1, so the
+    E8M0 scales of the blocks run from about 2^-44 to 2^107: the exact-dot
+    kernels (fused 128 x 128 and large tiles) fold every one of them into the
+    codes' conversion.  Codes and scales identical to the oracle's, and every
+    element of C within the dot-product bound, which scales with its own row
+    and column."""
+    from tests.gpu_helpers import abs_bound, compare_operands, run_gpu
+    from oracle import fmm
+    M, K, N = shape
+    A, B = gen.operands("gaussian", 1, M, K, N, seed=21)
+    ka = np.array([-11, -6, -2, 0, 3, 8, 14, 20, 26, 31, 34])
+    kb = np.array([-8, -4, 0, 1])
+    A[0] *= (10.0 ** ka[np.arange(M) % ka.size]).astype(np.float32)[:, None]
+    B[0] *= (10.0 ** kb[np.arange(N) % kb.size]).astype(np.float32)[None, :]
+    tabs = R.tables_f32(R.builtin_f64("tstar"), 1)
+    g = run_gpu("tstar", A, B, 1, 32, rule, exact=True, flags=flags)
+    assert g["layout"] == layout
+    o = fmm.fmm(A[0], B[0], tabs, 1, 32, rule)
+    compare_operands(g["ops"], o["a"], o["b"], 0, rule)
+    ex = [int(e) - 127 for e in np.unique(np.concatenate([o["a"]["scales"].ravel(), o["b"]["scales"].ravel()]))]
+    assert min(ex) <= -40 and max(ex) >= 100, (min(ex), max(ex))
+    Cg, Co = g["C"][0].astype(np.float64), o["C"]
+    assert np.isfinite(Cg).all()
+    S = abs_bound(o, tabs[2], 1, M, N)
+    bound = (2.0 ** -19 + (K // 2 + 7 + 8) * 2.0 ** -24) * S
+    assert (np.abs(Cg - Co) <= bound).all()
